@@ -1,0 +1,237 @@
+"""Benchmark of one GVA decode step on one MI355X.
+
+A step is the whole decode path of Algorithm 1 for one batch: append the
+step's new value rows and rotated positional key at position len-1, absorb
+and rotate the query inside the attention kernel, attend over every cached
+row in splits, and merge the splits.  Inputs are seeded synthetic tensors
+already resident in HBM before the timed region starts.
+
+Prints ONE JSON line.  ``value`` is whole-step throughput in GB/s of
+algorithmic bytes (every cached value / positional-key row read once, M and
+q read once, new rows read+written once, fp32 output written once) divided
+by the measured step time.
+
+  python bench.py [--steps K] [--warmup W] [--workload b32_t8k] [--splits S]
+                  [--unfused] [--no-cpu-baseline] [--copy-calibration MB]
+"""
+
+from __future__ import annotations
+
+import argparse
+import hashlib
+import json
+import math
+import os
+import sys
+import time
+
+import torch
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+import gva_inputs  # noqa: E402
+from paper_2609_13285_amd import gva, traffic  # noqa: E402
+
+METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s, B=32 T=8K bf16"
+HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD's published figure
+KERNEL_SRC = os.path.join(ROOT, "paper_2609_13285_amd", "csrc", "gva.hip")
+TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_b32_t8k.json")
+
+
+def kernel_sha() -> str:
+    with open(KERNEL_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()[:16]
+
+
+def measured_traffic(workload: str, splits: int):
+    """HBM bytes per decode launch from committed rocprofv3 counters, if they
+    were taken on the current kernel source with the same launch shape."""
+    try:
+        with open(TRAFFIC_FILE) as f:
+            rec = json.load(f)
+    except (OSError, ValueError):
+        return None
+    if rec.get("kernel_sha") != kernel_sha() or rec.get("workload") != workload \
+            or rec.get("num_splits") != splits:
+        return None
+    return rec.get("hbm_bytes_per_launch")
+
+
+def copy_calibration(mb: int, reps: int = 5):
+    """A plain device copy of known size, for scaling FETCH_SIZE/WRITE_SIZE."""
+    n = mb * (1 << 20) // 4
+    src = torch.ones(n, dtype=torch.float32, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(reps):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}))
+
+
+def cpu_baseline(w, inp, seq, pos, budget_s: float = 20.0):
+    """The fp64 oracle on the host cores, on a bounded sample of sequences."""
+    import oracle
+    threads = oracle.max_threads()
+    v = inp["v"].clone()
+    kr = inp["kr"].clone()
+    oracle.append(v, kr, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    order = list(range(w.batch))
+    done, t_used, nbytes = [], 0.0, 0
+    o_all = {}
+    while order and t_used < budget_s:
+        b = order.pop(0)
+        sl = slice(b, b + 1)
+        t0 = time.perf_counter()
+        o, _ = oracle.decode(inp["q"][sl], inp["m"], v[sl], kr[sl], inp["lens"][sl],
+                             rope_base=w.rope_base, n_threads=threads)
+        t_used += time.perf_counter() - t0
+        done.append(b)
+        o_all[b] = o[0]
+        nbytes += traffic.decode_bytes(inp["lens"][sl], 1, w.n_heads, w.n_groups, w.d_v,
+                                       w.d_c, w.d_r, 2 if w.dtype == "bf16" else 4)
+    rec = {"value": nbytes / t_used / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "seconds": round(t_used, 3),
+           "sample": f"fp64 oracle decode of {len(done)} of {w.batch} sequences "
+                     f"(all {w.n_heads} heads, full length) after the step's append"}
+    return rec, o_all
+
+
+def main():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--workload", default="b32_t8k", choices=sorted(gva_inputs.WORKLOADS))
+    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--unfused", action="store_true", help="run gva_absorb_query as its own kernel")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
+    args = ap.parse_args()
+
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(json.dumps({"error": "this build measures one GPU only; the decode path is "
+                          "single-GPU (see DESIGN.md for how it would shard)",
+                          "n_gpus": args.gpus}))
+        sys.exit(2)
+    if not torch.cuda.is_available():
+        print(json.dumps({"error": "no GPU visible"}))
+        sys.exit(1)
+    gva.lib()  # fail loudly if the HIP library is missing
+    if args.copy_calibration:
+        copy_calibration(args.copy_calibration)
+        return
+
+    w = gva_inputs.workload(args.workload)
+    inp = gva_inputs.make_inputs(w, args.seed)
+    d = gva.make_dims(w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, w.t_max, w.dtype,
+                      w.rope_base)
+    max_len = int(inp["lens"].max())
+    S = args.splits or gva.gva_pick_splits(d, max_len)
+    dev = {k: inp[k].cuda() for k in ("q", "m", "v", "kr", "lens", "v_new", "kr_new")}
+    seq = torch.arange(w.batch, dtype=torch.int32)
+    pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
+    seq_d, pos_d = seq.cuda(), pos.cuda()
+    bufs = gva.DecodeBuffers(d, S)
+    fused = not args.unfused
+    q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+    q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+    stream = torch.cuda.current_stream()
+
+    def step(ev_a=None, ev_b=None):
+        gva.gva_append_kv(d, dev["v"], dev["kr"], dev["v_new"], dev["kr_new"], seq_d, pos_d, stream)
+        if not fused:
+            gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
+        if ev_a is not None:
+            ev_a.record(stream)
+        if fused:
+            gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, bufs.o_part,
+                                     bufs.lse_part, q=dev["q"], m=dev["m"], stream=stream)
+        else:
+            gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, bufs.o_part,
+                                     bufs.lse_part, q_abs=q_abs,
+                                     q_rot=q_rot if w.d_r > 0 else None, stream=stream)
+        if ev_b is not None:
+            ev_b.record(stream)
+        gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+
+    # timed region 1: whole steps, no events inside
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    t_start.record(stream)
+    for _ in range(args.steps):
+        step()
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+
+    # timed region 2: the same steps with events around the attention kernel
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for a, b in evs:
+        step(a, b)
+    torch.cuda.synchronize()
+    kt = sorted(a.elapsed_time(b) for a, b in evs)
+    decode_ms = sum(kt) / len(kt)
+
+    elem = 2 if w.dtype == "bf16" else 4
+    lens = inp["lens"]
+    step_b = traffic.step_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
+                                appended_rows=w.batch)
+    dec_b = traffic.decode_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem)
+    value = step_b / (ms_per_step * 1e-3) / 1e9
+    achieved = dec_b / (decode_ms * 1e-3) / 1e9
+
+    out = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 5),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": w.dtype,
+        "data": "synthetic",
+        "config": {"workload": w.name, "batch": w.batch, "t_max": w.t_max,
+                   "n_heads": w.n_heads, "n_groups": w.n_groups, "d_v": w.d_v, "d_c": w.d_c,
+                   "d_r": w.d_r, "num_splits": S, "fused_absorb": fused,
+                   "total_cached_rows": int(lens.clamp(min=0).sum()), "parallelism": "none"},
+        "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
+        "tokens_per_s": round(w.batch / (ms_per_step * 1e-3), 1),
+        "tokens_heads_per_s": round(w.batch * w.n_heads / (ms_per_step * 1e-3), 1),
+        "roofline": {
+            "kernel": "decode_bf16_kernel" if w.dtype == "bf16" else "decode_f32_kernel",
+            "bound": "hbm",
+            "achieved": round(achieved, 2),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": measured_traffic(w.name, S),
+            "algorithmic_bytes_per_launch": dec_b,
+            "avg_launch_ms": round(decode_ms, 5),
+            "p10_p90_launch_ms": [round(kt[len(kt) // 10], 5), round(kt[(9 * len(kt)) // 10], 5)],
+        },
+        "cpu_baseline": None,
+    }
+
+    if not args.no_cpu_baseline:
+        o_gpu = bufs.o.cpu()
+        rec, o_ref = cpu_baseline(w, inp, seq, pos)
+        errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]
+        rec["max_abs_err_vs_gpu"] = max(errs) if errs else None
+        out["cpu_baseline"] = rec
+    print(json.dumps(out))
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,170 @@
+/*
+ * gva.h -- C ABI of libgva.so, the MI355X (gfx950) decode step of Grouped
+ * Value Attention with decoupled RoPE.
+ *
+ * One decode step (Algorithm 1 of the paper) is four calls:
+ *
+ *   gva_append_kv         write the new value rows and the rotated shared
+ *                         positional key into the caches (Algorithm 1, the
+ *                         append steps; eq. krope)
+ *   gva_absorb_query      q~_h = q^nope_h M_h^T and q^rope_h R_p^T
+ *                         (eq. absorb, Section 3.2; the query-rotation step)
+ *   gva_decode_attention  per split of the cached rows: scores
+ *                         q~ . V_g(h)[t] + q^rope . k^rope[t], scaled softmax
+ *                         and the weighted value sum, never forming a
+ *                         content key (Section 3.3; the scoring and output
+ *                         steps of Algorithm 1)
+ *   gva_combine           log-sum-exp merge of the split partials
+ *
+ * Conventions shared by every call
+ * --------------------------------
+ * - Every tensor argument is a DEVICE pointer to a dense, row-major array;
+ *   only `dims` is a host pointer.  The caller owns all memory.  The library
+ *   never allocates, frees or synchronises; each call enqueues its kernels
+ *   on `stream` (a hipStream_t; NULL is the null stream) and returns.
+ * - Storage dtype (`dims->dtype`) applies to q, M, the caches and the new
+ *   rows: GVA_DTYPE_BF16 (bfloat16) or GVA_DTYPE_F32.  Absorbed queries,
+ *   partials and outputs are always fp32.
+ * - Layouts (B batch, H query heads, G value groups, T = dims->t_max):
+ *     q        [B][H][d_c + d_r]   content slice first, then the positional
+ *                                  slice, unrotated
+ *     M        [H][d_v][d_c]       M_h maps a d_v-wide value to a d_c-wide
+ *                                  content key (K_h = V_g(h) M_h, eq. kvm)
+ *     v_cache  [B][G][T][d_v]      grouped value cache
+ *     kr_cache [B][T][d_r]         shared positional key cache, stored
+ *                                  already rotated
+ *     lens     [B] int32           cached rows per sequence; the query sits
+ *                                  at position lens[b]-1 (positions 0-based)
+ * - Head h reads value group g(h) = h / (H/G).
+ * - RoPE rotates interleaved pairs (2i, 2i+1) by the angle
+ *   p * rope_base^(-2i/d_r), formed in fp64, as the row-vector product
+ *   x R_p^T: (x0 cos a - x1 sin a, x0 sin a + x1 cos a).
+ * - Score scale: dims->scale, or 1/sqrt(d_c + d_r) when it is 0 (d_qk =
+ *   d_n + d_r, Section 3.3).
+ * - Device-resident indices are clamped, never trusted: lens[b] is read as
+ *   min(max(lens[b], 0), T); append rows whose seq/pos fall outside
+ *   [0,B) x [0,T) are skipped.
+ * - Errors: every call returns a gva_status.  All arguments are validated
+ *   on the host before anything is enqueued; a failed validation enqueues
+ *   nothing.  GVA_ERR_HIP reports a launch failure from the HIP runtime.
+ * - Calls are asynchronous; outputs must not alias inputs.  Results are
+ *   bitwise deterministic for a fixed num_splits.
+ */
+#ifndef GVA_H_
+#define GVA_H_
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum gva_status {
+  GVA_OK = 0,
+  GVA_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, bad dims or split count */
+  GVA_ERR_UNSUPPORTED = 2,  /* valid shape this build has no kernel for */
+  GVA_ERR_HIP = 3           /* the HIP runtime reported an error */
+} gva_status;
+
+typedef enum gva_dtype { GVA_DTYPE_F32 = 0, GVA_DTYPE_BF16 = 1 } gva_dtype;
+
+/* Problem shape; passed by host pointer to every call. */
+typedef struct gva_dims {
+  int32_t batch;      /* B >= 1 */
+  int32_t n_heads;    /* H >= 1, a multiple of n_groups */
+  int32_t n_groups;   /* G >= 1 */
+  int32_t d_v;        /* value width (the paper's d_h) */
+  int32_t d_c;        /* content query/key width (the paper's d_n) */
+  int32_t d_r;        /* shared positional width, even, >= 0 */
+  int32_t t_max;      /* cache capacity per sequence, >= 1 */
+  int32_t dtype;      /* gva_dtype */
+  double rope_base;   /* RoPE base (10000 in the paper's setting), > 0 */
+  double scale;       /* score scale; 0 selects 1/sqrt(d_c + d_r) */
+} gva_dims;
+
+/* Largest num_splits accepted by gva_decode_attention / gva_combine. */
+#define GVA_MAX_SPLITS 256
+
+/*
+ * gva_append_kv -- Algorithm 1, the cache-append steps, and eq. krope.
+ * For each r < n_rows, with b = seq[r], p = pos[r]:
+ *   v_cache[b][g][p][:] = v_new[r][g][:]              for every g < G
+ *   kr_cache[b][p][:]   = RoPE(kr_new[r][:], p)       rotated in fp64,
+ *                                                     rounded once (RNE)
+ * v_new [n_rows][G][d_v] and kr_new [n_rows][d_r] are device arrays in the
+ * storage dtype; kr_new is the unrotated x W_r.  seq/pos are device int32
+ * [n_rows].  Rows with b or p out of range are skipped.  Writing the same
+ * (b, p) twice with the same data is idempotent; two rows naming the same
+ * (b, p) in one call race.  n_rows == 0 is a no-op.
+ * Pointers: v_cache, v_new 16-byte aligned; kr_cache, kr_new 4-byte
+ * aligned (when d_r > 0).
+ */
+int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache,
+                  const void* v_new, const void* kr_new,
+                  const int32_t* seq, const int32_t* pos, int32_t n_rows,
+                  void* stream);
+
+/*
+ * gva_absorb_query -- eq. absorb (Section 3.2) and the query-rotation step
+ * of Algorithm 1, for every (b, h):
+ *   q_abs[b][h][i] = sum_k q[b][h][k] * M[h][i][k]        (q~ = q^nope M_h^T)
+ *   q_rot[b][h][:] = RoPE(q[b][h][d_c : d_c+d_r], lens[b]-1)
+ * Outputs are fp32 and unscaled.  q_rot may be NULL when d_r == 0.
+ */
+int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
+                     const int32_t* lens, float* q_abs, float* q_rot, void* stream);
+
+/*
+ * gva_decode_attention -- the attention steps of Algorithm 1 over split s
+ * of every sequence, for every (b, h, s):
+ *   rows    P = [s*c_b, min(L_b, (s+1)*c_b)),  L_b = lens[b] (clamped),
+ *           c_b = 32 * ceil(ceil(L_b / S) / 32),  S = num_splits
+ *   score   x_t = scale * ( q~_h . v_cache[b][g(h)][t] + q^rope_h . kr_cache[b][t] )
+ *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
+ *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)       (natural log)
+ * An empty P writes o_part = 0 and lse_part = -inf.  With S == 1 the
+ * partials are the final (o, lse).
+ * The query comes either raw -- q and m non-NULL, q_abs and q_rot NULL: the
+ * kernel absorbs and rotates it itself ahead of the attention loop (the
+ * fused path) -- or pre-absorbed by gva_absorb_query: q/m NULL, q_abs
+ * [B][H][d_v] fp32 and (if d_r > 0) q_rot [B][H][d_r] fp32 non-NULL.
+ * o_part [B][H][S][d_v] fp32, lse_part [B][H][S] fp32.
+ * Supported for bf16: d_v in {64, 128}, d_c a multiple of 32 (<= 512),
+ * d_r a multiple of 8 (<= 64), H/G in {1, 2, 4, 8}; for fp32: d_v <= 256,
+ * d_c <= 512, d_r <= 64, H/G <= 8.  Other valid shapes: GVA_ERR_UNSUPPORTED.
+ * Pointers: 16-byte aligned.
+ */
+int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
+                         const float* q_abs, const float* q_rot,
+                         const void* v_cache, const void* kr_cache,
+                         const int32_t* lens, int32_t num_splits,
+                         float* o_part, float* lse_part, void* stream);
+
+/*
+ * gva_combine -- log-sum-exp merge of split partials, for every (b, h):
+ *   LSE = log sum_s exp(lse_part[b][h][s]);
+ *   o[b][h][:] = sum_s exp(lse_part[b][h][s] - LSE) * o_part[b][h][s][:]
+ * Partials with lse = -inf are skipped; if all are, o = 0 and LSE = -inf.
+ * lse may be NULL.  o [B][H][d_v] fp32, lse [B][H] fp32.
+ */
+int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part,
+                int32_t num_splits, float* o, float* lse, void* stream);
+
+/*
+ * gva_pick_splits -- host heuristic: a num_splits for sequences of up to
+ * max_len rows on a device with n_cu compute units (0 = query device 0's).
+ * Pure host code; enqueues nothing.  Returns a value in [1, GVA_MAX_SPLITS].
+ */
+int gva_pick_splits(const gva_dims* dims, int32_t max_len, int32_t n_cu);
+
+/* Human-readable name of a gva_status value (static storage). */
+const char* gva_status_string(int status);
+
+/* ABI version of this header: major * 10000 + minor * 100 + patch. */
+int gva_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* GVA_H_ */

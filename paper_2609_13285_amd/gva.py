@@ -1,0 +1,224 @@
+"""Thin ctypes binding of libgva.so (declared in include/gva.h).
+
+Argument marshalling only: every function here checks the tensors it is
+given (device, dtype, shape, contiguity), passes raw device pointers and the
+current HIP stream, and raises :class:`GvaError` on a non-zero status.  All
+arithmetic runs in the HIP kernels.  There is no fallback: if libgva.so is
+missing, the first call raises.
+"""
+
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Tuple
+
+import torch
+
+LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgva.so")
+
+GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, 1, 2, 3
+GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
+GVA_MAX_SPLITS = 256
+EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
+           "gva_pick_splits", "gva_status_string", "gva_version")
+
+
+class GvaError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status_string(status)} ({status})")
+
+
+class GvaDims(ctypes.Structure):
+    _fields_ = [("batch", ctypes.c_int32), ("n_heads", ctypes.c_int32),
+                ("n_groups", ctypes.c_int32), ("d_v", ctypes.c_int32),
+                ("d_c", ctypes.c_int32), ("d_r", ctypes.c_int32),
+                ("t_max", ctypes.c_int32), ("dtype", ctypes.c_int32),
+                ("rope_base", ctypes.c_double), ("scale", ctypes.c_double)]
+
+    @property
+    def torch_dtype(self) -> torch.dtype:
+        return torch.bfloat16 if self.dtype == GVA_DTYPE_BF16 else torch.float32
+
+    def __repr__(self):
+        return ("GvaDims(" + ", ".join(f"{k}={getattr(self, k)}" for k, _ in self._fields_) + ")")
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    """Load libgva.so (once).  Raises GvaError-like RuntimeError if absent."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise RuntimeError(f"{LIB_PATH} is not built: run `python -m paper_2609_13285_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        P, I32 = ctypes.c_void_p, ctypes.c_int32
+        D = ctypes.POINTER(GvaDims)
+        L.gva_append_kv.argtypes = [D, P, P, P, P, P, P, I32, P]
+        L.gva_absorb_query.argtypes = [D, P, P, P, P, P, P]
+        L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, I32, P, P, P]
+        L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
+        L.gva_pick_splits.argtypes = [D, I32, I32]
+        L.gva_status_string.argtypes = [ctypes.c_int]
+        L.gva_status_string.restype = ctypes.c_char_p
+        L.gva_version.argtypes = []
+        for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
+                     "gva_pick_splits", "gva_version"):
+            getattr(L, name).restype = ctypes.c_int
+        _lib = L
+    return _lib
+
+
+def status_string(status: int) -> str:
+    return lib().gva_status_string(int(status)).decode()
+
+
+def make_dims(batch: int, n_heads: int, n_groups: int, d_v: int, d_c: int, d_r: int,
+              t_max: int, dtype, rope_base: float = 10000.0, scale: float = 0.0) -> GvaDims:
+    if isinstance(dtype, torch.dtype):
+        code = {torch.bfloat16: GVA_DTYPE_BF16, torch.float32: GVA_DTYPE_F32}[dtype]
+    elif isinstance(dtype, str):
+        code = {"bf16": GVA_DTYPE_BF16, "f32": GVA_DTYPE_F32}[dtype]
+    else:
+        code = int(dtype)
+    return GvaDims(batch, n_heads, n_groups, d_v, d_c, d_r, t_max, code, float(rope_base), float(scale))
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, torch.cuda.Stream):
+        return stream.cuda_stream
+    return int(stream)
+
+
+def _ptr(t: Optional[torch.Tensor], name: str, dtype=None, shape=None):
+    if t is None:
+        return None
+    if not isinstance(t, torch.Tensor):
+        raise TypeError(f"{name} must be a tensor")
+    if t.device.type != "cuda":
+        raise ValueError(f"{name} must be a GPU tensor")
+    if not t.is_contiguous():
+        raise ValueError(f"{name} must be contiguous")
+    if dtype is not None and t.dtype != dtype:
+        raise ValueError(f"{name} must be {dtype}, got {t.dtype}")
+    if shape is not None and tuple(t.shape) != tuple(shape):
+        raise ValueError(f"{name} must have shape {tuple(shape)}, got {tuple(t.shape)}")
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _check(fn: str, status: int):
+    if status != GVA_OK:
+        raise GvaError(fn, status)
+
+
+def gva_append_kv(dims: GvaDims, v_cache, kr_cache, v_new, kr_new, seq, pos, stream=None):
+    d = dims
+    dt = d.torch_dtype
+    n = seq.numel()
+    st = lib().gva_append_kv(
+        ctypes.byref(d),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)),
+        _ptr(v_new, "v_new", dt, (n, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (n, d.d_r)),
+        _ptr(seq, "seq", torch.int32, (n,)), _ptr(pos, "pos", torch.int32, (n,)),
+        n, _stream(stream))
+    _check("gva_append_kv", st)
+
+
+def gva_absorb_query(dims: GvaDims, q, m, lens, q_abs, q_rot, stream=None):
+    d = dims
+    dt = d.torch_dtype
+    st = lib().gva_absorb_query(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(q_abs, "q_abs", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(q_rot, "q_rot", torch.float32, (d.batch, d.n_heads, d.d_r)),
+        _stream(stream))
+    _check("gva_absorb_query", st)
+
+
+def gva_decode_attention(dims: GvaDims, v_cache, kr_cache, lens, num_splits: int, o_part, lse_part,
+                         q=None, m=None, q_abs=None, q_rot=None, stream=None):
+    d = dims
+    dt = d.torch_dtype
+    S = int(num_splits)
+    st = lib().gva_decode_attention(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(q_abs, "q_abs", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(q_rot, "q_rot", torch.float32, (d.batch, d.n_heads, d.d_r)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        S,
+        _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
+        _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
+        _stream(stream))
+    _check("gva_decode_attention", st)
+
+
+def gva_combine(dims: GvaDims, o_part, lse_part, num_splits: int, o, lse=None, stream=None):
+    d = dims
+    S = int(num_splits)
+    st = lib().gva_combine(
+        ctypes.byref(d),
+        _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
+        _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
+        S,
+        _ptr(o, "o", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(lse, "lse", torch.float32, (d.batch, d.n_heads)),
+        _stream(stream))
+    _check("gva_combine", st)
+
+
+def gva_pick_splits(dims: GvaDims, max_len: int = 0, n_cu: int = 0) -> int:
+    return int(lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(n_cu)))
+
+
+def gva_version() -> int:
+    return int(lib().gva_version())
+
+
+class DecodeBuffers:
+    """Device buffers for one decode step's split partials and outputs."""
+
+    def __init__(self, dims: GvaDims, num_splits: int, device="cuda"):
+        d = dims
+        self.num_splits = int(num_splits)
+        self.o_part = torch.empty(d.batch, d.n_heads, self.num_splits, d.d_v, dtype=torch.float32, device=device)
+        self.lse_part = torch.empty(d.batch, d.n_heads, self.num_splits, dtype=torch.float32, device=device)
+        self.o = torch.empty(d.batch, d.n_heads, d.d_v, dtype=torch.float32, device=device)
+        self.lse = torch.empty(d.batch, d.n_heads, dtype=torch.float32, device=device)
+
+
+def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
+           bufs: Optional[DecodeBuffers] = None, fused: bool = True,
+           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Absorb + attention + combine for one step; returns (o, lse) fp32.
+
+    ``fused`` runs the absorption inside the attention kernel; otherwise
+    gva_absorb_query runs first and the attention kernel reads its output.
+    """
+    S = int(num_splits)
+    if bufs is None or bufs.num_splits != S:
+        bufs = DecodeBuffers(dims, S, device=v_cache.device)
+    if fused:
+        gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
+                             q=q, m=m, stream=stream)
+    else:
+        q_abs = torch.empty(dims.batch, dims.n_heads, dims.d_v, dtype=torch.float32, device=v_cache.device)
+        q_rot = torch.empty(dims.batch, dims.n_heads, dims.d_r, dtype=torch.float32, device=v_cache.device)
+        gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
+        gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
+                             q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream)
+    gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
+    return bufs.o, bufs.lse

@@ -1,0 +1,129 @@
+"""The C ABI without a GPU: libgva.so loads, exports every entry point that
+include/gva.h declares, and host-side validation rejects bad arguments
+before anything is enqueued (no compute call runs here)."""
+
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_13285_amd import gva
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "gva.h")
+
+# fake device pointers: aligned, never dereferenced because validation fails first
+A = 0x10000
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(gva_\w+)\s*\(", text, flags=re.M)))
+
+
+def test_header_declares_the_four_calls():
+    names = declared_functions()
+    for n in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine"):
+        assert n in names
+    assert set(names) == set(gva.EXPORTS)
+
+
+def test_library_exports_every_declared_symbol():
+    lib = gva.lib()
+    for name in declared_functions():
+        assert hasattr(lib, name), name
+    assert gva.gva_version() == 10000
+
+
+def test_status_strings():
+    assert gva.status_string(0) == "ok"
+    assert "invalid" in gva.status_string(1)
+    assert "unsupported" in gva.status_string(2)
+    assert "HIP" in gva.status_string(3)
+    assert gva.status_string(99) == "unknown status"
+
+
+def dims(**kw):
+    base = dict(batch=2, n_heads=8, n_groups=2, d_v=128, d_c=128, d_r=16, t_max=64,
+                dtype="bf16", rope_base=10000.0, scale=0.0)
+    base.update(kw)
+    return gva.make_dims(**base)
+
+
+def decode_status(d, S=4, q=A, m=A, qa=None, qr=None, v=A, kr=A, lens=A, op=A, lp=A):
+    return gva.lib().gva_decode_attention(ctypes.byref(d), q, m, qa, qr, v, kr, lens, S, op, lp, None)
+
+
+@pytest.mark.parametrize("kw", [
+    dict(batch=0), dict(n_heads=0), dict(n_groups=0), dict(t_max=0),
+    dict(n_heads=6, n_groups=4),           # H not a multiple of G
+    dict(d_r=15),                          # odd positional width
+    dict(d_r=-2), dict(d_v=0), dict(dtype=7),
+    dict(scale=-1.0), dict(scale=float("nan")), dict(rope_base=0.0),
+])
+def test_bad_dims_rejected(kw):
+    assert decode_status(dims(**kw)) == gva.GVA_ERR_INVALID_ARG
+
+
+def test_bad_split_counts_rejected():
+    d = dims()
+    assert decode_status(d, S=0) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, S=gva.GVA_MAX_SPLITS + 1) == gva.GVA_ERR_INVALID_ARG
+    lib = gva.lib()
+    assert lib.gva_combine(ctypes.byref(d), A, A, 0, A, None, None) == gva.GVA_ERR_INVALID_ARG
+
+
+def test_null_and_misaligned_pointers_rejected():
+    d = dims()
+    assert decode_status(d, v=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, kr=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, lens=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, op=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, v=A + 2) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, op=A + 4) == gva.GVA_ERR_INVALID_ARG
+    # exactly one way to pass the query: raw (q, m) or absorbed (q_abs, q_rot)
+    assert decode_status(d, q=None, m=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, q=A, m=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, qa=A, qr=A) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, q=None, m=None, qa=A, qr=None) == gva.GVA_ERR_INVALID_ARG
+
+
+def test_unsupported_shapes_reported():
+    assert decode_status(dims(d_v=96)) == gva.GVA_ERR_UNSUPPORTED           # bf16 d_v
+    assert decode_status(dims(d_c=48)) == gva.GVA_ERR_UNSUPPORTED           # d_c % 32
+    assert decode_status(dims(d_r=12)) == gva.GVA_ERR_UNSUPPORTED           # d_r % 8
+    assert decode_status(dims(n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED  # H/G = 16
+    assert decode_status(dims(dtype="f32", d_v=512)) == gva.GVA_ERR_UNSUPPORTED
+    assert decode_status(dims(d_r=66)) == gva.GVA_ERR_UNSUPPORTED           # > 32 RoPE pairs
+
+
+def test_append_validation():
+    lib = gva.lib()
+    d = dims()
+    # n_rows == 0 is a no-op that succeeds without touching the device
+    assert lib.gva_append_kv(ctypes.byref(d), A, A, A, A, A, A, 0, None) == gva.GVA_OK
+    assert lib.gva_append_kv(ctypes.byref(d), A, A, A, A, A, A, -1, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_append_kv(ctypes.byref(d), None, A, A, A, A, A, 3, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_append_kv(ctypes.byref(d), A + 8, A, A, A, A, A, 3, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_append_kv(ctypes.byref(d), A, None, A, A, A, A, 3, None) == gva.GVA_ERR_INVALID_ARG
+    d2 = dims(d_v=4)  # 8-byte bf16 rows cannot be copied in 16-byte pieces
+    assert lib.gva_append_kv(ctypes.byref(d2), A, A, A, A, A, A, 3, None) == gva.GVA_ERR_UNSUPPORTED
+
+
+def test_absorb_validation():
+    lib = gva.lib()
+    d = dims()
+    assert lib.gva_absorb_query(ctypes.byref(d), None, A, A, A, A, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_absorb_query(ctypes.byref(d), A, A, A, A, None, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_absorb_query(None, A, A, A, A, A, None) == gva.GVA_ERR_INVALID_ARG
+
+
+def test_pick_splits_is_host_only_and_bounded():
+    d = dims(batch=32, n_heads=32, n_groups=8, t_max=8192)
+    s = gva.gva_pick_splits(d, 8192, 256)
+    assert 1 <= s <= gva.GVA_MAX_SPLITS
+    assert gva.gva_pick_splits(d, 100, 256) == 1          # short sequences: no split
+    d3 = dims(batch=4, n_heads=32, n_groups=8, t_max=131072, d_r=32)
+    assert gva.gva_pick_splits(d3, 131072, 256) >= 16     # few streams: many splits
