@@ -130,7 +130,9 @@ def main():
                       w.rope_base)
     max_len = int(inp["lens"].max())
     S = args.splits or gva.gva_pick_splits(d, max_len)
-    dev = {k: inp[k].cuda() for k in ("q", "m", "v", "kr", "lens", "v_new", "kr_new")}
+    dev = {k: inp[k].cuda() for k in ("q", "m", "lens", "v_new", "kr_new")}
+    dev["v"] = gva.tiled(inp["v"]).cuda()          # the library's cache layout
+    dev["kr"] = gva.tiled(inp["kr"]).cuda()
     seq = torch.arange(w.batch, dtype=torch.int32)
     pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
     seq_d, pos_d = seq.cuda(), pos.cuda()

@@ -30,11 +30,23 @@
  *                                  slice, unrotated
  *     M        [H][d_v][d_c]       M_h maps a d_v-wide value to a d_c-wide
  *                                  content key (K_h = V_g(h) M_h, eq. kvm)
- *     v_cache  [B][G][T][d_v]      grouped value cache
- *     kr_cache [B][T][d_r]         shared positional key cache, stored
- *                                  already rotated
+ *     v_cache  B*G streams of T rows x d_v   grouped value cache
+ *     kr_cache B streams of T rows x d_r     shared positional key cache,
+ *                                  stored already rotated
+ *   Both caches use the tiled layout below (their total sizes equal the
+ *   row-major [B][G][T][d_v] and [B][T][d_r] arrays).  They are written by
+ *   gva_append_kv; a caller that fills them itself must follow the layout.
  *     lens     [B] int32           cached rows per sequence; the query sits
  *                                  at position lens[b]-1 (positions 0-based)
+ * - Tiled cache layout.  Stream (b, g) of v_cache starts at element
+ *   (b*G + g)*T*d_v, stream b of kr_cache at b*T*d_r.  With D the row width
+ *   of the stream, E the element size and P = 16/E elements per 16-byte
+ *   piece, element (t, i) of a stream sits at element offset
+ *       (t/16)*16*D + ((i/P)*16 + t%16)*P + i%P
+ *   i.e. tiles of 16 rows, inside a tile the 16-byte pieces of the rows
+ *   ordered piece-major.  This lets one wave-wide 16-byte load fetch 1 KB of
+ *   contiguous memory into matrix-core operand order.  It requires T % 16 ==
+ *   0 and d_v, d_r multiples of P (8 for bf16, 4 for fp32).
  * - Head h reads value group g(h) = h / (H/G).
  * - RoPE rotates interleaved pairs (2i, 2i+1) by the angle
  *   p * rope_base^(-2i/d_r), formed in fp64, as the row-vector product
@@ -96,8 +108,9 @@ typedef struct gva_dims {
  * [n_rows].  Rows with b or p out of range are skipped.  Writing the same
  * (b, p) twice with the same data is idempotent; two rows naming the same
  * (b, p) in one call race.  n_rows == 0 is a no-op.
- * Pointers: v_cache, v_new 16-byte aligned; kr_cache, kr_new 4-byte
- * aligned (when d_r > 0).
+ * Pointers: v_cache, v_new, kr_cache 16-byte aligned; kr_new 4-byte
+ * aligned (the last two only when d_r > 0).  Shapes outside the tiled
+ * layout's requirements: GVA_ERR_UNSUPPORTED.
  */
 int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache,
                   const void* v_new, const void* kr_new,
@@ -110,6 +123,8 @@ int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache,
  *   q_abs[b][h][i] = sum_k q[b][h][k] * M[h][i][k]        (q~ = q^nope M_h^T)
  *   q_rot[b][h][:] = RoPE(q[b][h][d_c : d_c+d_r], lens[b]-1)
  * Outputs are fp32 and unscaled.  q_rot may be NULL when d_r == 0.
+ * bf16 needs d_v % 16 == 0, d_c % 32 == 0, d_r % 8 == 0 (matrix cores);
+ * fp32 takes any shape.  q, m, q_abs 16-byte aligned.
  */
 int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
                      const int32_t* lens, float* q_abs, float* q_rot, void* stream);
@@ -132,6 +147,7 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
  * Supported for bf16: d_v in {64, 128}, d_c a multiple of 32 (<= 512),
  * d_r a multiple of 8 (<= 64), H/G in {1, 2, 4, 8}; for fp32: d_v <= 256,
  * d_c <= 512, d_r <= 64, H/G <= 8.  Other valid shapes: GVA_ERR_UNSUPPORTED.
+ * Every shape must also satisfy the tiled cache layout (T % 16 == 0).
  * Pointers: 16-byte aligned.
  */
 int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
@@ -145,7 +161,7 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
  *   LSE = log sum_s exp(lse_part[b][h][s]);
  *   o[b][h][:] = sum_s exp(lse_part[b][h][s] - LSE) * o_part[b][h][s][:]
  * Partials with lse = -inf are skipped; if all are, o = 0 and LSE = -inf.
- * lse may be NULL.  o [B][H][d_v] fp32, lse [B][H] fp32.
+ * lse may be NULL.  o [B][H][d_v] fp32, lse [B][H] fp32; d_v <= 256.
  */
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part,
                 int32_t num_splits, float* o, float* lse, void* stream);

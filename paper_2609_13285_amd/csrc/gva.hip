@@ -8,29 +8,39 @@
 //
 // Kernels
 //   append_kernel        Algorithm 1 append steps + eq. krope (fp64 rotation)
-//   absorb_kernel        eq. absorb and the query rotation, standalone
-//   decode_bf16_kernel   the hot path: fused absorb prologue, then a
-//                        split-KV streaming loop over the value and
+//   absorb_bf16_kernel   eq. absorb + query rotation on the matrix cores
+//   absorb_f32_kernel    the same on the vector ALUs, fp32 storage
+//   decode_bf16_kernel   the hot path: split-KV streaming over the value and
 //                        positional-key rows of one (sequence, group, split)
-//                        on the matrix cores, with an online softmax
+//                        on the matrix cores, online softmax, optional fused
+//                        absorption prologue
 //   decode_f32_kernel    fp32-storage variant on the vector ALUs
 //   combine_kernel       log-sum-exp merge of the split partials
 //
+// Cache layout (MFMA-native).  Each (sequence, group) value stream and each
+// sequence's positional-key stream is stored in tiles of 16 rows; inside a
+// tile the row pieces of 16 bytes are ordered piece-major:
+//   element (t, i) of a stream with D columns of E bytes, P = 16/E:
+//     (t/16)*16*D + ((i/P)*16 + t%16)*P + i%P
+// A wave's 16-byte-per-lane load of 64 consecutive pieces then covers 1 KB
+// of contiguous memory while every lane receives exactly the 8 bf16 of one
+// row that its matrix-core operand slot needs (row = lane%16, columns
+// 8*(lane/16) .. +7 of a 32-column chunk).
+//
 // Hot-loop design (bf16).  A workgroup owns one (b, g, split); its 4 waves
-// take interleaved 32-row tiles.  Each lane loads 16-byte pieces of the V
-// rows straight into MFMA operand registers (no LDS round trip), and every
-// V tile serves all H/G heads of the group:
+// take interleaved 32-row tiles and keep DEPTH tiles in registers.  Every V
+// tile serves all H/G heads of the group:
 //   scores  S^T[t][n] = V[t][:] . Bq[:][n]           (v_mfma 16x16x32 bf16)
-//           columns n hold each head's absorbed query twice, as a bf16 high
-//           part and a bf16 low part (q~ = hi + lo to ~2^-16), mirrored so
-//           a DPP mirror adds the pair; the positional key rides as one more
+//           column n holds one head's absorbed query as a bf16 high part or
+//           low part (q~ = hi + lo to ~2^-16); the columns are mirrored so a
+//           DPP mirror adds the pair; the positional key rides as one more
 //           K-chunk of the same product
 //   P.V     O^T[i][n] += V^T[i][t] P[t][n]            (v_mfma 16x16x32 bf16)
-//           V^T comes from an identity-selector MFMA on the same registers,
-//           P again split hi + lo, so both products keep ~fp32 accuracy
+//           V^T comes from an identity-selector MFMA on the same registers;
+//           P is split hi + lo again, so both products keep ~fp32 accuracy
 // The score layout the MFMA returns (lane = column, registers = 4 rows) is
 // exactly the B-operand layout of the P.V product, so the softmax needs no
-// cross-lane shuffles except the max over the four 16-lane rows.
+// cross-lane traffic except the max over the four 16-lane rows.
 
 #include <hip/hip_runtime.h>
 #include <math.h>
@@ -49,10 +59,13 @@ typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
 
 constexpr int kWaves = 4;             // waves per workgroup in the decode kernels
 constexpr int kThreads = 64 * kWaves;
-constexpr int kTileRows = 32;         // rows per tile = split granularity
+constexpr int kTileRows = 32;         // rows per compute tile = split granularity
+constexpr int kLayoutRows = 16;       // rows per cache layout tile
 constexpr int kMaxPairs = 32;         // d_r / 2 <= 32
 constexpr float kLn2 = 0.693147180559945309417f;
 constexpr double kLog2e = 1.44269504088896340736;
+constexpr int kBufferWord3 = 0x00020000;   // raw buffer descriptor, 32-bit data format
+constexpr int kAuxNT = 2;                  // non-temporal: the V stream is read once
 
 // ------------------------------------------------------------ parameters
 struct AppendParams {
@@ -115,7 +128,7 @@ __device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t 
 // Round a double to bfloat16 in one step: round to float with round-to-odd
 // (truncate, then set the sticky bit if inexact), then nearest-even to bf16.
 // Round-to-odd onto a format with >= 2 extra bits makes the second rounding
-// exact-equivalent to a single rounding from the double.
+// equivalent to a single rounding from the double.
 __device__ __forceinline__ uint16_t f64_to_bf16_rne(double x) {
   if (x != x) return (uint16_t)0x7FC0;
   float f = (float)x;
@@ -139,6 +152,13 @@ __device__ __forceinline__ void store_from_f64<float>(float* p, int64_t i, doubl
 template <>
 __device__ __forceinline__ void store_from_f64<uint16_t>(uint16_t* p, int64_t i, double x) {
   p[i] = f64_to_bf16_rne(x);
+}
+
+// Element offset of (t, i) inside one stream of the tiled cache layout.
+template <typename T>
+__host__ __device__ __forceinline__ int64_t tiled_off(int64_t t, int i, int D) {
+  constexpr int P = 16 / (int)sizeof(T);
+  return (t / kLayoutRows) * kLayoutRows * D + ((int64_t)(i / P) * kLayoutRows + t % kLayoutRows) * P + i % P;
 }
 
 __device__ __forceinline__ int clamp_len(const int32_t* lens, int b, int t_max) {
@@ -176,6 +196,21 @@ __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
   return v;
+}
+
+// max of x over the four 16-lane rows of a wave (lanes l, l^16, l^32, l^48),
+// with the gfx950 row-swap permutes (no LDS round trip)
+__device__ __forceinline__ float max_over_rows(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
+}
+__device__ __forceinline__ float sum_over_rows(float x) {
+  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
+  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
+  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
 }
 
 // DPP control that pairs MFMA column n (a head's high part) with the column
@@ -217,55 +252,114 @@ __device__ __forceinline__ bf16x8 split_hi_lo(const float* x, bool lo) {
   return out;
 }
 
+__device__ __forceinline__ void rotate_pair(double x0, double x1, double a, double& y0, double& y1) {
+  double s, c;
+  sincos(a, &s, &c);
+  y0 = x0 * c - x1 * s;
+  y1 = x0 * s + x1 * c;
+}
+
 // ================================================================ append
+// One workgroup per new row.  The value pieces are loaded before seq/pos are
+// known (they are indexed by the row alone), so the kernel makes a single
+// dependent round trip to memory.
 template <typename T>
 __global__ void __launch_bounds__(256) append_kernel(AppendParams p) {
   const int r = blockIdx.x;
+  const int tid = threadIdx.x;
+  constexpr int P = 16 / sizeof(T);
+  const int pieces_per_row = p.d_v / P;
+  const int n_pieces = p.G * pieces_per_row;
+  const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const T*>(p.v_new) + (int64_t)r * p.G * p.d_v);
+  u32x4 piece = {0u, 0u, 0u, 0u};
+  if (tid < n_pieces) piece = src[tid];
+  const T* kin = static_cast<const T*>(p.kr_new) + (int64_t)r * p.d_r;
+  double k0 = 0.0, k1 = 0.0;
+  const bool has_pair = tid < p.d_r / 2;
+  if (has_pair) {
+    k0 = load_elem<T>(kin, 2 * tid);
+    k1 = load_elem<T>(kin, 2 * tid + 1);
+  }
   const int b = p.seq[r], ps = p.pos[r];
   if (b < 0 || b >= p.B || ps < 0 || ps >= p.t_max) return;
-  const int tid = threadIdx.x;
-  // value rows: 16-byte vectors (d_v * sizeof(T) is a multiple of 16)
-  constexpr int kVec = 16 / sizeof(T);
-  const int vec_per_row = p.d_v / kVec;
-  const u32x4* src = reinterpret_cast<const u32x4*>(static_cast<const T*>(p.v_new) + (int64_t)r * p.G * p.d_v);
-  for (int idx = tid; idx < p.G * vec_per_row; idx += blockDim.x) {
-    const int g = idx / vec_per_row, c = idx % vec_per_row;
-    T* dst = static_cast<T*>(p.v_cache) + (((int64_t)b * p.G + g) * p.t_max + ps) * p.d_v;
-    reinterpret_cast<u32x4*>(dst)[c] = src[idx];
+  for (int idx = tid; idx < n_pieces; idx += blockDim.x) {
+    if (idx != tid) piece = src[idx];
+    const int g = idx / pieces_per_row, c = idx % pieces_per_row;
+    T* stream = static_cast<T*>(p.v_cache) + ((int64_t)b * p.G + g) * p.t_max * p.d_v;
+    *reinterpret_cast<u32x4*>(stream + tiled_off<T>(ps, c * P, p.d_v)) = piece;
   }
-  // positional key: rotate each pair at position ps in fp64 (eq. krope)
-  const T* kin = static_cast<const T*>(p.kr_new) + (int64_t)r * p.d_r;
-  T* kout = static_cast<T*>(p.kr_cache) + ((int64_t)b * p.t_max + ps) * p.d_r;
-  for (int i = tid; i < p.d_r / 2; i += blockDim.x) {
-    const double x0 = load_elem<T>(kin, 2 * i), x1 = load_elem<T>(kin, 2 * i + 1);
-    const double a = (double)ps * p.inv_freq[i];
-    const double c = cos(a), s = sin(a);
-    store_from_f64<T>(kout, 2 * i, x0 * c - x1 * s);
-    store_from_f64<T>(kout, 2 * i + 1, x0 * s + x1 * c);
+  // positional key: rotate pair i at position ps in fp64 (eq. krope)
+  if (has_pair) {
+    T* kstream = static_cast<T*>(p.kr_cache) + (int64_t)b * p.t_max * p.d_r;
+    double y0, y1;
+    rotate_pair(k0, k1, (double)ps * p.inv_freq[tid], y0, y1);
+    const int64_t o = tiled_off<T>(ps, 2 * tid, p.d_r);   // the pair shares a piece
+    store_from_f64<T>(kstream, o, y0);
+    store_from_f64<T>(kstream, o + 1, y1);
   }
 }
 
 // ================================================================ absorb
-template <typename T>
-__global__ void __launch_bounds__(128) absorb_kernel(AbsorbParams p) {
+// bf16, matrix cores.  Workgroup = (head h, 16 sequences); wave w computes
+// the output blocks ib = w, w+4, ... of q~^T[i][b] = sum_k M_h[i][k] q[b][h][k]
+// (A = rows of M_h, B = the query rows, K = d_c).
+__global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
+  const int h = blockIdx.x;
+  const int b0 = blockIdx.y * 16;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, qd = lane >> 4;
+  const int W = p.d_c + p.d_r;
+  const uint16_t* qg = static_cast<const uint16_t*>(p.q);
+  const uint16_t* mh = static_cast<const uint16_t*>(p.m) + (int64_t)h * p.d_v * p.d_c;
+  const int bq = min(b0 + n, p.B - 1);                  // rows past B compute a duplicate
+  const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
+  const int nb = p.d_v / 16;
+  for (int ib = w; ib < nb; ib += kWaves) {
+    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int c = 0; c < p.d_c / 32; ++c) {
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
+      const bf16x8 x = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
+      acc = mfma16(a, x, acc);
+    }
+    // lane (n, qd) holds q~[b0 + n][16 ib + 4 qd + jj]
+    if (b0 + n < p.B)
+      *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(b0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
+  }
+  const int npair = p.d_r / 2;
+  for (int idx = tid; idx < 16 * npair; idx += kThreads) {
+    const int bl = idx / npair, i = idx % npair;
+    const int b = b0 + bl;
+    if (b >= p.B) continue;
+    const int L = clamp_len(p.lens, b, p.t_max);
+    const uint16_t* qr = qg + ((int64_t)b * p.H + h) * W + p.d_c;
+    double y0, y1;
+    rotate_pair(bf16_bits_to_f32(qr[2 * i]), bf16_bits_to_f32(qr[2 * i + 1]),
+                (double)(L > 0 ? L - 1 : 0) * p.inv_freq[i], y0, y1);
+    float* out = p.q_rot + ((int64_t)b * p.H + h) * p.d_r + 2 * i;
+    out[0] = (float)y0;
+    out[1] = (float)y1;
+  }
+}
+
+// fp32 storage, vector ALUs: one workgroup per (b, h).
+__global__ void __launch_bounds__(128) absorb_f32_kernel(AbsorbParams p) {
   const int bh = blockIdx.x;
   const int b = bh / p.H, h = bh % p.H;
   const int W = p.d_c + p.d_r;
-  const T* q = static_cast<const T*>(p.q) + (int64_t)bh * W;
-  const T* m = static_cast<const T*>(p.m) + (int64_t)h * p.d_v * p.d_c;
+  const float* q = static_cast<const float*>(p.q) + (int64_t)bh * W;
+  const float* m = static_cast<const float*>(p.m) + (int64_t)h * p.d_v * p.d_c;
   for (int i = threadIdx.x; i < p.d_v; i += blockDim.x) {
     float acc = 0.f;
-    for (int k = 0; k < p.d_c; ++k) acc = fmaf(load_elem<T>(q, k), load_elem<T>(m, (int64_t)i * p.d_c + k), acc);
+    for (int k = 0; k < p.d_c; ++k) acc = fmaf(q[k], m[(int64_t)i * p.d_c + k], acc);
     p.q_abs[(int64_t)bh * p.d_v + i] = acc;
   }
   const int L = clamp_len(p.lens, b, p.t_max);
-  const double pos = L > 0 ? (double)(L - 1) : 0.0;
   for (int i = threadIdx.x; i < p.d_r / 2; i += blockDim.x) {
-    const double x0 = load_elem<T>(q, p.d_c + 2 * i), x1 = load_elem<T>(q, p.d_c + 2 * i + 1);
-    const double a = pos * p.inv_freq[i];
-    const double c = cos(a), s = sin(a);
-    p.q_rot[(int64_t)bh * p.d_r + 2 * i] = (float)(x0 * c - x1 * s);
-    p.q_rot[(int64_t)bh * p.d_r + 2 * i + 1] = (float)(x0 * s + x1 * c);
+    double y0, y1;
+    rotate_pair(q[p.d_c + 2 * i], q[p.d_c + 2 * i + 1], (double)(L > 0 ? L - 1 : 0) * p.inv_freq[i], y0, y1);
+    p.q_rot[(int64_t)bh * p.d_r + 2 * i] = (float)y0;
+    p.q_rot[(int64_t)bh * p.d_r + 2 * i + 1] = (float)y1;
   }
 }
 
@@ -277,7 +371,8 @@ struct DecodeCfg {
   static constexpr int NC = DV / 32;                         // K-chunks per V row
   static constexpr int NB = DV / 16;                         // 16-wide i-blocks of the output
   static constexpr int DEPTH = DV >= 128 ? 3 : 4;
-  static constexpr int QS_STRIDE = DV + 4;                   // padded LDS row (floats)
+  static constexpr int CR = 16 / NB;                         // d_c chunks per absorption round
+  static constexpr int QS_STRIDE = DV + 4;                   // padded LDS rows (floats)
   static constexpr int QR_STRIDE = 32 * NRC + 4;
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
   static constexpr int LDS_RED = kWaves * HPG * (DV + 2);
@@ -293,7 +388,7 @@ struct Tile {
 template <int HPG, int DV, int NRC>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
   using Cfg = DecodeCfg<HPG, DV, NRC>;
-  constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH;
+  constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
   __shared__ float lds[Cfg::LDS_FLOATS];
 
   const int item = xcd_remap(blockIdx.x, gridDim.x);
@@ -301,97 +396,211 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int bs = item / p.G;
   const int s = bs % p.S;
   const int b = bs / p.S;
-  const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int n = lane & 15, qd = lane >> 4;     // MFMA column and 16-lane row
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform (SGPR)
+  const int n = lane & 15, qd = lane >> 4;     // MFMA column / row slot and 16-lane row
   const int h0 = g * HPG;
   const int L = clamp_len(p.lens, b, p.t_max);
   int r0, r1;
   split_rows(L, p.S, s, r0, r1);
-
-  // ---- prologue: absorbed, rotated, scaled queries of the group's heads
-  float* qs = lds;                                  // [HPG][QS_STRIDE]
-  float* qr = lds + HPG * Cfg::QS_STRIDE;           // [HPG][QR_STRIDE]
-  if (p.fused) {
-    // q~_h = q^nope_h M_h^T on the matrix cores: A = M_h rows (i), K = d_c,
-    // B = the query chunk broadcast to all 16 columns.
-    const uint16_t* qg = static_cast<const uint16_t*>(p.q);
-    const uint16_t* mg = static_cast<const uint16_t*>(p.m);
-    const int W = p.d_c + p.d_r;
-    for (int hl = w; hl < HPG; hl += kWaves) {
-      const int h = h0 + hl;
-      f32x4 acc[NB];
-#pragma unroll
-      for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
-      const uint16_t* qrow = qg + ((int64_t)b * p.H + h) * W;
-      const uint16_t* mh = mg + (int64_t)h * DV * p.d_c;
-      for (int c = 0; c < p.d_c / 32; ++c) {
-        const bf16x8 bq = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
-        bf16x8 am[NB];
-#pragma unroll
-        for (int ib = 0; ib < NB; ++ib)
-          am[ib] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
-#pragma unroll
-        for (int ib = 0; ib < NB; ++ib) acc[ib] = mfma16(am[ib], bq, acc[ib]);
-      }
-      if (n == 0) {
-#pragma unroll
-        for (int ib = 0; ib < NB; ++ib)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) qs[hl * Cfg::QS_STRIDE + 16 * ib + 4 * qd + jj] = acc[ib][jj] * p.scale_log2;
-      }
-    }
-    const int L1 = L > 0 ? L - 1 : 0;
-    const int npair = p.d_r / 2;
-    for (int idx = tid; idx < HPG * 16 * NRC; idx += kThreads) {
-      const int hl = idx / (16 * NRC), i = idx % (16 * NRC);
-      float y0 = 0.f, y1 = 0.f;
-      if (i < npair) {
-        const uint16_t* qrow = qg + ((int64_t)b * p.H + h0 + hl) * W + p.d_c;
-        const double x0 = bf16_bits_to_f32(qrow[2 * i]), x1 = bf16_bits_to_f32(qrow[2 * i + 1]);
-        const double a = (double)L1 * p.inv_freq[i];
-        const double c = cos(a), sn = sin(a);
-        y0 = (float)((x0 * c - x1 * sn) * (double)p.scale_log2);
-        y1 = (float)((x0 * sn + x1 * c) * (double)p.scale_log2);
-      }
-      qr[hl * Cfg::QR_STRIDE + 2 * i] = y0;
-      qr[hl * Cfg::QR_STRIDE + 2 * i + 1] = y1;
-    }
-  } else {
-    for (int idx = tid; idx < HPG * DV; idx += kThreads) {
-      const int hl = idx / DV, i = idx % DV;
-      qs[hl * Cfg::QS_STRIDE + i] = p.q_abs[((int64_t)b * p.H + h0 + hl) * DV + i] * p.scale_log2;
-    }
-    for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads) {
-      const int hl = idx / (32 * NRC), j = idx % (32 * NRC);
-      qr[hl * Cfg::QR_STRIDE + j] =
-          j < p.d_r ? p.q_rot[((int64_t)b * p.H + h0 + hl) * p.d_r + j] * p.scale_log2 : 0.f;
-    }
-  }
-  __syncthreads();
+  const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
 
   // Column roles: [hi_0 .. hi_{HPG-1}, lo_{HPG-1} .. lo_0, zero padding].
   const bool active = n < 2 * HPG;
   const bool is_lo = n >= HPG;
   const int col_head = !active ? 0 : (is_lo ? 2 * HPG - 1 - n : n);
-  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+
+  // ---- streaming setup.  Rows are read through buffer descriptors that end
+  // at the split's last layout tile: a tile past the end reads as zeros
+  // without touching memory, so prefetches are issued unconditionally (the
+  // wait counts stay static) and cost no traffic.  Each load is addressed as
+  // a loop-invariant per-lane offset plus the tile base in a scalar
+  // register.  Rows past the split inside its last layout tile may hold
+  // never-written data; the tail tile zeroes them before use.
+  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(vbase), (short)0, r1c * DV * 2, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kbase), (short)0, r1c * p.d_r * 2, kBufferWord3);
+  const int kpieces = p.d_r / 8;              // 16-byte pieces per key row
+  const int v_lane = qd * 256 + n * 16;       // piece qd of row n (of a 32-column chunk)
+  int k_lane[NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int rc = 0; rc < NRC; ++rc)            // lanes past d_r re-read a valid piece (weight 0)
+    k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
+  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
+
+  const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
+  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
+  auto tile_row = [&](int j) { return r0 + (w + kWaves * j) * kTileRows; };
+  auto load_tile = [&](Tile<DV, NRC>& t, int row0) {
+    const int lt = row0 / kLayoutRows;         // first layout tile (uniform)
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int vsoff = (lt + hf) * v_tile_bytes;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, kAuxNT));
+      const int ksoff = (lt + hf) * k_tile_bytes;
+#pragma unroll
+      for (int rc = 0; rc < NRC; ++rc)
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], ksoff, 0));
+    }
+  };
+  Tile<DV, NRC> buf[DEPTH];
+
+  // ---- prologue: absorbed, rotated, scaled queries as MFMA B operands.
+  // The query loads are issued before the V prefetch: loads retire in order,
+  // so waiting for the query does not wait for the prefetched tiles.
   bf16x8 bq[NC];
-#pragma unroll
-  for (int c = 0; c < NC; ++c) {
-    const float* src = qs + col_head * Cfg::QS_STRIDE + 32 * c + 8 * qd;
-    float x[8];
-#pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = src[j];
-    bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
-  }
   bf16x8 bk[NRC > 0 ? NRC : 1];
+  if (!p.fused) {
+    const int hq = h0 + col_head;
+    const float* qa = p.q_abs + ((int64_t)b * p.H + hq) * DV + 8 * qd;
+    f32x4 xa[NC][2];
 #pragma unroll
-  for (int rc = 0; rc < NRC; ++rc) {
-    const float* src = qr + col_head * Cfg::QR_STRIDE + 32 * rc + 8 * qd;
-    float x[8];
+    for (int c = 0; c < NC; ++c) {
+      xa[c][0] = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      xa[c][1] = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+    }
+    f32x4 xr[NRC > 0 ? NRC : 1][2];
 #pragma unroll
-    for (int j = 0; j < 8; ++j) x[j] = src[j];
-    bk[rc] = active ? split_hi_lo(x, is_lo) : zero8;
+    for (int rc = 0; rc < NRC; ++rc) {
+      const int j0 = min(32 * rc + 8 * qd, p.d_r - 8);    // lanes past d_r: any valid piece
+      const float* qr = p.q_rot + ((int64_t)b * p.H + hq) * p.d_r + j0;
+      xr[rc][0] = *reinterpret_cast<const f32x4*>(qr);
+      xr[rc][1] = *reinterpret_cast<const f32x4*>(qr + 4);
+    }
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int d = 0; d < DEPTH - 1; ++d) {
+      load_tile(buf[d], tile_row(d));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = xa[c][0][j] * p.scale_log2;
+        x[4 + j] = xa[c][1][j] * p.scale_log2;
+      }
+      bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const bool in_range = 32 * rc + 8 * qd < p.d_r;
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[j] = xr[rc][0][j] * p.scale_log2;
+        x[4 + j] = xr[rc][1][j] * p.scale_log2;
+      }
+      bk[rc] = (active && in_range) ? split_hi_lo(x, is_lo) : zero8;
+    }
+  } else {
+    // Fused absorption: q~_h = q^nope_h M_h^T on the matrix cores, wave w
+    // taking heads w, w+4, ...; A = rows i of M_h (K = d_c), B = the query
+    // chunk broadcast to all 16 columns.  The first round of M/q loads and
+    // the raw positional query go out before the V prefetch.
+    float* qs = lds;                                  // [HPG][QS_STRIDE]
+    float* qrs = lds + HPG * Cfg::QS_STRIDE;          // [HPG][QR_STRIDE]
+    const uint16_t* qg = static_cast<const uint16_t*>(p.q);
+    const uint16_t* mg = static_cast<const uint16_t*>(p.m);
+    const int W = p.d_c + p.d_r;
+    const int nck = p.d_c / 32;
+    // raw positional query pairs, one pair per thread
+    const int npair = p.d_r / 2;
+    const bool has_pair = tid < HPG * npair;
+    float rq0 = 0.f, rq1 = 0.f;
+    int pair_h = 0, pair_i = 0;
+    if (has_pair) {
+      pair_h = tid / npair;
+      pair_i = tid % npair;
+      const uint16_t* qrow = qg + ((int64_t)b * p.H + h0 + pair_h) * W + p.d_c + 2 * pair_i;
+      const uint32_t two = *reinterpret_cast<const uint32_t*>(qrow);
+      rq0 = bf16_bits_to_f32(two & 0xFFFFu);
+      rq1 = bf16_bits_to_f32(two >> 16);
+    }
+    bool prefetched = false;
+    for (int hl = w; hl < HPG; hl += kWaves) {
+      const int h = h0 + hl;
+      const uint16_t* qrow = qg + ((int64_t)b * p.H + h) * W;
+      const uint16_t* mh = mg + (int64_t)h * DV * p.d_c;
+      f32x4 acc[NB];
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+      for (int c0 = 0; c0 < nck; c0 += CR) {
+        bf16x8 am[CR][NB];
+        bf16x8 xq[CR];
+#pragma unroll
+        for (int cr = 0; cr < CR; ++cr) {
+          const int c = min(c0 + cr, nck - 1);
+          xq[cr] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
+#pragma unroll
+          for (int ib = 0; ib < NB; ++ib)
+            am[cr][ib] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
+        }
+        if (!prefetched) {
+          __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+          for (int d = 0; d < DEPTH - 1; ++d) {
+            load_tile(buf[d], tile_row(d));
+            __builtin_amdgcn_sched_barrier(0);
+          }
+          prefetched = true;
+        }
+#pragma unroll
+        for (int cr = 0; cr < CR; ++cr)
+          if (c0 + cr < nck)
+#pragma unroll
+            for (int ib = 0; ib < NB; ++ib) acc[ib] = mfma16(am[cr][ib], xq[cr], acc[ib]);
+      }
+      if (n == 0) {
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib)
+          *reinterpret_cast<f32x4*>(qs + hl * Cfg::QS_STRIDE + 16 * ib + 4 * qd) = acc[ib] * p.scale_log2;
+      }
+    }
+    if (!prefetched) {       // waves without a head of their own
+#pragma unroll
+      for (int d = 0; d < DEPTH - 1; ++d) {
+        load_tile(buf[d], tile_row(d));
+        __builtin_amdgcn_sched_barrier(0);
+      }
+    }
+    // rotate the positional query at position L-1 (fp64 angle)
+    for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads)
+      qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + idx % (32 * NRC)] = 0.f;
+    __syncthreads();
+    if (has_pair) {
+      double y0, y1;
+      rotate_pair(rq0, rq1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], y0, y1);
+      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i] = (float)(y0 * (double)p.scale_log2);
+      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = (float)(y1 * (double)p.scale_log2);
+    }
+    __syncthreads();
+    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const float* src = qs + col_head * Cfg::QS_STRIDE + 32 * c + 8 * qd;
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = src[j];
+      bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const float* src = qrs + col_head * Cfg::QR_STRIDE + 32 * rc + 8 * qd;
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) x[j] = src[j];
+      bk[rc] = active ? split_hi_lo(x, is_lo) : zero8;
+    }
   }
+
   // identity selectors for the V transpose: E_half[k][n] = (k == n + 16 half)
   bf16x8 esel[2];
 #pragma unroll
@@ -404,36 +613,23 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   }
 
   // ---- streaming loop
-  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
-  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
-  const int kvec = p.d_r / 8;                      // 16-byte vectors per key row
-
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 acc[NB];
 #pragma unroll
   for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 
-  const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
-  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
-
-  auto tile_row = [&](int j) { return r0 + (w + kWaves * j) * kTileRows; };
-  auto load_tile = [&](Tile<DV, NRC>& t, int row0) {
+  auto compute_tile = [&](Tile<DV, NRC>& t, int row0) {
+    if (row0 + kTileRows > r1) {             // ragged tail: clear rows past the split
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      int row = row0 + 16 * hf + n;
-      row = row < r1 ? row : r1 - 1;   // clamp: rows past the end are finite, masked later
-      const u32x4* vr = reinterpret_cast<const u32x4*>(vbase + (int64_t)row * DV);
+      for (int hf = 0; hf < 2; ++hf) {
+        const bool dead = row0 + 16 * hf + n >= r1;
 #pragma unroll
-      for (int c = 0; c < NC; ++c) t.v[hf][c] = as_bf16x8(__builtin_nontemporal_load(vr + 4 * c + qd));
+        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
 #pragma unroll
-      for (int rc = 0; rc < NRC; ++rc) {
-        int kv = 4 * rc + qd;
-        kv = kv < kvec ? kv : kvec - 1;  // lanes past d_r reload a valid piece; its weight is 0
-        t.k[hf][rc] = as_bf16x8(*(reinterpret_cast<const u32x4*>(kbase + (int64_t)row * p.d_r) + kv));
+        for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
       }
     }
-  };
-  auto compute_tile = [&](const Tile<DV, NRC>& t, int row0) {
     // scores: rows 16*hf + 4*qd + jj of the tile, column n
     f32x4 sc[2];
 #pragma unroll
@@ -452,7 +648,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
         const float v = sc[hf][jj];
         x[4 * hf + jj] = v + mirror<HPG>(v);   // hi + lo part of the same head
       }
-    if (row0 + kTileRows > r1) {
+    if (row0 + kTileRows > r1) {             // ragged tail: rows past the split
 #pragma unroll
       for (int k = 0; k < 8; ++k)
         if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) >= r1) x[k] = -INFINITY;
@@ -460,10 +656,9 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     float mt = x[0];
 #pragma unroll
     for (int k = 1; k < 8; ++k) mt = fmaxf(mt, x[k]);
-    mt = fmaxf(mt, __shfl_xor(mt, 16, 64));
-    mt = fmaxf(mt, __shfl_xor(mt, 32, 64));
+    mt = max_over_rows(mt);
     const float m_new = fmaxf(m_run, mt);
-    if (__ballot(m_new > m_run) != 0) {
+    if (__ballot(m_new > m_run) != 0) {      // rescale only when a max grew
       const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
       l_run *= alpha;
 #pragma unroll
@@ -499,25 +694,23 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       }
   };
 
-  Tile<DV, NRC> buf[DEPTH];
-#pragma unroll
-  for (int d = 0; d < DEPTH - 1; ++d)
-    if (d < my_tiles) load_tile(buf[d], tile_row(d));
+  // DEPTH-stage register pipeline: tile j+DEPTH-1 is requested before tile
+  // j is consumed.  Every iteration issues the same loads, so the waits the
+  // compiler places are exact; the scheduling barrier keeps each tile's
+  // loads in issue order, so the oldest tile is always the first to land.
   for (int jt = 0; jt < my_tiles; jt += DEPTH) {
 #pragma unroll
     for (int d = 0; d < DEPTH; ++d) {
       const int j = jt + d;
-      if (j < my_tiles) {
-        const int jn = j + DEPTH - 1;
-        if (jn < my_tiles) load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(jn));
-        compute_tile(buf[d], tile_row(j));
-      }
+      if (j >= my_tiles) break;
+      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(buf[d], tile_row(j));
     }
   }
 
   // ---- merge the waves and write this split's partial
-  l_run += __shfl_xor(l_run, 16, 64);
-  l_run += __shfl_xor(l_run, 32, 64);
+  l_run = sum_over_rows(l_run);
 #pragma unroll
   for (int ib = 0; ib < NB; ++ib)
 #pragma unroll
@@ -603,11 +796,10 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
     for (int idx = tid; idx < hpg * (DR / 2); idx += kThreads) {
       const int hl = idx / (DR / 2), i = idx % (DR / 2);
       const float* qrow = qg + ((int64_t)b * p.H + h0 + hl) * W + p.d_c;
-      const double x0 = qrow[2 * i], x1 = qrow[2 * i + 1];
-      const double a = (double)L1 * p.inv_freq[i];
-      const double c = cos(a), sn = sin(a);
-      qr[hl][2 * i] = (float)((x0 * c - x1 * sn) * (double)p.scale_log2);
-      qr[hl][2 * i + 1] = (float)((x0 * sn + x1 * c) * (double)p.scale_log2);
+      double y0, y1;
+      rotate_pair(qrow[2 * i], qrow[2 * i + 1], (double)L1 * p.inv_freq[i], y0, y1);
+      qr[hl][2 * i] = (float)(y0 * (double)p.scale_log2);
+      qr[hl][2 * i + 1] = (float)(y1 * (double)p.scale_log2);
     }
   } else {
     for (int idx = tid; idx < hpg * DV; idx += kThreads) {
@@ -644,16 +836,14 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 #pragma unroll
       for (int h = 0; h < kF32MaxHpg; ++h) sc[h] = 0.f;
       if (valid) {
-        const float* vr = vb + (int64_t)t * DV;
         for (int i = 0; i < DV; ++i) {
-          const float v = vr[i];
+          const float v = vb[tiled_off<float>(t, i, DV)];
 #pragma unroll
           for (int h = 0; h < kF32MaxHpg; ++h)
             if (h < hpg) sc[h] = fmaf(qs[h][i], v, sc[h]);
         }
-        const float* kr = kb + (int64_t)t * DR;
         for (int j = 0; j < DR; ++j) {
-          const float k = kr[j];
+          const float k = kb[tiled_off<float>(t, j, DR)];
 #pragma unroll
           for (int h = 0; h < kF32MaxHpg; ++h)
             if (h < hpg) sc[h] = fmaf(qr[h][j], k, sc[h]);
@@ -679,12 +869,11 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
     if (has) {
       const int nrow = r1 - row0 < 64 ? r1 - row0 : 64;
       for (int t = 0; t < nrow; ++t) {
-        const float* vr = vb + (int64_t)(row0 + t) * DV;
 #pragma unroll
         for (int u = 0; u < 4; ++u) {
           const int i = lane + 64 * u;
           if (i < DV) {
-            const float v = vr[i];
+            const float v = vb[tiled_off<float>(row0 + t, i, DV)];
 #pragma unroll
             for (int h = 0; h < kF32MaxHpg; ++h)
               if (h < hpg) acc[h][u] = fmaf(pb[w][t][h], v, acc[h][u]);
@@ -731,33 +920,43 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 }
 
 // =============================================================== combine
-__global__ void __launch_bounds__(128) combine_kernel(CombineParams p) {
-  __shared__ float wts[GVA_MAX_SPLITS];
-  __shared__ float lse_row;
-  const int row = blockIdx.x;
+// One wave per (b, h) row, lane = output element (up to 4 per lane).  A
+// single pass keeps a running log-sum-exp and rescales the running sum;
+// the split loads do not depend on each other, so they overlap.
+constexpr int kCombineMaxDv = 256;
+
+__global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * kWaves + (threadIdx.x >> 6);
+  if (row >= p.rows) return;
   const float* lp = p.lse_part + (int64_t)row * p.S;
-  if (threadIdx.x == 0) {
-    float mx = -INFINITY;
-    for (int s = 0; s < p.S; ++s) mx = fmaxf(mx, lp[s]);
-    float z = 0.f;
-    if (mx != -INFINITY)
-      for (int s = 0; s < p.S; ++s)
-        if (lp[s] != -INFINITY) z += expf(lp[s] - mx);
-    lse_row = mx == -INFINITY ? -INFINITY : mx + logf(z);
-  }
-  __syncthreads();
-  const float big = lse_row;
-  for (int s = threadIdx.x; s < p.S; s += blockDim.x)
-    wts[s] = (big == -INFINITY || lp[s] == -INFINITY) ? 0.f : expf(lp[s] - big);
-  __syncthreads();
   const float* op = p.o_part + (int64_t)row * p.S * p.d_v;
-  for (int i = threadIdx.x; i < p.d_v; i += blockDim.x) {
-    float o = 0.f;
-    for (int s = 0; s < p.S; ++s)
-      if (wts[s] != 0.f) o = fmaf(wts[s], op[(int64_t)s * p.d_v + i], o);
-    p.o[(int64_t)row * p.d_v + i] = o;
+  float m = -INFINITY, z = 0.f;
+  float acc[4] = {0.f, 0.f, 0.f, 0.f};
+  for (int s = 0; s < p.S; ++s) {
+    const float l = lp[s];
+    float v[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = lane + 64 * u;
+      v[u] = i < p.d_v ? op[(int64_t)s * p.d_v + i] : 0.f;
+    }
+    if (l == -INFINITY) continue;          // an empty split carries no rows
+    const float mn = fmaxf(m, l);
+    const float a = m == -INFINITY ? 0.f : expf(m - mn);
+    const float wgt = expf(l - mn);
+    z = z * a + wgt;
+#pragma unroll
+    for (int u = 0; u < 4; ++u) acc[u] = acc[u] * a + wgt * v[u];
+    m = mn;
   }
-  if (p.lse != nullptr && threadIdx.x == 0) p.lse[row] = big;
+  const float inv = z > 0.f ? 1.f / z : 0.f;
+#pragma unroll
+  for (int u = 0; u < 4; ++u) {
+    const int i = lane + 64 * u;
+    if (i < p.d_v) p.o[(int64_t)row * p.d_v + i] = acc[u] * inv;
+  }
+  if (p.lse != nullptr && lane == 0) p.lse[row] = m == -INFINITY ? -INFINITY : m + logf(z);
 }
 
 // ================================================================== host
@@ -772,11 +971,22 @@ int check_dims(const gva_dims* d) {
   if (!(d->scale >= 0.0) || !isfinite(d->scale)) return GVA_ERR_INVALID_ARG;
   if (d->d_r > 0 && (!(d->rope_base > 0.0) || !isfinite(d->rope_base))) return GVA_ERR_INVALID_ARG;
   if (d->d_c + d->d_r < 1) return GVA_ERR_INVALID_ARG;
-  if (d->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
   return GVA_OK;
 }
 
 size_t elem_size(const gva_dims* d) { return d->dtype == GVA_DTYPE_BF16 ? 2 : 4; }
+
+// The tiled cache layout needs whole layout tiles and whole 16-byte pieces.
+int check_cache_layout(const gva_dims* d) {
+  const int piece = (int)(16 / elem_size(d));
+  if (d->t_max % kLayoutRows != 0) return GVA_ERR_UNSUPPORTED;
+  if (d->d_v % piece != 0 || d->d_r % piece != 0) return GVA_ERR_UNSUPPORTED;
+  if (d->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
+  // buffer offsets are 32-bit; keep headroom for prefetches past the end
+  const double stream_bytes = (double)d->t_max * (double)(d->d_v > d->d_r ? d->d_v : d->d_r) * elem_size(d);
+  if (stream_bytes >= 2147483648.0 - 16777216.0) return GVA_ERR_UNSUPPORTED;
+  return GVA_OK;
+}
 
 void fill_inv_freq(const gva_dims* d, double* out) {
   for (int i = 0; i < kMaxPairs; ++i)
@@ -828,7 +1038,7 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
 
 extern "C" {
 
-int gva_version(void) { return 10000; }
+int gva_version(void) { return 10100; }
 
 const char* gva_status_string(int status) {
   switch (status) {
@@ -851,8 +1061,9 @@ int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const voi
   if (dims->d_r > 0 && (!kr_cache || !kr_new)) return GVA_ERR_INVALID_ARG;
   if (!aligned(v_cache, 16) || !aligned(v_new, 16) || !aligned(seq, 4) || !aligned(pos, 4))
     return GVA_ERR_INVALID_ARG;
-  if (dims->d_r > 0 && (!aligned(kr_cache, 4) || !aligned(kr_new, 4))) return GVA_ERR_INVALID_ARG;
-  if ((dims->d_v * elem_size(dims)) % 16 != 0) return GVA_ERR_UNSUPPORTED;
+  if (dims->d_r > 0 && (!aligned(kr_cache, 16) || !aligned(kr_new, 4))) return GVA_ERR_INVALID_ARG;
+  st = check_cache_layout(dims);
+  if (st != GVA_OK) return st;
   AppendParams p;
   p.v_cache = v_cache;
   p.kr_cache = kr_cache;
@@ -881,9 +1092,10 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const i
   if (st != GVA_OK) return st;
   if (!q || !m || !lens || !q_abs) return GVA_ERR_INVALID_ARG;
   if (dims->d_r > 0 && !q_rot) return GVA_ERR_INVALID_ARG;
-  if (!aligned(q, elem_size(dims)) || !aligned(m, elem_size(dims)) || !aligned(lens, 4) ||
-      !aligned(q_abs, 4) || (q_rot && !aligned(q_rot, 4)))
+  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(lens, 4) || !aligned(q_abs, 16) ||
+      (q_rot && !aligned(q_rot, 4)))
     return GVA_ERR_INVALID_ARG;
+  if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
   AbsorbParams p;
   p.q = q;
   p.m = m;
@@ -898,11 +1110,13 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const i
   p.t_max = dims->t_max;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
-  const dim3 grid(dims->batch * dims->n_heads);
-  if (dims->dtype == GVA_DTYPE_BF16)
-    hipLaunchKernelGGL(absorb_kernel<uint16_t>, grid, dim3(128), 0, s, p);
-  else
-    hipLaunchKernelGGL(absorb_kernel<float>, grid, dim3(128), 0, s, p);
+  if (dims->dtype == GVA_DTYPE_BF16) {
+    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
+    const dim3 grid(dims->n_heads, (dims->batch + 15) / 16);
+    hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(absorb_f32_kernel, dim3(dims->batch * dims->n_heads), dim3(128), 0, s, p);
+  }
   return launch_status();
 }
 
@@ -926,6 +1140,8 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   if (!aligned(v_cache, 16) || !aligned(lens, 4) || !aligned(o_part, 16) || !aligned(lse_part, 4) ||
       (dims->d_r > 0 && !aligned(kr_cache, 16)))
     return GVA_ERR_INVALID_ARG;
+  st = check_cache_layout(dims);
+  if (st != GVA_OK) return st;
 
   const int hpg = dims->n_heads / dims->n_groups;
   const long long n_items = (long long)dims->batch * dims->n_groups * num_splits;
@@ -977,6 +1193,7 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   if (!o_part || !lse_part || !o) return GVA_ERR_INVALID_ARG;
   if (!aligned(o_part, 4) || !aligned(lse_part, 4) || !aligned(o, 4) || (lse && !aligned(lse, 4)))
     return GVA_ERR_INVALID_ARG;
+  if (dims->d_v > kCombineMaxDv) return GVA_ERR_UNSUPPORTED;
   CombineParams p;
   p.o_part = o_part;
   p.lse_part = lse_part;
@@ -985,7 +1202,8 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   p.rows = dims->batch * dims->n_heads;
   p.S = num_splits;
   p.d_v = dims->d_v;
-  hipLaunchKernelGGL(combine_kernel, dim3(p.rows), dim3(128), 0, static_cast<hipStream_t>(stream), p);
+  const dim3 grid((p.rows + kWaves - 1) / kWaves);
+  hipLaunchKernelGGL(combine_kernel, grid, dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
 }
 
@@ -1001,9 +1219,10 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int32_t n_cu) {
   }
   if (max_len <= 0) max_len = dims->t_max;
   const long long streams = (long long)dims->batch * dims->n_groups;
-  // aim for ~4 resident workgroups per CU, but keep each split >= 256 rows
-  long long s = (4LL * n_cu + streams - 1) / streams;
-  const long long max_by_len = (max_len + 255) / 256;
+  // one resident workgroup per CU already streams at close to the HBM
+  // ceiling; more splits only add per-split prologue, merge and partials
+  long long s = (n_cu + streams - 1) / streams;
+  const long long max_by_len = (max_len + 511) / 512;     // keep splits >= 512 rows
   if (s > max_by_len) s = max_by_len;
   if (s < 1) s = 1;
   if (s > GVA_MAX_SPLITS) s = GVA_MAX_SPLITS;

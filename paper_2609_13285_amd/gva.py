@@ -188,6 +188,28 @@ def gva_version() -> int:
     return int(lib().gva_version())
 
 
+def tiled(x: torch.Tensor) -> torch.Tensor:
+    """A row-major cache [..., T, D] rearranged into the library's tiled
+    layout (same shape and dtype): tiles of 16 rows, inside a tile the
+    16-byte row pieces ordered piece-major (include/gva.h).  Storage
+    plumbing for callers that fill a cache themselves instead of through
+    gva_append_kv."""
+    *lead, T, D = x.shape
+    P = 16 // x.element_size()
+    if T % 16 or D % P:
+        raise ValueError(f"tiled layout needs T % 16 == 0 and D % {P} == 0")
+    y = x.reshape(*lead, T // 16, 16, D // P, P).transpose(-3, -2).contiguous()
+    return y.reshape(*lead, T, D)
+
+
+def untiled(y: torch.Tensor) -> torch.Tensor:
+    """Inverse of :func:`tiled`: the row-major view of a tiled cache."""
+    *lead, T, D = y.shape
+    P = 16 // y.element_size()
+    x = y.reshape(*lead, T // 16, D // P, 16, P).transpose(-3, -2).contiguous()
+    return x.reshape(*lead, T, D)
+
+
 class DecodeBuffers:
     """Device buffers for one decode step's split partials and outputs."""
 

@@ -27,7 +27,11 @@ def dims_of(w: gva_inputs.Workload) -> gva.GvaDims:
 
 
 def upload(inp: Dict[str, torch.Tensor]) -> Dict[str, torch.Tensor]:
-    return {k: v.cuda() for k, v in inp.items()}
+    """Copy the inputs to the GPU; the caches go in the library's tiled layout."""
+    out = {}
+    for k, v in inp.items():
+        out[k] = gva.tiled(v).cuda() if k in ("v", "kr", "k_gqa") else v.cuda()
+    return out
 
 
 def run_decode(w, dev: Dict[str, torch.Tensor], S: int, fused: bool = True, lens=None):

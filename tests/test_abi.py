@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = gva.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert gva.gva_version() == 10000
+    assert gva.gva_version() == 10100
 
 
 def test_status_strings():
@@ -97,6 +97,8 @@ def test_unsupported_shapes_reported():
     assert decode_status(dims(n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED  # H/G = 16
     assert decode_status(dims(dtype="f32", d_v=512)) == gva.GVA_ERR_UNSUPPORTED
     assert decode_status(dims(d_r=66)) == gva.GVA_ERR_UNSUPPORTED           # > 32 RoPE pairs
+    assert decode_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED         # tiled layout: T % 16
+    assert decode_status(dims(dtype="f32", d_r=6)) == gva.GVA_ERR_UNSUPPORTED  # fp32 pieces of 4
 
 
 def test_append_validation():
@@ -126,4 +128,19 @@ def test_pick_splits_is_host_only_and_bounded():
     assert 1 <= s <= gva.GVA_MAX_SPLITS
     assert gva.gva_pick_splits(d, 100, 256) == 1          # short sequences: no split
     d3 = dims(batch=4, n_heads=32, n_groups=8, t_max=131072, d_r=32)
-    assert gva.gva_pick_splits(d3, 131072, 256) >= 16     # few streams: many splits
+    assert gva.gva_pick_splits(d3, 131072, 256) >= 8      # few streams: many splits
+
+
+def test_tiled_layout_matches_header_formula():
+    import torch
+    for dtype, P in ((torch.bfloat16, 8), (torch.float32, 4)):
+        T, D = 48, 24
+        x = torch.arange(T * D, dtype=torch.float32).reshape(T, D).to(dtype)
+        y = gva.tiled(x).reshape(-1)
+        for t in range(T):
+            for i in range(D):
+                off = (t // 16) * 16 * D + ((i // P) * 16 + t % 16) * P + i % P
+                assert y[off] == x[t, i]
+        assert torch.equal(gva.untiled(gva.tiled(x)), x)
+    z = torch.randn(2, 3, 32, 16).to(torch.bfloat16)
+    assert torch.equal(gva.untiled(gva.tiled(z)), z)
