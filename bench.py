@@ -12,7 +12,7 @@ q read once, new rows read+written once, fp32 output written once) divided
 by the measured step time.
 
   python bench.py [--steps K] [--warmup W] [--workload b32_t8k] [--splits S]
-                  [--unfused] [--no-cpu-baseline] [--copy-calibration MB]
+                  [--absorb auto|fused|separate] [--no-cpu-baseline]
 """
 
 from __future__ import annotations
@@ -69,6 +69,43 @@ def copy_calibration(mb: int, reps: int = 5):
     print(json.dumps({"copy_calibration_bytes": n * 4, "reps": reps}))
 
 
+def _pmc_means(csv_path: str, counter: str):
+    """Mean of one counter per kernel name in a rocprofv3 counter CSV."""
+    import csv
+    acc = {}
+    with open(csv_path) as f:
+        for r in csv.DictReader(f):
+            if r["Counter_Name"] != counter:
+                continue
+            acc.setdefault(r["Kernel_Name"], []).append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}
+
+
+def write_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload, splits, copy_mb):
+    """HBM bytes per decode launch from FETCH_SIZE / WRITE_SIZE, each scaled
+    by what the same counter reads for a plain device copy of known size."""
+    def pick(means, key):
+        hits = [v for k, v in means.items() if key in k]
+        if not hits:
+            raise SystemExit(f"no {key} dispatch in the counter file")
+        return hits[0]
+    copy_bytes = copy_mb * (1 << 20)
+    f_copy = pick(_pmc_means(copy_fetch_csv, "FETCH_SIZE"), "copyBuffer")
+    w_copy = pick(_pmc_means(copy_write_csv, "WRITE_SIZE"), "copyBuffer")
+    f_dec = pick(_pmc_means(fetch_csv, "FETCH_SIZE"), "decode_bf16_kernel")
+    w_dec = pick(_pmc_means(write_csv, "WRITE_SIZE"), "decode_bf16_kernel")
+    rec = {"workload": workload, "num_splits": splits, "kernel_sha": kernel_sha(),
+           "fetch_scale_bytes_per_unit": copy_bytes / f_copy,
+           "write_scale_bytes_per_unit": copy_bytes / w_copy,
+           "fetch_bytes_per_launch": f_dec * copy_bytes / f_copy,
+           "write_bytes_per_launch": w_dec * copy_bytes / w_copy}
+    rec["hbm_bytes_per_launch"] = round(rec["fetch_bytes_per_launch"] + rec["write_bytes_per_launch"])
+    os.makedirs(os.path.dirname(TRAFFIC_FILE), exist_ok=True)
+    with open(TRAFFIC_FILE, "w") as f:
+        json.dump(rec, f, indent=1)
+    print(json.dumps(rec))
+
+
 def cpu_baseline(w, inp, seq, pos, budget_s: float = 20.0):
     """The fp64 oracle on the host cores, on a bounded sample of sequences."""
     import oracle
@@ -105,10 +142,18 @@ def main():
     ap.add_argument("--workload", default="b32_t8k", choices=sorted(gva_inputs.WORKLOADS))
     ap.add_argument("--splits", type=int, default=0)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--unfused", action="store_true", help="run gva_absorb_query as its own kernel")
+    ap.add_argument("--absorb", choices=("auto", "fused", "separate"), default="auto",
+                    help="absorb the query inside the attention kernel (fused) or in its own "
+                         "gva_absorb_query launch (separate); auto picks by split count")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--copy-calibration", type=int, default=0, metavar="MB")
+    ap.add_argument("--write-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
+                    "COPY_WRITE_CSV"), help="summarise rocprofv3 --pmc CSVs into the traffic record")
+    ap.add_argument("--copy-mb", type=int, default=1024)
     args = ap.parse_args()
+    if args.write_traffic:
+        write_traffic(*args.write_traffic, args.workload, args.splits or 1, args.copy_mb)
+        return
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -129,7 +174,7 @@ def main():
     d = gva.make_dims(w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, w.t_max, w.dtype,
                       w.rope_base)
     max_len = int(inp["lens"].max())
-    S = args.splits or gva.gva_pick_splits(d, max_len)
+    S = args.splits or gva.splits_for(d, inp["lens"])
     dev = {k: inp[k].cuda() for k in ("q", "m", "lens", "v_new", "kr_new")}
     dev["v"] = gva.tiled(inp["v"]).cuda()          # the library's cache layout
     dev["kr"] = gva.tiled(inp["kr"]).cuda()
@@ -137,7 +182,7 @@ def main():
     pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
     seq_d, pos_d = seq.cuda(), pos.cuda()
     bufs = gva.DecodeBuffers(d, S)
-    fused = not args.unfused
+    fused = gva.prefer_fused(S) if args.absorb == "auto" else args.absorb == "fused"
     q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
     q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
@@ -157,7 +202,8 @@ def main():
                                      q_rot=q_rot if w.d_r > 0 else None, stream=stream)
         if ev_b is not None:
             ev_b.record(stream)
-        gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
+        if S > 1:   # with one split the attention kernel's partial is the output
+            gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
     for _ in range(args.warmup):
         step()
@@ -227,7 +273,7 @@ def main():
     }
 
     if not args.no_cpu_baseline:
-        o_gpu = bufs.o.cpu()
+        o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
         rec, o_ref = cpu_baseline(w, inp, seq, pos)
         errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]
         rec["max_abs_err_vs_gpu"] = max(errs) if errs else None

@@ -167,11 +167,13 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
                 int32_t num_splits, float* o, float* lse, void* stream);
 
 /*
- * gva_pick_splits -- host heuristic: a num_splits for sequences of up to
- * max_len rows on a device with n_cu compute units (0 = query device 0's).
- * Pure host code; enqueues nothing.  Returns a value in [1, GVA_MAX_SPLITS].
+ * gva_pick_splits -- host heuristic: a num_splits for a batch whose longest
+ * sequence has max_len rows and whose lengths sum to total_len (0 = unknown:
+ * every sequence taken as max_len), on a device with n_cu compute units
+ * (0 = ask the current device).  Pure host code; enqueues nothing.  Returns
+ * a value in [1, GVA_MAX_SPLITS].
  */
-int gva_pick_splits(const gva_dims* dims, int32_t max_len, int32_t n_cu);
+int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu);
 
 /* Human-readable name of a gva_status value (static storage). */
 const char* gva_status_string(int status);

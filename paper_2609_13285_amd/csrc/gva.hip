@@ -1207,7 +1207,7 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   return launch_status();
 }
 
-int gva_pick_splits(const gva_dims* dims, int32_t max_len, int32_t n_cu) {
+int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu) {
   if (check_dims(dims) != GVA_OK) return 1;
   if (n_cu <= 0) {
     int dev = 0, cu = 0;
@@ -1217,13 +1217,20 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int32_t n_cu) {
     else
       n_cu = 256;
   }
-  if (max_len <= 0) max_len = dims->t_max;
+  if (max_len <= 0 || max_len > dims->t_max) max_len = dims->t_max;
   const long long streams = (long long)dims->batch * dims->n_groups;
-  // one resident workgroup per CU already streams at close to the HBM
-  // ceiling; more splits only add per-split prologue, merge and partials
+  if (total_len <= 0) total_len = (long long)dims->batch * max_len;
+  // One resident workgroup per CU already streams close to the HBM
+  // ceiling, and every split adds a fixed prologue/merge cost of a few
+  // microseconds, so: enough splits to give each CU one workgroup, but no
+  // split shorter than ~1 MB of value rows.
   long long s = (n_cu + streams - 1) / streams;
-  const long long max_by_len = (max_len + 511) / 512;     // keep splits >= 512 rows
-  if (s > max_by_len) s = max_by_len;
+  const long long row_bytes = (long long)dims->d_v * (long long)elem_size(dims);
+  const long long max_by_bytes = ((long long)max_len * row_bytes + (1 << 20) - 1) >> 20;
+  if (s > max_by_bytes) s = max_by_bytes;
+  // Lengths spread widely (mean below half the longest): the longest
+  // sequences set the tail, so cut them finer.
+  if (2 * total_len < (long long)dims->batch * max_len) s *= 2;
   if (s < 1) s = 1;
   if (s > GVA_MAX_SPLITS) s = GVA_MAX_SPLITS;
   return (int)s;

@@ -61,7 +61,7 @@ def lib() -> ctypes.CDLL:
         L.gva_absorb_query.argtypes = [D, P, P, P, P, P, P]
         L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
-        L.gva_pick_splits.argtypes = [D, I32, I32]
+        L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
@@ -180,8 +180,21 @@ def gva_combine(dims: GvaDims, o_part, lse_part, num_splits: int, o, lse=None, s
     _check("gva_combine", st)
 
 
-def gva_pick_splits(dims: GvaDims, max_len: int = 0, n_cu: int = 0) -> int:
-    return int(lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(n_cu)))
+def gva_pick_splits(dims: GvaDims, max_len: int = 0, total_len: int = 0, n_cu: int = 0) -> int:
+    return int(lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(total_len), int(n_cu)))
+
+
+def splits_for(dims: GvaDims, lens: torch.Tensor, n_cu: int = 0) -> int:
+    """gva_pick_splits for the lengths in ``lens`` (host copy)."""
+    L = lens.detach().to("cpu", torch.int64).clamp(0, dims.t_max)
+    return gva_pick_splits(dims, int(L.max()) if L.numel() else 0, int(L.sum()), n_cu)
+
+
+def prefer_fused(num_splits: int) -> bool:
+    """Fuse the absorption into the attention kernel when each (sequence,
+    group) has at most two splits; with more splits every workgroup would
+    redo the absorption, so a separate absorb launch is cheaper."""
+    return int(num_splits) <= 2
 
 
 def gva_version() -> int:
@@ -223,7 +236,7 @@ class DecodeBuffers:
 
 
 def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
-           bufs: Optional[DecodeBuffers] = None, fused: bool = True,
+           bufs: Optional[DecodeBuffers] = None, fused: Optional[bool] = None,
            stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Absorb + attention + combine for one step; returns (o, lse) fp32.
 
@@ -231,6 +244,8 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
     gva_absorb_query runs first and the attention kernel reads its output.
     """
     S = int(num_splits)
+    if fused is None:
+        fused = prefer_fused(S)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
     if fused:
@@ -242,5 +257,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
         gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
                              q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream)
+    if S == 1:   # a single split's partial is already the final result
+        return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
     return bufs.o, bufs.lse

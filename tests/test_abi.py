@@ -124,11 +124,17 @@ def test_absorb_validation():
 
 def test_pick_splits_is_host_only_and_bounded():
     d = dims(batch=32, n_heads=32, n_groups=8, t_max=8192)
-    s = gva.gva_pick_splits(d, 8192, 256)
-    assert 1 <= s <= gva.GVA_MAX_SPLITS
-    assert gva.gva_pick_splits(d, 100, 256) == 1          # short sequences: no split
+    assert gva.gva_pick_splits(d, 8192, 0, 256) == 1       # 256 streams fill 256 CUs
+    assert gva.gva_pick_splits(d, 100, 0, 256) == 1        # short sequences: no split
     d3 = dims(batch=4, n_heads=32, n_groups=8, t_max=131072, d_r=32)
-    assert gva.gva_pick_splits(d3, 131072, 256) >= 8      # few streams: many splits
+    assert gva.gva_pick_splits(d3, 131072, 0, 256) == 8    # few long streams
+    d4 = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
+    even = gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)
+    spread = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256)
+    assert spread == 2 * even                              # widely spread lengths
+    for S in (even, spread):
+        assert 1 <= S <= gva.GVA_MAX_SPLITS
+    assert not gva.prefer_fused(4) and gva.prefer_fused(1)
 
 
 def test_tiled_layout_matches_header_formula():

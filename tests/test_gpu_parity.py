@@ -43,7 +43,7 @@ def test_decode_matches_oracle(name, seed, fused):
     o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
                                    rope_base=w.rope_base)
     dev = upload(inp)
-    S = gva.gva_pick_splits(dims_of(w), w.t_max)
+    S = gva.splits_for(dims_of(w), inp["lens"])
     for splits in sorted({1, 3, S}):
         note(f"{name} seed={seed} fused={fused} S={splits}")
         o, lse, _, _ = run_decode(w, dev, splits, fused=fused)
@@ -254,7 +254,7 @@ def test_full_size_sampled(name):
     note(f"{name}: drawing inputs")
     inp = gva_inputs.make_inputs(w, 0)
     d = dims_of(w)
-    S = gva.gva_pick_splits(d, int(inp["lens"].max()))
+    S = gva.splits_for(d, inp["lens"])
     dev = upload({k: inp[k] for k in ("q", "m", "v", "kr", "lens")})
     note(f"{name}: decode S={S}")
     o, lse, _, _ = run_decode(w, dev, S)

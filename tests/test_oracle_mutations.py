@@ -1,0 +1,66 @@
+"""Plant plausible mistakes in a copy of the oracle's C source (on the CPU)
+and check that the pins catch every one of them."""
+
+import ctypes
+import os
+import subprocess
+
+import pytest
+
+import oracle
+import test_oracle_pins as pins
+
+SRC = oracle._SRC
+
+# (name, original text, mutated text)
+MUTANTS = [
+    ("rotation sign", "y[2 * i] = x0 * c - x1 * s;", "y[2 * i] = x0 * c + x1 * s;"),
+    ("transposed M", "ld(m, ((int64_t)h * d_v + i) * d_c + k, dt_m)",
+     "ld(m, ((int64_t)h * d_c + k) * d_v + i, dt_m)"),
+    ("dropped positional term", "s[t] = scale * (content + positional);", "s[t] = scale * content;"),
+    ("scale without d_r", "scale = 1.0 / sqrt((double)(d_c + d_r));", "scale = 1.0 / sqrt((double)d_c);"),
+    ("group map", "const int b = bh / H, h = bh % H, g = h / hpg;\n    int L = lens[b];\n    if (L < 0) L = 0;\n    if (L > T_max) L = T_max;\n    int t0",
+     "const int b = bh / H, h = bh % H, g = h % G;\n    int L = lens[b];\n    if (L < 0) L = 0;\n    if (L > T_max) L = T_max;\n    int t0"),
+    ("query position", "const int64_t p = L > 0 ? L - 1 : 0;", "const int64_t p = L;"),
+    ("combine weight", "double w = exp(x - big);", "double w = exp(x - mx);"),
+    ("double rounding", "double n = nearbyint(scaled);", "double n = nearbyint((double)(float)scaled);"),
+    ("last row dropped", "for (int t = 0; t < n; ++t) {\n      double w", "for (int t = 0; t < n - 1; ++t) {\n      double w"),
+]
+
+PIN_TESTS = [
+    lambda o: pins.test_absorbed_matches_explicit_reconstruction(o, 8, 4, 2),
+    lambda o: pins.test_absorbed_matches_explicit_reconstruction(o, 4, 6, 3),
+    lambda o: pins.test_absorbed_query_is_q_times_m_transpose(o),
+    lambda o: pins.test_weights_sum_to_one_and_match_softmax(o),
+    lambda o: pins.test_two_rows_closed_form(o),
+    lambda o: pins.test_rope_matches_complex_form_and_invariants(o),
+    lambda o: pins.test_position_shift_leaves_output_unchanged(o),
+    lambda o: pins.test_split_and_combine_equals_unsplit(o, 3),
+    lambda o: pins.test_round_bf16_single_rounding(o),
+    lambda o: pins.test_zero_query_gives_mean_value(o),
+]
+
+
+@pytest.mark.parametrize("name,orig,mut", MUTANTS, ids=[m[0] for m in MUTANTS])
+def test_every_planted_mistake_fails_a_pin(tmp_path, monkeypatch, name, orig, mut):
+    text = open(SRC).read()
+    assert orig in text, f"mutation site for {name!r} not found"
+    src = tmp_path / "mutant.c"
+    src.write_text(text.replace(orig, mut, 1))
+    so = tmp_path / "libmutant.so"
+    subprocess.run(["gcc", "-O1", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-o", str(so),
+                    str(src), "-lm"], check=True)
+    saved = oracle._lib
+    monkeypatch.setattr(oracle, "LIB_PATH", str(so))
+    oracle._lib = None
+    try:
+        oracle._load()
+        caught = []
+        for pin in PIN_TESTS:
+            try:
+                pin(oracle)
+            except AssertionError:
+                caught.append(pin)
+        assert caught, f"no pin catches the mutant {name!r}"
+    finally:
+        oracle._lib = saved
