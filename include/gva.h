@@ -143,6 +143,15 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
  * kernel absorbs and rotates it itself ahead of the attention loop (the
  * fused path) -- or pre-absorbed by gva_absorb_query: q/m NULL, q_abs
  * [B][H][d_v] fp32 and (if d_r > 0) q_rot [B][H][d_r] fp32 non-NULL.
+ * The current token, appended and attended in one launch (optional):
+ * v_new [B][G][d_v] and kr_new [B][d_r] (unrotated, storage dtype, as for
+ * gva_append_kv) are the rows of position lens[b]-1 of every sequence with
+ * lens[b] >= 1.  The call then stores them into the caches at that
+ * position exactly as gva_append_kv does (same rotation and rounding) and
+ * attends over them without reading them back, so the result equals
+ * gva_append_kv followed by this call without the new rows.  Pass both
+ * NULL when the caches already hold row lens[b]-1; kr_new may be NULL when
+ * d_r == 0.  v_new 16-byte aligned, kr_new 4-byte aligned.
  * o_part [B][H][S][d_v] fp32, lse_part [B][H][S] fp32.
  * Supported for bf16: d_v in {64, 128}, d_c a multiple of 32 (<= 512),
  * d_r a multiple of 8 (<= 64), H/G in {1, 2, 4, 8}; for fp32: d_v <= 256,
@@ -152,9 +161,9 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
  */
 int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
                          const float* q_abs, const float* q_rot,
-                         const void* v_cache, const void* kr_cache,
-                         const int32_t* lens, int32_t num_splits,
-                         float* o_part, float* lse_part, void* stream);
+                         void* v_cache, void* kr_cache,
+                         const int32_t* lens, const void* v_new, const void* kr_new,
+                         int32_t num_splits, float* o_part, float* lse_part, void* stream);
 
 /*
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):

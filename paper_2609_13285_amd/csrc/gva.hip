@@ -94,11 +94,13 @@ struct DecodeParams {
   const void* m;
   const float* q_abs;     // pre-absorbed path
   const float* q_rot;
-  const void* v;
-  const void* kr;
+  void* v;                                 // caches: read, and row L-1 written when pending
+  void* kr;
   const int32_t* lens;
   float* o_part;
   float* lse_part;
+  const void* v_new;      // optional: the current token's rows, used in place
+  const void* kr_new;     // of cache row len-1 (see gva_decode_attention)
   int32_t B, H, G, d_v, d_c, d_r, t_max, S;
   float scale_log2;       // score scale * log2(e): softmax runs in base 2
   int32_t fused;
@@ -252,6 +254,29 @@ __device__ __forceinline__ bf16x8 split_hi_lo(const float* x, bool lo) {
   return out;
 }
 
+// cos/sin of an fp64 angle, evaluated in fp32 after an exact reduction by
+// multiples of 2 pi in fp64 (Cody-Waite with 2 pi split into two doubles;
+// each fma subtracts an exactly formed product).  Accurate to fp32 rounding
+// for |a| < 2^40, which covers every position times a RoPE frequency <= 1.
+__device__ __forceinline__ void sincos_reduced(double a, float& s, float& c) {
+  constexpr double kInv2Pi = 0.15915494309189533577;
+  constexpr double k2PiHi = 6.28318530717958623200;    // 2 pi rounded to double
+  constexpr double k2PiLo = 2.44929359829470635445e-16; // 2 pi - k2PiHi
+  const double k = rint(a * kInv2Pi);
+  double r = fma(-k, k2PiHi, a);
+  r = fma(-k, k2PiLo, r);
+  sincosf((float)r, &s, &c);
+}
+
+// The query's positional slice, rotated at position pos and scaled: fp32 is
+// all the score needs.
+__device__ __forceinline__ void rotate_query_pair(float x0, float x1, double a, float scale, float& y0, float& y1) {
+  float s, c;
+  sincos_reduced(a, s, c);
+  y0 = (x0 * c - x1 * s) * scale;
+  y1 = (x0 * s + x1 * c) * scale;
+}
+
 __device__ __forceinline__ void rotate_pair(double x0, double x1, double a, double& y0, double& y1) {
   double s, c;
   sincos(a, &s, &c);
@@ -304,41 +329,55 @@ __global__ void __launch_bounds__(256) append_kernel(AppendParams p) {
 // the output blocks ib = w, w+4, ... of q~^T[i][b] = sum_k M_h[i][k] q[b][h][k]
 // (A = rows of M_h, B = the query rows, K = d_c).
 __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
+  constexpr int kMaxChunks = 16;                          // d_c <= 512
   const int h = blockIdx.x;
   const int b0 = blockIdx.y * 16;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, qd = lane >> 4;
   const int W = p.d_c + p.d_r;
+  const int nck = p.d_c / 32;
   const uint16_t* qg = static_cast<const uint16_t*>(p.q);
   const uint16_t* mh = static_cast<const uint16_t*>(p.m) + (int64_t)h * p.d_v * p.d_c;
   const int bq = min(b0 + n, p.B - 1);                  // rows past B compute a duplicate
   const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
+  // the positional pair of this thread, loaded with everything else
+  const int npair = p.d_r / 2;
+  const bool has_pair = tid < 16 * npair && b0 + (npair > 0 ? tid / npair : 0) < p.B;
+  float r0 = 0.f, r1 = 0.f;
+  int pb = 0, pi = 0;
+  if (has_pair) {
+    pb = b0 + tid / npair;
+    pi = tid % npair;
+    const uint32_t two = *reinterpret_cast<const uint32_t*>(qg + ((int64_t)pb * p.H + h) * W + p.d_c + 2 * pi);
+    r0 = bf16_bits_to_f32(two & 0xFFFFu);
+    r1 = bf16_bits_to_f32(two >> 16);
+  }
+  bf16x8 xq[kMaxChunks];
+#pragma unroll
+  for (int c = 0; c < kMaxChunks; ++c)
+    if (c < nck) xq[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
   const int nb = p.d_v / 16;
   for (int ib = w; ib < nb; ib += kWaves) {
+    bf16x8 a[kMaxChunks];
+#pragma unroll
+    for (int c = 0; c < kMaxChunks; ++c)
+      if (c < nck) a[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
     f32x4 acc = {0.f, 0.f, 0.f, 0.f};
-    for (int c = 0; c < p.d_c / 32; ++c) {
-      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
-      const bf16x8 x = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
-      acc = mfma16(a, x, acc);
-    }
+#pragma unroll
+    for (int c = 0; c < kMaxChunks; ++c)
+      if (c < nck) acc = mfma16(a[c], xq[c], acc);
     // lane (n, qd) holds q~[b0 + n][16 ib + 4 qd + jj]
     if (b0 + n < p.B)
       *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(b0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
   }
-  const int npair = p.d_r / 2;
-  for (int idx = tid; idx < 16 * npair; idx += kThreads) {
-    const int bl = idx / npair, i = idx % npair;
-    const int b = b0 + bl;
-    if (b >= p.B) continue;
-    const int L = clamp_len(p.lens, b, p.t_max);
-    const uint16_t* qr = qg + ((int64_t)b * p.H + h) * W + p.d_c;
-    double y0, y1;
-    rotate_pair(bf16_bits_to_f32(qr[2 * i]), bf16_bits_to_f32(qr[2 * i + 1]),
-                (double)(L > 0 ? L - 1 : 0) * p.inv_freq[i], y0, y1);
-    float* out = p.q_rot + ((int64_t)b * p.H + h) * p.d_r + 2 * i;
-    out[0] = (float)y0;
-    out[1] = (float)y1;
+  if (has_pair) {
+    const int L = clamp_len(p.lens, pb, p.t_max);
+    float y0, y1;
+    rotate_query_pair(r0, r1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pi], 1.f, y0, y1);
+    float* out = p.q_rot + ((int64_t)pb * p.H + h) * p.d_r + 2 * pi;
+    out[0] = y0;
+    out[1] = y1;
   }
 }
 
@@ -370,8 +409,10 @@ template <int HPG, int DV, int NRC>
 struct DecodeCfg {
   static constexpr int NC = DV / 32;                         // K-chunks per V row
   static constexpr int NB = DV / 16;                         // 16-wide i-blocks of the output
-  static constexpr int DEPTH = DV >= 128 ? 3 : 4;
-  static constexpr int CR = 16 / NB;                         // d_c chunks per absorption round
+  static constexpr int DEPTH = DV >= 128 ? 2 : 3;
+  // d_c chunks per absorption round: one round of 32 loads where the
+  // registers allow it (no spills), else rounds of 16
+  static constexpr int CR = ((DV >= 128 && NRC < 2 && HPG <= 4) ? 32 : 16) / NB;
   static constexpr int QS_STRIDE = DV + 4;                   // padded LDS rows (floats)
   static constexpr int QR_STRIDE = 32 * NRC + 4;
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
@@ -389,7 +430,7 @@ template <int HPG, int DV, int NRC>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
   using Cfg = DecodeCfg<HPG, DV, NRC>;
   constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
-  __shared__ float lds[Cfg::LDS_FLOATS];
+  __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
   const int item = xcd_remap(blockIdx.x, gridDim.x);
   const int g = item % p.G;
@@ -403,6 +444,10 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int L = clamp_len(p.lens, b, p.t_max);
   int r0, r1;
   split_rows(L, p.S, s, r0, r1);
+  // With the current token's rows given, the split holding row L-1 takes
+  // that row from them and streams only the rows before it from the cache.
+  const bool pending = p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
+  if (pending) r1 = L - 1;
   const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
 
   // Column roles: [hi_0 .. hi_{HPG-1}, lo_{HPG-1} .. lo_0, zero padding].
@@ -449,6 +494,20 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     }
   };
   Tile<DV, NRC> buf[DEPTH];
+
+  // The pending row's raw values: one 16-byte value piece per thread of the
+  // first DV/8 threads, one positional pair per thread of the first d_r/2.
+  u32x4 pend_piece = {0u, 0u, 0u, 0u};
+  float pend_k0 = 0.f, pend_k1 = 0.f;
+  if (pending) {
+    if (tid < DV / 8)
+      pend_piece = *(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.v_new) + ((int64_t)b * p.G + g) * DV) + tid);
+    if (tid < p.d_r / 2) {
+      const uint32_t two = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(p.kr_new) + (int64_t)b * p.d_r + 2 * tid);
+      pend_k0 = bf16_bits_to_f32(two & 0xFFFFu);
+      pend_k1 = bf16_bits_to_f32(two >> 16);
+    }
+  }
 
   // ---- prologue: absorbed, rotated, scaled queries as MFMA B operands.
   // The query loads are issued before the V prefetch: loads retire in order,
@@ -571,15 +630,18 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
         __builtin_amdgcn_sched_barrier(0);
       }
     }
-    // rotate the positional query at position L-1 (fp64 angle)
-    for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads)
-      qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + idx % (32 * NRC)] = 0.f;
-    __syncthreads();
+    // rotate the positional query at position L-1 (fp64 angle, reduced
+    // exactly, fp32 rotation); the padding past d_r is written as zeros in
+    // the same phase, so one barrier covers both
     if (has_pair) {
-      double y0, y1;
-      rotate_pair(rq0, rq1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], y0, y1);
-      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i] = (float)(y0 * (double)p.scale_log2);
-      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = (float)(y1 * (double)p.scale_log2);
+      float y0, y1;
+      rotate_query_pair(rq0, rq1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], p.scale_log2, y0, y1);
+      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i] = y0;
+      qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = y1;
+    }
+    for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads) {
+      const int j = idx % (32 * NRC);
+      if (j >= p.d_r) qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + j] = 0.f;
     }
     __syncthreads();
     const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
@@ -619,11 +681,11 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 
-  auto compute_tile = [&](Tile<DV, NRC>& t, int row0) {
-    if (row0 + kTileRows > r1) {             // ragged tail: clear rows past the split
+  auto compute_tile = [&](Tile<DV, NRC>& t, int row0, int row_end) {
+    if (row0 + kTileRows > row_end) {        // ragged tail: clear rows past the end
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
-        const bool dead = row0 + 16 * hf + n >= r1;
+        const bool dead = row0 + 16 * hf + n >= row_end;
 #pragma unroll
         for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
 #pragma unroll
@@ -648,10 +710,10 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
         const float v = sc[hf][jj];
         x[4 * hf + jj] = v + mirror<HPG>(v);   // hi + lo part of the same head
       }
-    if (row0 + kTileRows > r1) {             // ragged tail: rows past the split
+    if (row0 + kTileRows > row_end) {        // ragged tail: rows past the end
 #pragma unroll
       for (int k = 0; k < 8; ++k)
-        if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) >= r1) x[k] = -INFINITY;
+        if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) >= row_end) x[k] = -INFINITY;
     }
     float mt = x[0];
 #pragma unroll
@@ -705,7 +767,56 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       if (j >= my_tiles) break;
       load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
       __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], tile_row(j));
+      compute_tile(buf[d], tile_row(j), r1);
+    }
+  }
+
+  // ---- the pending row (current token): staged through LDS, then wave 0
+  // scores it as a one-row tile, exactly as if it had been read from the
+  // cache after gva_append_kv (same rotation and rounding)
+  if (pending) {
+    __syncthreads();                        // prologue LDS no longer needed
+    uint16_t* prow = reinterpret_cast<uint16_t*>(lds);          // [DV] value, then [32*NRC] key
+    // the append: this workgroup is the only reader of row L-1 of stream
+    // (b, g) in this launch, so it also stores the row into the caches (the
+    // shared positional key once, by group 0)
+    uint16_t* vcache = static_cast<uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+    uint16_t* kcache = static_cast<uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+    if (tid < DV / 8) {
+      *(reinterpret_cast<u32x4*>(prow) + tid) = pend_piece;
+      *reinterpret_cast<u32x4*>(vcache + tiled_off<uint16_t>(L - 1, 8 * tid, DV)) = pend_piece;
+    }
+    for (int idx = tid; idx < 16 * NRC; idx += kThreads) {
+      uint16_t y0b = 0, y1b = 0;
+      if (idx < p.d_r / 2) {
+        double y0, y1;
+        rotate_pair(pend_k0, pend_k1, (double)(L - 1) * p.inv_freq[idx], y0, y1);
+        y0b = f64_to_bf16_rne(y0);
+        y1b = f64_to_bf16_rne(y1);
+        if (g == 0) {
+          const int64_t o = tiled_off<uint16_t>(L - 1, 2 * idx, p.d_r);
+          kcache[o] = y0b;
+          kcache[o + 1] = y1b;
+        }
+      }
+      prow[DV + 2 * idx] = y0b;
+      prow[DV + 2 * idx + 1] = y1b;
+    }
+    __syncthreads();
+    if (w == 0) {
+      Tile<DV, NRC> t;
+      const u32x4* pv = reinterpret_cast<const u32x4*>(prow);
+#pragma unroll
+      for (int c = 0; c < NC; ++c) {
+        t.v[0][c] = n == 0 ? as_bf16x8(pv[4 * c + qd]) : zero8;
+        t.v[1][c] = zero8;
+      }
+#pragma unroll
+      for (int rc = 0; rc < NRC; ++rc) {
+        t.k[0][rc] = n == 0 ? as_bf16x8(pv[DV / 8 + 4 * rc + qd]) : zero8;
+        t.k[1][rc] = zero8;
+      }
+      compute_tile(t, L - 1, L);
     }
   }
 
@@ -779,6 +890,8 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
   const int L = clamp_len(p.lens, b, p.t_max);
   int r0, r1;
   split_rows(L, p.S, s, r0, r1);
+  const bool pending = p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
+  if (pending) r1 = L - 1;
 
   if (p.fused) {
     const float* qg = static_cast<const float*>(p.q);
@@ -882,6 +995,47 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
       }
     }
     __syncthreads();
+  }
+
+  // the pending row (current token), taken from v_new / kr_new with the
+  // rotation and rounding gva_append_kv would store, added by wave 0
+  if (pending && w == 0) {
+    const float* vn = static_cast<const float*>(p.v_new) + ((int64_t)b * p.G + g) * DV;
+    float vv[4];
+#pragma unroll
+    for (int u = 0; u < 4; ++u) vv[u] = lane + 64 * u < DV ? vn[lane + 64 * u] : 0.f;
+    float kk = 0.f;
+    if (lane < DR) {
+      const float* kn = static_cast<const float*>(p.kr_new) + (int64_t)b * DR;
+      double y0, y1;
+      const int pi = lane / 2;
+      rotate_pair(kn[2 * pi], kn[2 * pi + 1], (double)(L - 1) * p.inv_freq[pi], y0, y1);
+      kk = (float)((lane & 1) ? y1 : y0);
+    }
+    // the append of row L-1 (this wave is its only reader in this launch)
+    float* vcache = static_cast<float*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+#pragma unroll
+    for (int u = 0; u < 4; ++u)
+      if (lane + 64 * u < DV) vcache[tiled_off<float>(L - 1, lane + 64 * u, DV)] = vv[u];
+    if (g == 0 && lane < DR)
+      (static_cast<float*>(p.kr) + (int64_t)b * p.t_max * DR)[tiled_off<float>(L - 1, lane, DR)] = kk;
+#pragma unroll
+    for (int h = 0; h < kF32MaxHpg; ++h) {
+      if (h < hpg) {
+        float part = lane < DR ? qr[h][lane] * kk : 0.f;
+#pragma unroll
+        for (int u = 0; u < 4; ++u)
+          if (lane + 64 * u < DV) part = fmaf(qs[h][lane + 64 * u], vv[u], part);
+        const float x = wave_sum(part);
+        const float m_new = fmaxf(m_run[h], x);
+        const float alpha = __builtin_amdgcn_exp2f(m_run[h] - m_new);
+        const float pr = __builtin_amdgcn_exp2f(x - m_new);
+        l_run[h] = l_run[h] * alpha + pr;
+#pragma unroll
+        for (int u = 0; u < 4; ++u) acc[h][u] = acc[h][u] * alpha + pr * vv[u];
+        m_run[h] = m_new;
+      }
+    }
   }
 
 #pragma unroll
@@ -1038,7 +1192,7 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
 
 extern "C" {
 
-int gva_version(void) { return 10100; }
+int gva_version(void) { return 10200; }
 
 const char* gva_status_string(int status) {
   switch (status) {
@@ -1121,9 +1275,9 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const i
 }
 
 int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, const float* q_abs,
-                         const float* q_rot, const void* v_cache, const void* kr_cache,
-                         const int32_t* lens, int32_t num_splits, float* o_part, float* lse_part,
-                         void* stream) {
+                         const float* q_rot, void* v_cache, void* kr_cache,
+                         const int32_t* lens, const void* v_new, const void* kr_new,
+                         int32_t num_splits, float* o_part, float* lse_part, void* stream) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
@@ -1139,6 +1293,9 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   if (dims->d_r > 0 && !kr_cache) return GVA_ERR_INVALID_ARG;
   if (!aligned(v_cache, 16) || !aligned(lens, 4) || !aligned(o_part, 16) || !aligned(lse_part, 4) ||
       (dims->d_r > 0 && !aligned(kr_cache, 16)))
+    return GVA_ERR_INVALID_ARG;
+  if (!v_new && kr_new) return GVA_ERR_INVALID_ARG;          // the pending row comes whole
+  if (v_new && (!aligned(v_new, 16) || (dims->d_r > 0 && (!kr_new || !aligned(kr_new, 4)))))
     return GVA_ERR_INVALID_ARG;
   st = check_cache_layout(dims);
   if (st != GVA_OK) return st;
@@ -1157,6 +1314,8 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   p.lens = lens;
   p.o_part = o_part;
   p.lse_part = lse_part;
+  p.v_new = v_new;
+  p.kr_new = kr_new;
   p.B = dims->batch;
   p.H = dims->n_heads;
   p.G = dims->n_groups;

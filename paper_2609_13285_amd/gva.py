@@ -59,7 +59,7 @@ def lib() -> ctypes.CDLL:
         D = ctypes.POINTER(GvaDims)
         L.gva_append_kv.argtypes = [D, P, P, P, P, P, P, I32, P]
         L.gva_absorb_query.argtypes = [D, P, P, P, P, P, P]
-        L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, I32, P, P, P]
+        L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
         L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32]
         L.gva_status_string.argtypes = [ctypes.c_int]
@@ -146,7 +146,8 @@ def gva_absorb_query(dims: GvaDims, q, m, lens, q_abs, q_rot, stream=None):
 
 
 def gva_decode_attention(dims: GvaDims, v_cache, kr_cache, lens, num_splits: int, o_part, lse_part,
-                         q=None, m=None, q_abs=None, q_rot=None, stream=None):
+                         q=None, m=None, q_abs=None, q_rot=None, v_new=None, kr_new=None,
+                         stream=None):
     d = dims
     dt = d.torch_dtype
     S = int(num_splits)
@@ -159,6 +160,8 @@ def gva_decode_attention(dims: GvaDims, v_cache, kr_cache, lens, num_splits: int
         _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
         _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)),
         _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(v_new, "v_new", dt, (d.batch, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (d.batch, d.d_r)),
         S,
         _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
@@ -237,26 +240,30 @@ class DecodeBuffers:
 
 def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
            bufs: Optional[DecodeBuffers] = None, fused: Optional[bool] = None,
-           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+           v_new=None, kr_new=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Absorb + attention + combine for one step; returns (o, lse) fp32.
 
     ``fused`` runs the absorption inside the attention kernel; otherwise
     gva_absorb_query runs first and the attention kernel reads its output.
+    ``v_new``/``kr_new`` are the current token's rows: the attention call
+    stores them at cache row len-1 (as gva_append_kv would) and attends over
+    them in the same launch.
     """
     S = int(num_splits)
     if fused is None:
         fused = prefer_fused(S)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
+    pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None)
     if fused:
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
-                             q=q, m=m, stream=stream)
+                             q=q, m=m, stream=stream, **pend)
     else:
         q_abs = torch.empty(dims.batch, dims.n_heads, dims.d_v, dtype=torch.float32, device=v_cache.device)
         q_rot = torch.empty(dims.batch, dims.n_heads, dims.d_r, dtype=torch.float32, device=v_cache.device)
         gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
-                             q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream)
+                             q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream, **pend)
     if S == 1:   # a single split's partial is already the final result
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = gva.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert gva.gva_version() == 10100
+    assert gva.gva_version() == 10200
 
 
 def test_status_strings():
@@ -52,8 +52,8 @@ def dims(**kw):
     return gva.make_dims(**base)
 
 
-def decode_status(d, S=4, q=A, m=A, qa=None, qr=None, v=A, kr=A, lens=A, op=A, lp=A):
-    return gva.lib().gva_decode_attention(ctypes.byref(d), q, m, qa, qr, v, kr, lens, S, op, lp, None)
+def decode_status(d, S=4, q=A, m=A, qa=None, qr=None, v=A, kr=A, lens=A, op=A, lp=A, vn=None, kn=None):
+    return gva.lib().gva_decode_attention(ctypes.byref(d), q, m, qa, qr, v, kr, lens, vn, kn, S, op, lp, None)
 
 
 @pytest.mark.parametrize("kw", [
@@ -88,6 +88,10 @@ def test_null_and_misaligned_pointers_rejected():
     assert decode_status(d, q=A, m=None) == gva.GVA_ERR_INVALID_ARG
     assert decode_status(d, qa=A, qr=A) == gva.GVA_ERR_INVALID_ARG
     assert decode_status(d, q=None, m=None, qa=A, qr=None) == gva.GVA_ERR_INVALID_ARG
+    # the current token's row comes whole: value and positional key together
+    assert decode_status(d, vn=None, kn=A) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, vn=A, kn=None) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, vn=A + 4, kn=A) == gva.GVA_ERR_INVALID_ARG
 
 
 def test_unsupported_shapes_reported():

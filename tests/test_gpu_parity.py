@@ -269,3 +269,63 @@ def test_full_size_sampled(name):
     idx = torch.tensor(picks)
     _check(w, o[idx], lse[idx], o_ref, lse_ref, f"{name}/sampled")
     assert torch.isfinite(o).all()
+
+
+# ---------------------------------------------- current token from the step
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+def test_current_token_row_matches_append_then_decode(dtype):
+    # The attention call appends row len-1 from v_new/kr_new and attends over
+    # it without reading it back: the cache's copy of that row is NaN here,
+    # so reading it would poison the output.  After the call the caches hold
+    # exactly what gva_append_kv stores.
+    T = 160
+    w = gva_inputs.Workload("pending", 6, T, 16, 4, 64, 64, 16, dtype=dtype)
+    lens = torch.tensor([T, 1, 33, 64, 97, 2], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 43, lens=lens)
+    B = w.batch
+    seq = torch.arange(B, dtype=torch.int32)
+    pos = (inp["lens"] - 1).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"])
+    itype = torch.int16 if dtype == "bf16" else torch.int32
+    d = dims_of(w)
+    for b in range(B):
+        inp["v"][b, :, int(pos[b])] = float("nan")
+        inp["kr"][b, int(pos[b])] = float("nan")
+    for S in (1, 3):
+        for fused in (True, False):
+            note(f"pending row {dtype} S={S} fused={fused}")
+            dev = upload(inp)
+            o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S,
+                                fused=fused, v_new=dev["v_new"], kr_new=dev["kr_new"])
+            torch.cuda.synchronize()
+            _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"pending/{dtype}/S{S}/fused={fused}")
+            assert torch.equal(gva.untiled(dev["v"].cpu()).view(itype), v_ref.view(itype))
+            assert torch.equal(gva.untiled(dev["kr"].cpu()).view(itype), k_ref.view(itype))
+
+
+def test_append_and_attend_in_one_launch_full_step():
+    # Algorithm 1 as the bench runs it on the 350M-model shape: the attention
+    # call appends the step's rows and attends over them; a repeated step at
+    # the same position leaves the caches unchanged (the append is idempotent).
+    w = gva_inputs.workload("gva350m_b8_t2k")
+    inp = gva_inputs.make_inputs(w, 47, lens=torch.tensor([2048, 1500, 7, 1, 2048, 33, 900, 64]))
+    B = w.batch
+    seq = torch.arange(B, dtype=torch.int32)
+    pos = (inp["lens"] - 1).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"])
+    dev = upload(inp)
+    d = dims_of(w)
+    S = gva.splits_for(d, inp["lens"])
+    itype = torch.int16
+    for rep in range(2):
+        note(f"append+attend in one launch, S={S}, rep {rep}")
+        o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S,
+                            v_new=dev["v_new"], kr_new=dev["kr_new"])
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"append+attend/rep{rep}")
+        assert torch.equal(gva.untiled(dev["v"].cpu()).view(itype), v_ref.view(itype))
+        assert torch.equal(gva.untiled(dev["kr"].cpu()).view(itype), k_ref.view(itype))
