@@ -158,6 +158,73 @@ def cpu_baseline(w, inp, seq, pos, budget_s: float = 20.0, min_s: float = 10.0):
     return rec, o_all
 
 
+MALL_BYTES = 256 << 20
+
+
+def timed(step, steps: int, stream) -> float:
+    """Mean ms per step over ``steps`` calls of step(i), bracketed by events
+    on ``stream`` with no events inside."""
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    t_start.record(stream)
+    for i in range(steps):
+        step(i)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    return t_start.elapsed_time(t_end) / steps
+
+
+def gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream):
+    """Attention only (the caches as stored, no append), GVA against the
+    matched GQA baseline on the same values, lengths and query content
+    slice, each rotating through its own cache copies; both merge their
+    splits with gva_combine."""
+    n = len(caches)
+    k_tiled = gva.tiled(inp["k_gqa"])
+    kcaches = [k_tiled.cuda() for _ in range(n)]
+    del k_tiled
+    bufs = gva.DecodeBuffers(d, S)
+    q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+    q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+
+    def gva_attn(i):
+        vc, kc = caches[i % n]
+        if fused:
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
+                                     q=dev["q"], m=dev["m"], stream=stream)
+        else:
+            gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
+                                     q_abs=q_abs, q_rot=q_rot if w.d_r > 0 else None, stream=stream)
+        if S > 1:
+            gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
+
+    def gqa_attn(i):
+        gva.gva_gqa_decode_attention(d, dev["q"], kcaches[i % n], caches[i % n][0], dev["lens"], S,
+                                     bufs.o_part, bufs.lse_part, stream=stream)
+        if S > 1:
+            gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
+
+    for i in range(args.warmup):
+        gva_attn(i)
+        gqa_attn(i)
+    t_gva = timed(gva_attn, args.steps, stream)
+    t_gqa = timed(gqa_attn, args.steps, stream)
+    elem = 2
+    out_b = w.batch * w.n_heads * w.d_v * 4
+    b_gva = traffic.decode_bytes(inp["lens"], w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c,
+                                 w.d_r, elem) + out_b
+    b_gqa = traffic.gqa_decode_bytes(inp["lens"], w.batch, w.n_heads, w.n_groups, w.d_v, elem) + out_b
+    del kcaches
+    return {"what": "attention only (caches as stored), GVA vs matched GQA, same splits",
+            "gva_ms": round(t_gva, 5), "gqa_ms": round(t_gqa, 5),
+            "time_ratio_gva_over_gqa": round(t_gva / t_gqa, 4),
+            "gva_bytes": b_gva, "gqa_bytes": b_gqa, "byte_ratio_gva_over_gqa": round(b_gva / b_gqa, 4),
+            "gva_GBps": round(b_gva / (t_gva * 1e-3) / 1e9, 1),
+            "gqa_GBps": round(b_gqa / (t_gqa * 1e-3) / 1e9, 1)}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -174,6 +241,11 @@ def main():
     ap.add_argument("--write-traffic", nargs=4, metavar=("FETCH_CSV", "WRITE_CSV", "COPY_FETCH_CSV",
                     "COPY_WRITE_CSV"), help="summarise rocprofv3 --pmc CSVs into the traffic record")
     ap.add_argument("--copy-mb", type=int, default=1024)
+    ap.add_argument("--cache-copies", type=int, default=0,
+                    help="cache copies the steps rotate through (0: enough that the bytes one "
+                         "rotation streams exceed twice the 256 MB last-level cache, at least 2)")
+    ap.add_argument("--no-gqa", action="store_true",
+                    help="skip the matched-GQA comparison on workloads that carry a GQA key cache")
     args = ap.parse_args()
     if args.write_traffic:
         write_traffic(*args.write_traffic, args.workload, args.splits or 1, args.copy_mb)
@@ -199,9 +271,16 @@ def main():
                       w.rope_base)
     max_len = int(inp["lens"].max())
     S = args.splits or gva.splits_for(d, inp["lens"])
+    elem = 2 if w.dtype == "bf16" else 4
+    lens = inp["lens"]
+    dec_b = traffic.decode_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem)
+    # Rotate through enough cache copies that no step finds its rows left in
+    # the 256 MB last-level cache (MALL) by the previous one.
+    n_copies = args.cache_copies or min(64, max(2, math.ceil(2 * MALL_BYTES / dec_b)))
     dev = {k: inp[k].cuda() for k in ("q", "m", "lens", "v_new", "kr_new")}
-    dev["v"] = gva.tiled(inp["v"]).cuda()          # the library's cache layout
-    dev["kr"] = gva.tiled(inp["kr"]).cuda()
+    v_tiled, kr_tiled = gva.tiled(inp["v"]), gva.tiled(inp["kr"])   # the library's cache layout
+    caches = [(v_tiled.cuda(), kr_tiled.cuda()) for _ in range(n_copies)]
+    del v_tiled, kr_tiled
     seq = torch.arange(w.batch, dtype=torch.int32)
     pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
     bufs = gva.DecodeBuffers(d, S)
@@ -211,18 +290,19 @@ def main():
     stream = torch.cuda.current_stream()
     pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"] if w.d_r > 0 else None)
 
-    def step(ev_a=None, ev_b=None):
+    def step(i, ev_a=None, ev_b=None):
         # Algorithm 1: the attention call appends the current token's rows to
         # the caches and attends over them in the same launch.
+        vc, kc = caches[i % n_copies]
         if not fused:
             gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
         if ev_a is not None:
             ev_a.record(stream)
         if fused:
-            gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, bufs.o_part,
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part,
                                      bufs.lse_part, q=dev["q"], m=dev["m"], stream=stream, **pend)
         else:
-            gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, bufs.o_part,
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part,
                                      bufs.lse_part, q_abs=q_abs,
                                      q_rot=q_rot if w.d_r > 0 else None, stream=stream, **pend)
         if ev_b is not None:
@@ -230,35 +310,23 @@ def main():
         if S > 1:   # with one split the attention kernel's partial is the output
             gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
-    for _ in range(args.warmup):
-        step()
+    for i in range(args.warmup):
+        step(i)
     torch.cuda.synchronize()
-
-    # timed region 1: whole steps, no events inside
-    t_start = torch.cuda.Event(enable_timing=True)
-    t_end = torch.cuda.Event(enable_timing=True)
-    t_start.record(stream)
-    for _ in range(args.steps):
-        step()
-    t_end.record(stream)
-    torch.cuda.synchronize()
-    ms_per_step = t_start.elapsed_time(t_end) / args.steps
+    ms_per_step = timed(step, args.steps, stream)
 
     # timed region 2: the same steps with events around the attention kernel
     evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
            for _ in range(args.steps)]
     torch.cuda.synchronize()
-    for a, b in evs:
-        step(a, b)
+    for i, (a, b) in enumerate(evs):
+        step(i, a, b)
     torch.cuda.synchronize()
     kt = sorted(a.elapsed_time(b) for a, b in evs)
     decode_ms = sum(kt) / len(kt)
 
-    elem = 2 if w.dtype == "bf16" else 4
-    lens = inp["lens"]
     step_b = traffic.step_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
                                 appended_rows=w.batch)
-    dec_b = traffic.decode_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem)
     value = step_b / (ms_per_step * 1e-3) / 1e9
     achieved = dec_b / (decode_ms * 1e-3) / 1e9
 
@@ -278,7 +346,8 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "t_max": w.t_max,
                    "n_heads": w.n_heads, "n_groups": w.n_groups, "d_v": w.d_v, "d_c": w.d_c,
                    "d_r": w.d_r, "num_splits": S, "fused_absorb": fused,
-                   "total_cached_rows": int(lens.clamp(min=0).sum()), "parallelism": "none"},
+                   "total_cached_rows": int(lens.clamp(min=0).sum()), "cache_copies": n_copies,
+                   "parallelism": "none"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
         "tokens_per_s": round(w.batch / (ms_per_step * 1e-3), 1),
         "tokens_heads_per_s": round(w.batch * w.n_heads / (ms_per_step * 1e-3), 1),
@@ -297,8 +366,10 @@ def main():
         "cpu_baseline": None,
     }
 
+    o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
+    if w.gqa and not args.no_gqa:
+        out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream)
     if not args.no_cpu_baseline:
-        o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
         rec, o_ref = cpu_baseline(w, inp, seq, pos)
         errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]
         rec["max_abs_err_vs_gpu"] = max(errs) if errs else None

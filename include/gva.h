@@ -16,6 +16,10 @@
  *                         steps of Algorithm 1)
  *   gva_combine           log-sum-exp merge of the split partials
  *
+ * The matched grouped-query baseline the paper measures GVA against
+ * (explicit key stream per group) has its own attention call,
+ * gva_gqa_decode_attention, sharing the layout, splits and gva_combine.
+ *
  * Conventions shared by every call
  * --------------------------------
  * - Every tensor argument is a DEVICE pointer to a dense, row-major array;
@@ -164,6 +168,29 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
                          void* v_cache, void* kr_cache,
                          const int32_t* lens, const void* v_new, const void* kr_new,
                          int32_t num_splits, float* o_part, float* lse_part, void* stream);
+
+/*
+ * gva_gqa_decode_attention -- the matched grouped-query attention baseline
+ * that GVA is measured against (Section 2, GQA; Section 3.4 compares the
+ * caches): one explicit key stream per group, stored already rotated as a
+ * standard GQA cache is, and no positional term.  For every (b, h, s):
+ *   rows    P as in gva_decode_attention (same split rule)
+ *   score   x_t = scale * q[b][h][0 : d_v] . k_cache[b][g(h)][t]
+ *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
+ *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)
+ * with scale = dims->scale, or 1/sqrt(d_v) when it is 0.  The key width is
+ * d_v; d_c, d_r and rope_base are not used.  Empty P and S == 1 behave as in
+ * gva_decode_attention; gva_combine merges the partials.
+ * q [B][H][q_stride] in the storage dtype (only the first d_v entries of a
+ * row are read); k_cache and v_cache: B*G streams of T rows x d_v in the
+ * tiled layout.  Read only: the caches are not modified.
+ * Supported: bf16, d_v in {64, 128}, H/G in {1, 2, 4, 8}, q_stride a
+ * multiple of 8, T % 16 == 0; other valid shapes: GVA_ERR_UNSUPPORTED.
+ * q_stride < d_v: GVA_ERR_INVALID_ARG.  Pointers: 16-byte aligned.
+ */
+int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stride,
+                             const void* k_cache, const void* v_cache, const int32_t* lens,
+                             int32_t num_splits, float* o_part, float* lse_part, void* stream);
 
 /*
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):

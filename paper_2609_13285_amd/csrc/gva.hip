@@ -101,6 +101,8 @@ struct DecodeParams {
   float* lse_part;
   const void* v_new;      // optional: the current token's rows, used in place
   const void* kr_new;     // of cache row len-1 (see gva_decode_attention)
+  const void* k_gqa;      // matched-GQA baseline: explicit key cache (tiled like v)
+  int32_t q_stride;       // matched-GQA baseline: elements per query row
   int32_t B, H, G, d_v, d_c, d_r, t_max, S;
   float scale_log2;       // score scale * log2(e): softmax runs in base 2
   int32_t fused;
@@ -420,15 +422,22 @@ struct DecodeCfg {
   static constexpr int LDS_FLOATS = LDS_PRO > LDS_RED ? LDS_PRO : LDS_RED;
 };
 
-template <int DV, int NRC>
+template <int DV, int NRC, bool GQA>
 struct Tile {
   bf16x8 v[2][DV / 32];                // [16-row half][K-chunk]
   bf16x8 k[2][NRC > 0 ? NRC : 1];      // positional key, [half][chunk]
+  bf16x8 kc[2][GQA ? DV / 32 : 1];     // matched-GQA baseline: explicit key rows
 };
 
-template <int HPG, int DV, int NRC>
+// GQA = true builds the matched grouped-query baseline the paper compares
+// against (Section 2): the scores read an explicit, already-rotated key
+// stream per group instead of the value rows, with no positional term and
+// the raw query; P.V, the softmax, the splits and the layout are shared, so
+// the two kernels differ only in the bytes they must stream.
+template <int HPG, int DV, int NRC, bool GQA = false>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
   using Cfg = DecodeCfg<HPG, DV, NRC>;
+  using TileT = Tile<DV, NRC, GQA>;
   constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
@@ -446,7 +455,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   split_rows(L, p.S, s, r0, r1);
   // With the current token's rows given, the split holding row L-1 takes
   // that row from them and streams only the rows before it from the cache.
-  const bool pending = p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
+  const bool pending = !GQA && p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
   if (pending) r1 = L - 1;
   const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
 
@@ -468,6 +477,11 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       const_cast<uint16_t*>(vbase), (short)0, r1c * DV * 2, kBufferWord3);
   const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(kbase), (short)0, r1c * p.d_r * 2, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
+                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
+                            : static_cast<const void*>(vbase)),
+      (short)0, r1c * DV * 2, kBufferWord3);
   const int kpieces = p.d_r / 8;              // 16-byte pieces per key row
   const int v_lane = qd * 256 + n * 16;       // piece qd of row n (of a 32-column chunk)
   int k_lane[NRC > 0 ? NRC : 1];
@@ -479,11 +493,16 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
   const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
   auto tile_row = [&](int j) { return r0 + (w + kWaves * j) * kTileRows; };
-  auto load_tile = [&](Tile<DV, NRC>& t, int row0) {
+  auto load_tile = [&](TileT& t, int row0) {
     const int lt = row0 / kLayoutRows;         // first layout tile (uniform)
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int vsoff = (lt + hf) * v_tile_bytes;
+      if constexpr (GQA) {                     // keys first: the scores need them first
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          t.kc[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kcres, v_lane + 1024 * c, vsoff, kAuxNT));
+      }
 #pragma unroll
       for (int c = 0; c < NC; ++c)
         t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, kAuxNT));
@@ -493,7 +512,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
         t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], ksoff, 0));
     }
   };
-  Tile<DV, NRC> buf[DEPTH];
+  TileT buf[DEPTH];
 
   // The pending row's raw values: one 16-byte value piece per thread of the
   // first DV/8 threads, one positional pair per thread of the first d_r/2.
@@ -514,7 +533,31 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   // so waiting for the query does not wait for the prefetched tiles.
   bf16x8 bq[NC];
   bf16x8 bk[NRC > 0 ? NRC : 1];
-  if (!p.fused) {
+  if constexpr (GQA) {
+    // the raw query's first DV entries, scaled, split hi + lo
+    const int hq = h0 + col_head;
+    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.H + hq) * p.q_stride + 8 * qd;
+    u32x4 xq[NC];
+#pragma unroll
+    for (int c = 0; c < NC; ++c) xq[c] = *reinterpret_cast<const u32x4*>(qrow + 32 * c);
+    __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+    for (int d = 0; d < DEPTH - 1; ++d) {
+      load_tile(buf[d], tile_row(d));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      float x[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        x[2 * j] = bf16_bits_to_f32(xq[c][j] & 0xFFFFu) * p.scale_log2;
+        x[2 * j + 1] = bf16_bits_to_f32(xq[c][j] >> 16) * p.scale_log2;
+      }
+      bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
+    }
+  } else if (!p.fused) {
     const int hq = h0 + col_head;
     const float* qa = p.q_abs + ((int64_t)b * p.H + hq) * DV + 8 * qd;
     f32x4 xa[NC][2];
@@ -681,13 +724,17 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
   const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 
-  auto compute_tile = [&](Tile<DV, NRC>& t, int row0, int row_end) {
+  auto compute_tile = [&](TileT& t, int row0, int row_end) {
     if (row0 + kTileRows > row_end) {        // ragged tail: clear rows past the end
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         const bool dead = row0 + 16 * hf + n >= row_end;
 #pragma unroll
         for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
+        if constexpr (GQA) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) t.kc[hf][c] = dead ? zero8 : t.kc[hf][c];
+        }
 #pragma unroll
         for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
       }
@@ -698,7 +745,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     for (int hf = 0; hf < 2; ++hf) {
       sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int c = 0; c < NC; ++c) sc[hf] = mfma16(t.v[hf][c], bq[c], sc[hf]);
+      for (int c = 0; c < NC; ++c) sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[c], sc[hf]);
 #pragma unroll
       for (int rc = 0; rc < NRC; ++rc) sc[hf] = mfma16(t.k[hf][rc], bk[rc], sc[hf]);
     }
@@ -804,7 +851,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     }
     __syncthreads();
     if (w == 0) {
-      Tile<DV, NRC> t;
+      TileT t;
       const u32x4* pv = reinterpret_cast<const u32x4*>(prow);
 #pragma unroll
       for (int c = 0; c < NC; ++c) {
@@ -1178,6 +1225,25 @@ DecodeFn pick_dv(int dv, int nrc) {
   return nullptr;
 }
 
+template <int DV>
+DecodeFn pick_gqa_hpg(int hpg) {
+  switch (hpg) {
+    case 1: return decode_bf16_kernel<1, DV, 0, true>;
+    case 2: return decode_bf16_kernel<2, DV, 0, true>;
+    case 4: return decode_bf16_kernel<4, DV, 0, true>;
+    case 8: return decode_bf16_kernel<8, DV, 0, true>;
+  }
+  return nullptr;
+}
+
+DecodeFn pick_gqa_decode(int hpg, int dv) {
+  switch (dv) {
+    case 64: return pick_gqa_hpg<64>(hpg);
+    case 128: return pick_gqa_hpg<128>(hpg);
+  }
+  return nullptr;
+}
+
 DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
   switch (hpg) {
     case 1: return pick_dv<1>(dv, nrc);
@@ -1192,7 +1258,7 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
 
 extern "C" {
 
-int gva_version(void) { return 10200; }
+int gva_version(void) { return 10300; }
 
 const char* gva_status_string(int status) {
   switch (status) {
@@ -1316,6 +1382,8 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   p.lse_part = lse_part;
   p.v_new = v_new;
   p.kr_new = kr_new;
+  p.k_gqa = nullptr;
+  p.q_stride = 0;
   p.B = dims->batch;
   p.H = dims->n_heads;
   p.G = dims->n_groups;
@@ -1341,6 +1409,49 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
       return GVA_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(decode_f32_kernel, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   }
+  return launch_status();
+}
+
+int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stride,
+                             const void* k_cache, const void* v_cache, const int32_t* lens,
+                             int32_t num_splits, float* o_part, float* lse_part, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
+  if (!q || !k_cache || !v_cache || !lens || !o_part || !lse_part) return GVA_ERR_INVALID_ARG;
+  if (q_stride < dims->d_v) return GVA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) ||
+      !aligned(o_part, 16) || !aligned(lse_part, 4))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->dtype != GVA_DTYPE_BF16 || q_stride % 8 != 0) return GVA_ERR_UNSUPPORTED;
+  if (dims->t_max % kLayoutRows != 0) return GVA_ERR_UNSUPPORTED;
+  if ((double)dims->t_max * dims->d_v * 2.0 >= 2147483648.0 - 16777216.0) return GVA_ERR_UNSUPPORTED;
+  const int hpg = dims->n_heads / dims->n_groups;
+  DecodeFn fn = pick_gqa_decode(hpg, dims->d_v);
+  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
+  const long long n_items = (long long)dims->batch * dims->n_groups * num_splits;
+  if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
+
+  DecodeParams p;
+  memset(&p, 0, sizeof(p));
+  p.q = q;
+  p.v = const_cast<void*>(v_cache);       // read only: the GQA kernel never appends
+  p.k_gqa = k_cache;
+  p.q_stride = q_stride;
+  p.lens = lens;
+  p.o_part = o_part;
+  p.lse_part = lse_part;
+  p.B = dims->batch;
+  p.H = dims->n_heads;
+  p.G = dims->n_groups;
+  p.d_v = dims->d_v;
+  p.d_c = dims->d_v;
+  p.d_r = 0;
+  p.t_max = dims->t_max;
+  p.S = num_splits;
+  const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
+  p.scale_log2 = (float)(sc * kLog2e);
+  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
 }
 

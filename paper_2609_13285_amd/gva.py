@@ -21,7 +21,7 @@ GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, 1, 2, 3
 GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
-           "gva_pick_splits", "gva_status_string", "gva_version")
+           "gva_gqa_decode_attention", "gva_pick_splits", "gva_status_string", "gva_version")
 
 
 class GvaError(RuntimeError):
@@ -61,12 +61,13 @@ def lib() -> ctypes.CDLL:
         L.gva_absorb_query.argtypes = [D, P, P, P, P, P, P]
         L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
+        L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, P, P, P]
         L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
-                     "gva_pick_splits", "gva_version"):
+                     "gva_gqa_decode_attention", "gva_pick_splits", "gva_version"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -183,6 +184,29 @@ def gva_combine(dims: GvaDims, o_part, lse_part, num_splits: int, o, lse=None, s
     _check("gva_combine", st)
 
 
+def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int, o_part,
+                             lse_part, stream=None):
+    """The matched-GQA baseline; ``q`` is [B, H, q_stride] with the query's
+    first d_v entries used."""
+    d = dims
+    dt = d.torch_dtype
+    S = int(num_splits)
+    if not isinstance(q, torch.Tensor) or q.dim() != 3:
+        raise ValueError("q must be a [B, H, q_stride] tensor")
+    st = lib().gva_gqa_decode_attention(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, q.shape[-1])),
+        int(q.shape[-1]),
+        _ptr(k_cache, "k_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        S,
+        _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
+        _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
+        _stream(stream))
+    _check("gva_gqa_decode_attention", st)
+
+
 def gva_pick_splits(dims: GvaDims, max_len: int = 0, total_len: int = 0, n_cu: int = 0) -> int:
     return int(lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(total_len), int(n_cu)))
 
@@ -265,6 +289,19 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
                              q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream, **pend)
     if S == 1:   # a single split's partial is already the final result
+        return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
+    gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
+    return bufs.o, bufs.lse
+
+
+def gqa_decode(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int,
+               bufs: Optional[DecodeBuffers] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Matched-GQA attention + combine for one step; returns (o, lse) fp32."""
+    S = int(num_splits)
+    if bufs is None or bufs.num_splits != S:
+        bufs = DecodeBuffers(dims, S, device=v_cache.device)
+    gva_gqa_decode_attention(dims, q, k_cache, v_cache, lens, S, bufs.o_part, bufs.lse_part, stream=stream)
+    if S == 1:
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
     return bufs.o, bufs.lse

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = gva.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert gva.gva_version() == 10200
+    assert gva.gva_version() == 10300
 
 
 def test_status_strings():
@@ -154,3 +154,22 @@ def test_tiled_layout_matches_header_formula():
         assert torch.equal(gva.untiled(gva.tiled(x)), x)
     z = torch.randn(2, 3, 32, 16).to(torch.bfloat16)
     assert torch.equal(gva.untiled(gva.tiled(z)), z)
+
+
+def gqa_status(d, q=A, stride=None, k=A, v=A, lens=A, S=2, op=A, lp=A):
+    stride = d.d_v + 16 if stride is None else stride
+    return gva.lib().gva_gqa_decode_attention(ctypes.byref(d), q, stride, k, v, lens, S, op, lp, None)
+
+
+def test_gqa_validation():
+    d = dims(n_heads=16, n_groups=2)
+    assert gqa_status(dims(batch=0)) == gva.GVA_ERR_INVALID_ARG
+    for kw in (dict(q=None), dict(k=None), dict(v=None), dict(lens=None), dict(op=None),
+               dict(lp=None), dict(k=A + 2), dict(op=A + 4), dict(S=0),
+               dict(S=gva.GVA_MAX_SPLITS + 1), dict(stride=64)):
+        assert gqa_status(d, **kw) == gva.GVA_ERR_INVALID_ARG, kw
+    assert gqa_status(dims(dtype="f32")) == gva.GVA_ERR_UNSUPPORTED          # bf16 only
+    assert gqa_status(dims(d_v=96), stride=96) == gva.GVA_ERR_UNSUPPORTED
+    assert gqa_status(dims(n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED   # H/G = 16
+    assert gqa_status(d, stride=132) == gva.GVA_ERR_UNSUPPORTED             # 16-byte query rows
+    assert gqa_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED

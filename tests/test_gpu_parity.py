@@ -329,3 +329,72 @@ def test_append_and_attend_in_one_launch_full_step():
         _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"append+attend/rep{rep}")
         assert torch.equal(gva.untiled(dev["v"].cpu()).view(itype), v_ref.view(itype))
         assert torch.equal(gva.untiled(dev["kr"].cpu()).view(itype), k_ref.view(itype))
+
+
+# ------------------------------------------------ matched-GQA baseline kernel
+@pytest.mark.parametrize("hpg,dv", [(1, 64), (2, 128), (4, 64), (8, 128)])
+def test_gqa_baseline_matches_oracle(hpg, dv):
+    G = 2
+    w = gva_inputs.Workload("gqa", 5, 304, G * hpg, G, dv, dv, 16, dtype="bf16", gqa=True)
+    lens = torch.tensor([304, 0, 1, 33, 207], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 11, lens=lens)
+    o_ref, lse_ref = oracle.gqa_decode(inp["q"], inp["k_gqa"], inp["v"], inp["lens"], d_k=dv)
+    dev = upload(inp)
+    d = dims_of(w)
+    for S in (1, 3, 8):
+        note(f"gqa hpg={hpg} dv={dv} S={S}")
+        o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S)
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"gqa/hpg{hpg}/dv{dv}/S{S}")
+
+
+def test_gqa_baseline_partials_and_untouched_caches():
+    # every split partial against the oracle on that split's rows; the
+    # caches are read only
+    w = gva_inputs.Workload("gqa", 3, 208, 16, 2, 128, 128, 16, dtype="bf16", gqa=True)
+    lens = torch.tensor([208, 95, 17], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 5, lens=lens)
+    dev = upload(inp)
+    k0, v0 = dev["k_gqa"].clone(), dev["v"].clone()
+    d = dims_of(w)
+    S = 4
+    bufs = gva.DecodeBuffers(d, S)
+    gva.gva_gqa_decode_attention(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S,
+                                 bufs.o_part, bufs.lse_part)
+    torch.cuda.synchronize()
+    op, lp = bufs.o_part.cpu(), bufs.lse_part.cpu()
+    for s, (lo, hi) in enumerate(zip(*oracle.split_bounds(inp["lens"], S))):
+        for b in range(w.batch):
+            a, e = int(lo[b]), int(hi[b])
+            if a >= e:
+                assert torch.all(op[b, :, s] == 0) and torch.all(lp[b, :, s] == float("-inf"))
+                continue
+            sl = slice(b, b + 1)
+            o_ref, lse_ref = oracle.gqa_decode(inp["q"][sl], inp["k_gqa"][sl, :, a:e].contiguous(),
+                                               inp["v"][sl, :, a:e].contiguous(),
+                                               torch.tensor([e - a], dtype=torch.int32), d_k=w.d_v)
+            _check(w, op[sl, :, s], lp[sl, :, s], o_ref, lse_ref, f"gqa partial b{b} s{s}")
+    assert torch.equal(dev["k_gqa"], k0) and torch.equal(dev["v"], v0)
+
+
+@pytest.mark.slow
+def test_gqa_baseline_full_size_sampled():
+    w = gva_inputs.workload("ragged_b64")
+    note("ragged_b64 gqa: drawing inputs")
+    inp = gva_inputs.make_inputs(w, 0)
+    d = dims_of(w)
+    S = gva.splits_for(d, inp["lens"])
+    dev = upload({k: inp[k] for k in ("q", "v", "k_gqa", "lens")})
+    note(f"ragged_b64 gqa: decode S={S}")
+    o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S)
+    o, lse = o.cpu(), lse.cpu()
+    del dev
+    torch.cuda.empty_cache()
+    lens = inp["lens"]
+    picks = sorted({0, w.batch - 1, int(lens.argmax()), int(lens.argmin())})
+    sub = sub_batch(inp, picks)
+    note(f"ragged_b64 gqa: oracle on sequences {picks}")
+    o_ref, lse_ref = oracle.gqa_decode(sub["q"], sub["k_gqa"], sub["v"], sub["lens"], d_k=w.d_v)
+    idx = torch.tensor(picks)
+    _check(w, o[idx], lse[idx], o_ref, lse_ref, "ragged_b64 gqa/sampled")
+    assert torch.isfinite(o).all()
