@@ -175,7 +175,7 @@ def timed(step, steps: int, stream) -> float:
     return t_start.elapsed_time(t_end) / steps
 
 
-def gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream):
+def gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches, stream):
     """Attention only (the caches as stored, no append), GVA against the
     matched GQA baseline on the same values, lengths and query content
     slice, each rotating through its own cache copies; both merge their
@@ -192,17 +192,18 @@ def gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream):
         vc, kc = caches[i % n]
         if fused:
             gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
-                                     q=dev["q"], m=dev["m"], stream=stream)
+                                     q=dev["q"], m=dev["m"], split_rows=split_rows, stream=stream)
         else:
             gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
             gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
-                                     q_abs=q_abs, q_rot=q_rot if w.d_r > 0 else None, stream=stream)
+                                     q_abs=q_abs, q_rot=q_rot if w.d_r > 0 else None,
+                                     split_rows=split_rows, stream=stream)
         if S > 1:
             gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
     def gqa_attn(i):
         gva.gva_gqa_decode_attention(d, dev["q"], kcaches[i % n], caches[i % n][0], dev["lens"], S,
-                                     bufs.o_part, bufs.lse_part, stream=stream)
+                                     bufs.o_part, bufs.lse_part, split_rows=split_rows, stream=stream)
         if S > 1:
             gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
@@ -217,7 +218,7 @@ def gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream):
                                  w.d_r, elem) + out_b
     b_gqa = traffic.gqa_decode_bytes(inp["lens"], w.batch, w.n_heads, w.n_groups, w.d_v, elem) + out_b
     del kcaches
-    return {"what": "attention only (caches as stored), GVA vs matched GQA, same splits",
+    return {"what": "attention only (caches as stored), GVA vs matched GQA, same split plan",
             "gva_ms": round(t_gva, 5), "gqa_ms": round(t_gqa, 5),
             "time_ratio_gva_over_gqa": round(t_gva / t_gqa, 4),
             "gva_bytes": b_gva, "gqa_bytes": b_gqa, "byte_ratio_gva_over_gqa": round(b_gva / b_gqa, 4),
@@ -231,7 +232,10 @@ def main():
     ap.add_argument("--steps", type=int, default=100)
     ap.add_argument("--warmup", type=int, default=10)
     ap.add_argument("--workload", default="b32_t8k", choices=sorted(gva_inputs.WORKLOADS))
-    ap.add_argument("--splits", type=int, default=0)
+    ap.add_argument("--splits", type=int, default=0,
+                    help="splits per sequence (0: gva_pick_splits' plan)")
+    ap.add_argument("--split-rows", type=int, default=0,
+                    help="with --splits: fixed rows per split (0: even splits)")
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--absorb", choices=("auto", "fused", "separate"), default="auto",
                     help="absorb the query inside the attention kernel (fused) or in its own "
@@ -270,7 +274,10 @@ def main():
     d = gva.make_dims(w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, w.t_max, w.dtype,
                       w.rope_base)
     max_len = int(inp["lens"].max())
-    S = args.splits or gva.splits_for(d, inp["lens"])
+    if args.splits:
+        S, split_rows = args.splits, args.split_rows
+    else:
+        S, split_rows = gva.plan_for(d, inp["lens"])
     elem = 2 if w.dtype == "bf16" else 4
     lens = inp["lens"]
     dec_b = traffic.decode_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem)
@@ -288,7 +295,8 @@ def main():
     q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
     q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
-    pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"] if w.d_r > 0 else None)
+    pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"] if w.d_r > 0 else None,
+                split_rows=split_rows)
 
     def step(i, ev_a=None, ev_b=None):
         # Algorithm 1: the attention call appends the current token's rows to
@@ -345,7 +353,7 @@ def main():
         "data": "synthetic",
         "config": {"workload": w.name, "batch": w.batch, "t_max": w.t_max,
                    "n_heads": w.n_heads, "n_groups": w.n_groups, "d_v": w.d_v, "d_c": w.d_c,
-                   "d_r": w.d_r, "num_splits": S, "fused_absorb": fused,
+                   "d_r": w.d_r, "num_splits": S, "split_rows": split_rows, "fused_absorb": fused,
                    "total_cached_rows": int(lens.clamp(min=0).sum()), "cache_copies": n_copies,
                    "parallelism": "none"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
@@ -368,7 +376,8 @@ def main():
 
     o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
     if w.gqa and not args.no_gqa:
-        out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, fused, dev, caches, stream)
+        out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches,
+                                               stream)
     if not args.no_cpu_baseline:
         rec, o_ref = cpu_baseline(w, inp, seq, pos)
         errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]

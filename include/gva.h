@@ -136,13 +136,19 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
 /*
  * gva_decode_attention -- the attention steps of Algorithm 1 over split s
  * of every sequence, for every (b, h, s):
- *   rows    P = [s*c_b, min(L_b, (s+1)*c_b)),  L_b = lens[b] (clamped),
- *           c_b = 32 * ceil(ceil(L_b / S) / 32),  S = num_splits
+ *   rows    P = [s*c_b, e),  e = min(L_b, (s+1)*c_b) for s < S-1, e = L_b
+ *           for s = S-1;  L_b = lens[b] (clamped to [0, T]),  S = num_splits,
+ *           c_b = split_rows when split_rows > 0 (fixed chunks: every
+ *           split of every sequence gets the same rows, for ragged
+ *           batches), else c_b = 32 * ceil(ceil(L_b / S) / 32) (even
+ *           splits per sequence)
  *   score   x_t = scale * ( q~_h . v_cache[b][g(h)][t] + q^rope_h . kr_cache[b][t] )
  *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
  *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)       (natural log)
- * An empty P writes o_part = 0 and lse_part = -inf.  With S == 1 the
- * partials are the final (o, lse).
+ * An empty P writes lse_part = -inf; its o_part is written (zeros) only for
+ * s = 0 and is otherwise left untouched (gva_combine never reads it).  With
+ * S == 1 the partials are the final (o, lse).  split_rows must be a
+ * non-negative multiple of 32.
  * The query comes either raw -- q and m non-NULL, q_abs and q_rot NULL: the
  * kernel absorbs and rotates it itself ahead of the attention loop (the
  * fused path) -- or pre-absorbed by gva_absorb_query: q/m NULL, q_abs
@@ -167,14 +173,15 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
                          const float* q_abs, const float* q_rot,
                          void* v_cache, void* kr_cache,
                          const int32_t* lens, const void* v_new, const void* kr_new,
-                         int32_t num_splits, float* o_part, float* lse_part, void* stream);
+                         int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
+                         void* stream);
 
 /*
  * gva_gqa_decode_attention -- the matched grouped-query attention baseline
  * that GVA is measured against (Section 2, GQA; Section 3.4 compares the
  * caches): one explicit key stream per group, stored already rotated as a
  * standard GQA cache is, and no positional term.  For every (b, h, s):
- *   rows    P as in gva_decode_attention (same split rule)
+ *   rows    P as in gva_decode_attention (same split rule and split_rows)
  *   score   x_t = scale * q[b][h][0 : d_v] . k_cache[b][g(h)][t]
  *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
  *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)
@@ -190,26 +197,32 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
  */
 int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stride,
                              const void* k_cache, const void* v_cache, const int32_t* lens,
-                             int32_t num_splits, float* o_part, float* lse_part, void* stream);
+                             int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
+                             void* stream);
 
 /*
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):
  *   LSE = log sum_s exp(lse_part[b][h][s]);
  *   o[b][h][:] = sum_s exp(lse_part[b][h][s] - LSE) * o_part[b][h][s][:]
- * Partials with lse = -inf are skipped; if all are, o = 0 and LSE = -inf.
+ * Partials with lse = -inf are skipped without reading their o_part; if
+ * all are, o = 0 and LSE = -inf.
  * lse may be NULL.  o [B][H][d_v] fp32, lse [B][H] fp32; d_v <= 256.
  */
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part,
                 int32_t num_splits, float* o, float* lse, void* stream);
 
 /*
- * gva_pick_splits -- host heuristic: a num_splits for a batch whose longest
- * sequence has max_len rows and whose lengths sum to total_len (0 = unknown:
- * every sequence taken as max_len), on a device with n_cu compute units
- * (0 = ask the current device).  Pure host code; enqueues nothing.  Returns
- * a value in [1, GVA_MAX_SPLITS].
+ * gva_pick_splits -- host heuristic: the split plan for a batch whose
+ * longest sequence has max_len rows and whose lengths sum to total_len
+ * (0 = unknown: every sequence taken as max_len), on a device with n_cu
+ * compute units (0 = ask the current device).  Returns num_splits in
+ * [1, GVA_MAX_SPLITS]; when split_rows is non-NULL it receives the
+ * split_rows to pass with it (0 = even splits; fixed chunks are chosen for
+ * widely spread lengths).  With split_rows NULL the plan uses even splits
+ * only.  Pure host code; enqueues nothing.
  */
-int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu);
+int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
+                    int32_t* split_rows);
 
 /* Human-readable name of a gva_status value (static storage). */
 const char* gva_status_string(int status);

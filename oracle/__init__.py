@@ -197,19 +197,23 @@ def gqa_decode(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, lens: torch.Te
     return o, lse
 
 
-def split_bounds(lens: torch.Tensor, num_splits: int, tile: int = 32):
+def split_bounds(lens: torch.Tensor, num_splits: int, tile: int = 32, split_rows: int = 0):
     """Row ranges [begin, end) of every split, per sequence: [S][B] each.
 
-    Split s of a sequence with L rows covers [s*c, min(L, (s+1)*c)) with
-    c = tile * ceil(ceil(L / S) / tile); trailing splits may be empty.
+    Split s of a sequence with L rows covers [s*c, min(L, (s+1)*c)), except
+    that the last split ends at L.  c = split_rows when it is positive,
+    else c = tile * ceil(ceil(L / S) / tile).  Trailing splits may be empty.
     """
     L = lens.to(torch.int64).clamp(min=0)
-    per = (L + num_splits - 1) // num_splits
-    chunk = ((per + tile - 1) // tile) * tile
+    if split_rows > 0:
+        chunk = torch.full_like(L, int(split_rows))
+    else:
+        per = (L + num_splits - 1) // num_splits
+        chunk = ((per + tile - 1) // tile) * tile
     begins, ends = [], []
     for s in range(num_splits):
         b = torch.minimum(chunk * s, L)
-        e = torch.minimum(chunk * (s + 1), L)
+        e = L if s == num_splits - 1 else torch.minimum(chunk * (s + 1), L)
         begins.append(b.to(torch.int32))
         ends.append(e.to(torch.int32))
     return begins, ends

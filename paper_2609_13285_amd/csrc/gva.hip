@@ -104,6 +104,7 @@ struct DecodeParams {
   const void* k_gqa;      // matched-GQA baseline: explicit key cache (tiled like v)
   int32_t q_stride;       // matched-GQA baseline: elements per query row
   int32_t B, H, G, d_v, d_c, d_r, t_max, S;
+  int32_t split_rows;     // fixed rows per split (0: the even rule)
   float scale_log2;       // score scale * log2(e): softmax runs in base 2
   int32_t fused;
   double inv_freq[kMaxPairs];
@@ -170,12 +171,19 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int b, int t_max) 
   return L < 0 ? 0 : (L > t_max ? t_max : L);
 }
 
-// Split s of a sequence with L rows: [s*c, min(L, (s+1)*c)),
-// c = kTileRows * ceil(ceil(L / S) / kTileRows).
-__device__ __forceinline__ void split_rows(int L, int S, int s, int& r0, int& r1) {
-  int per = (L + S - 1) / S;
-  int chunk = ((per + kTileRows - 1) / kTileRows) * kTileRows;
-  long long a = (long long)chunk * s, e = (long long)chunk * (s + 1);
+// Split s of a sequence with L rows covers [s*c, e): e = min(L, (s+1)*c)
+// for s < S-1 and e = L for the last split.  c is the caller's fixed chunk
+// when positive (a multiple of kTileRows), else the even rule
+// c = kTileRows * ceil(ceil(L / S) / kTileRows), under which the last split
+// ends at L anyway.
+__device__ __forceinline__ void split_rows(int L, int S, int fixed, int s, int& r0, int& r1) {
+  int chunk = fixed;
+  if (chunk <= 0) {
+    const int per = (L + S - 1) / S;
+    chunk = ((per + kTileRows - 1) / kTileRows) * kTileRows;
+  }
+  const long long a = (long long)chunk * s;
+  const long long e = s == S - 1 ? (long long)L : (long long)chunk * (s + 1);
   r0 = (int)(a < L ? a : L);
   r1 = (int)(e < L ? e : L);
 }
@@ -189,6 +197,31 @@ __device__ __forceinline__ int xcd_remap(int x, int n) {
   const int per = n / 8, rem = n % 8;
   const int xcd = x % 8, slot = x / 8;
   return xcd * per + (xcd < rem ? xcd : rem) + slot;
+}
+
+// Workgroup -> (sequence b, split s, group g).  The G groups of one
+// (b, s) always land on one XCD, next to each other.
+//  - Even splits: XCD-contiguous items (xcd_remap), B * S * G workgroups.
+//  - Fixed chunks: chunk s of sequence b goes to XCD (b + s) mod 8, so every
+//    sequence's chunks are dealt over all XCDs and short sequences spread
+//    by b: the XCDs get near-equal shares of a ragged batch.  The grid is
+//    B * S8 * G with S8 = S rounded up to 8; workgroups whose s >= S are
+//    padding and return false.
+__device__ __forceinline__ bool work_item(const DecodeParams& p, int& b, int& s, int& g) {
+  if (p.split_rows > 0) {
+    const int x = blockIdx.x, xcd = x & 7, slot = x >> 3;
+    g = slot % p.G;
+    const int t = slot / p.G;
+    b = t % p.B;
+    s = 8 * (t / p.B) + ((xcd - (b & 7)) & 7);
+    return s < p.S;
+  }
+  const int item = xcd_remap(blockIdx.x, gridDim.x);
+  g = item % p.G;
+  const int bs = item / p.G;
+  s = bs % p.S;
+  b = bs / p.S;
+  return true;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -441,18 +474,19 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
-  const int item = xcd_remap(blockIdx.x, gridDim.x);
-  const int g = item % p.G;
-  const int bs = item / p.G;
-  const int s = bs % p.S;
-  const int b = bs / p.S;
+  int b, s, g;
+  if (!work_item(p, b, s, g)) return;          // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform (SGPR)
   const int n = lane & 15, qd = lane >> 4;     // MFMA column / row slot and 16-lane row
   const int h0 = g * HPG;
   const int L = clamp_len(p.lens, b, p.t_max);
   int r0, r1;
-  split_rows(L, p.S, s, r0, r1);
+  split_rows(L, p.S, p.split_rows, s, r0, r1);
+  if (r0 >= r1 && s > 0) {                     // an empty split past the first: lse only
+    if (tid < HPG) p.lse_part[((int64_t)b * p.H + h0 + tid) * p.S + s] = -INFINITY;
+    return;
+  }
   // With the current token's rows given, the split holding row L-1 takes
   // that row from them and streams only the rows before it from the cache.
   const bool pending = !GQA && p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
@@ -926,17 +960,18 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
   __shared__ float red_ml[kWaves][kF32MaxHpg][2];
   __shared__ float red_o[kWaves][kF32MaxHpg][kF32MaxDv];
 
-  const int item = xcd_remap(blockIdx.x, gridDim.x);
-  const int g = item % p.G;
-  const int bs = item / p.G;
-  const int s = bs % p.S;
-  const int b = bs / p.S;
+  int b, s, g;
+  if (!work_item(p, b, s, g)) return;          // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int hpg = p.H / p.G, h0 = g * hpg;
   const int DV = p.d_v, DR = p.d_r;
   const int L = clamp_len(p.lens, b, p.t_max);
   int r0, r1;
-  split_rows(L, p.S, s, r0, r1);
+  split_rows(L, p.S, p.split_rows, s, r0, r1);
+  if (r0 >= r1 && s > 0) {                     // an empty split past the first: lse only
+    if (tid < hpg) p.lse_part[((int64_t)b * p.H + h0 + tid) * p.S + s] = -INFINITY;
+    return;
+  }
   const bool pending = p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
   if (pending) r1 = L - 1;
 
@@ -1125,6 +1160,8 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 // single pass keeps a running log-sum-exp and rescales the running sum;
 // the split loads do not depend on each other, so they overlap.
 constexpr int kCombineMaxDv = 256;
+constexpr long long kChunkItemsPerCu = 2;         // fixed-chunk splits: chunks per CU
+constexpr long long kMinChunkBytes = 128 << 10;   // fixed-chunk splits: value bytes per chunk
 
 __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   const int lane = threadIdx.x & 63;
@@ -1132,24 +1169,59 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   if (row >= p.rows) return;
   const float* lp = p.lse_part + (int64_t)row * p.S;
   const float* op = p.o_part + (int64_t)row * p.S * p.d_v;
-  float m = -INFINITY, z = 0.f;
+  // the row's split LSEs, up to 4 per lane (S <= 256), and their maximum
+  float l[4];
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) {
+    const int s = lane + 64 * k;
+    l[k] = s < p.S ? lp[s] : -INFINITY;
+    mx = fmaxf(mx, l[k]);
+  }
+  mx = wave_max(mx);
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
-  for (int s = 0; s < p.S; ++s) {
-    const float l = lp[s];
-    float v[4];
+  float z = 0.f;
+  if (mx != -INFINITY) {
+    float wk[4];
 #pragma unroll
-    for (int u = 0; u < 4; ++u) {
-      const int i = lane + 64 * u;
-      v[u] = i < p.d_v ? op[(int64_t)s * p.d_v + i] : 0.f;
+    for (int k = 0; k < 4; ++k) {
+      wk[k] = l[k] == -INFINITY ? 0.f : expf(l[k] - mx);
+      z += wk[k];
     }
-    if (l == -INFINITY) continue;          // an empty split carries no rows
-    const float mn = fmaxf(m, l);
-    const float a = m == -INFINITY ? 0.f : expf(m - mn);
-    const float wgt = expf(l - mn);
-    z = z * a + wgt;
+    z = wave_sum(z);
+    // only the splits with rows are read, 8 at a time so their loads overlap
 #pragma unroll
-    for (int u = 0; u < 4; ++u) acc[u] = acc[u] * a + wgt * v[u];
-    m = mn;
+    for (int k = 0; k < 4; ++k) {
+      if (64 * k >= p.S) break;
+      unsigned long long mask = __ballot(l[k] != -INFINITY);
+      while (mask != 0ull) {
+        int sel[8];
+        float wsel[8];
+#pragma unroll
+        for (int j = 0; j < 8; ++j) {
+          sel[j] = -1;
+          wsel[j] = 0.f;
+          if (mask != 0ull) {
+            const int bit = __builtin_ctzll(mask);
+            mask &= mask - 1ull;
+            sel[j] = 64 * k + bit;
+            wsel[j] = __shfl(wk[k], bit, 64);
+          }
+        }
+        float v[8][4];
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) {
+            const int i = lane + 64 * u;
+            v[j][u] = (sel[j] >= 0 && i < p.d_v) ? op[(int64_t)sel[j] * p.d_v + i] : 0.f;
+          }
+#pragma unroll
+        for (int j = 0; j < 8; ++j)
+#pragma unroll
+          for (int u = 0; u < 4; ++u) acc[u] = fmaf(wsel[j], v[j][u], acc[u]);
+      }
+    }
   }
   const float inv = z > 0.f ? 1.f / z : 0.f;
 #pragma unroll
@@ -1157,7 +1229,7 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
     const int i = lane + 64 * u;
     if (i < p.d_v) p.o[(int64_t)row * p.d_v + i] = acc[u] * inv;
   }
-  if (p.lse != nullptr && lane == 0) p.lse[row] = m == -INFINITY ? -INFINITY : m + logf(z);
+  if (p.lse != nullptr && lane == 0) p.lse[row] = mx == -INFINITY ? -INFINITY : mx + logf(z);
 }
 
 // ================================================================== host
@@ -1197,6 +1269,12 @@ void fill_inv_freq(const gva_dims* d, double* out) {
 float scale_log2(const gva_dims* d) {
   const double sc = d->scale > 0.0 ? d->scale : 1.0 / sqrt((double)(d->d_c + d->d_r));
   return (float)(sc * kLog2e);
+}
+
+// Workgroups of a decode launch (see work_item).
+long long decode_grid(const gva_dims* d, int num_splits, int split_rows) {
+  const long long s = split_rows > 0 ? ((num_splits + 7LL) & ~7LL) : num_splits;
+  return (long long)d->batch * d->n_groups * s;
 }
 
 int launch_status() {
@@ -1258,7 +1336,7 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
 
 extern "C" {
 
-int gva_version(void) { return 10300; }
+int gva_version(void) { return 10400; }
 
 const char* gva_status_string(int status) {
   switch (status) {
@@ -1343,10 +1421,12 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const i
 int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, const float* q_abs,
                          const float* q_rot, void* v_cache, void* kr_cache,
                          const int32_t* lens, const void* v_new, const void* kr_new,
-                         int32_t num_splits, float* o_part, float* lse_part, void* stream) {
+                         int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
+                         void* stream) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
+  if (split_rows < 0 || split_rows % kTileRows != 0) return GVA_ERR_INVALID_ARG;
   const bool fused = q != nullptr || m != nullptr;
   if (fused) {
     if (!q || !m || q_abs || q_rot) return GVA_ERR_INVALID_ARG;
@@ -1367,7 +1447,7 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   if (st != GVA_OK) return st;
 
   const int hpg = dims->n_heads / dims->n_groups;
-  const long long n_items = (long long)dims->batch * dims->n_groups * num_splits;
+  const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p;
@@ -1392,6 +1472,7 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   p.d_r = dims->d_r;
   p.t_max = dims->t_max;
   p.S = num_splits;
+  p.split_rows = split_rows;
   p.scale_log2 = scale_log2(dims);
   p.fused = fused ? 1 : 0;
   fill_inv_freq(dims, p.inv_freq);
@@ -1414,10 +1495,12 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
 
 int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stride,
                              const void* k_cache, const void* v_cache, const int32_t* lens,
-                             int32_t num_splits, float* o_part, float* lse_part, void* stream) {
+                             int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
+                             void* stream) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
+  if (split_rows < 0 || split_rows % kTileRows != 0) return GVA_ERR_INVALID_ARG;
   if (!q || !k_cache || !v_cache || !lens || !o_part || !lse_part) return GVA_ERR_INVALID_ARG;
   if (q_stride < dims->d_v) return GVA_ERR_INVALID_ARG;
   if (!aligned(q, 16) || !aligned(k_cache, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) ||
@@ -1429,7 +1512,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   const int hpg = dims->n_heads / dims->n_groups;
   DecodeFn fn = pick_gqa_decode(hpg, dims->d_v);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const long long n_items = (long long)dims->batch * dims->n_groups * num_splits;
+  const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p;
@@ -1449,6 +1532,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   p.d_r = 0;
   p.t_max = dims->t_max;
   p.S = num_splits;
+  p.split_rows = split_rows;
   const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
   p.scale_log2 = (float)(sc * kLog2e);
   hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
@@ -1477,7 +1561,9 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   return launch_status();
 }
 
-int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu) {
+int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
+                    int32_t* split_rows) {
+  if (split_rows != nullptr) *split_rows = 0;
   if (check_dims(dims) != GVA_OK) return 1;
   if (n_cu <= 0) {
     int dev = 0, cu = 0;
@@ -1490,17 +1576,37 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
   if (max_len <= 0 || max_len > dims->t_max) max_len = dims->t_max;
   const long long streams = (long long)dims->batch * dims->n_groups;
   if (total_len <= 0) total_len = (long long)dims->batch * max_len;
-  // One resident workgroup per CU already streams close to the HBM
-  // ceiling, and every split adds a fixed prologue/merge cost of a few
-  // microseconds, so: enough splits to give each CU one workgroup, but no
-  // split shorter than ~1 MB of value rows.
-  long long s = (n_cu + streams - 1) / streams;
   const long long row_bytes = (long long)dims->d_v * (long long)elem_size(dims);
+  const bool spread = 2 * total_len < (long long)dims->batch * max_len;
+  if (spread && split_rows != nullptr) {
+    // Ragged lengths: fixed chunks, so every workgroup streams about the
+    // same bytes whatever its sequence's length.  About kChunkItemsPerCu
+    // chunks per CU, none shorter than kMinChunkBytes of value rows.
+    const long long stream_rows = total_len * dims->n_groups;
+    long long c = (stream_rows + kChunkItemsPerCu * n_cu - 1) / (kChunkItemsPerCu * n_cu);
+    const long long min_rows = (kMinChunkBytes + row_bytes - 1) / row_bytes;
+    if (c < min_rows) c = min_rows;
+    c = (c + kTileRows - 1) / kTileRows * kTileRows;
+    long long s = (max_len + c - 1) / c;
+    if (s > GVA_MAX_SPLITS) {
+      c = ((max_len + GVA_MAX_SPLITS - 1) / GVA_MAX_SPLITS + kTileRows - 1) / kTileRows * kTileRows;
+      s = (max_len + c - 1) / c;
+    }
+    if (s > 1) {
+      *split_rows = (int32_t)c;
+      return (int)s;
+    }
+  }
+  // Even splits.  One resident workgroup per CU already streams close to
+  // the HBM ceiling, and every split adds a fixed prologue/merge cost of a
+  // few microseconds, so: enough splits to give each CU one workgroup, but
+  // no split shorter than ~1 MB of value rows.
+  long long s = (n_cu + streams - 1) / streams;
   const long long max_by_bytes = ((long long)max_len * row_bytes + (1 << 20) - 1) >> 20;
   if (s > max_by_bytes) s = max_by_bytes;
   // Lengths spread widely (mean below half the longest): the longest
   // sequences set the tail, so cut them finer.
-  if (2 * total_len < (long long)dims->batch * max_len) s *= 2;
+  if (spread) s *= 2;
   if (s < 1) s = 1;
   if (s > GVA_MAX_SPLITS) s = GVA_MAX_SPLITS;
   return (int)s;

@@ -59,10 +59,10 @@ def lib() -> ctypes.CDLL:
         D = ctypes.POINTER(GvaDims)
         L.gva_append_kv.argtypes = [D, P, P, P, P, P, P, I32, P]
         L.gva_absorb_query.argtypes = [D, P, P, P, P, P, P]
-        L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, P, P, P]
+        L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
-        L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, P, P, P]
-        L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32]
+        L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, I32, P, P, P]
+        L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32, ctypes.POINTER(I32)]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
@@ -148,7 +148,7 @@ def gva_absorb_query(dims: GvaDims, q, m, lens, q_abs, q_rot, stream=None):
 
 def gva_decode_attention(dims: GvaDims, v_cache, kr_cache, lens, num_splits: int, o_part, lse_part,
                          q=None, m=None, q_abs=None, q_rot=None, v_new=None, kr_new=None,
-                         stream=None):
+                         split_rows: int = 0, stream=None):
     d = dims
     dt = d.torch_dtype
     S = int(num_splits)
@@ -164,6 +164,7 @@ def gva_decode_attention(dims: GvaDims, v_cache, kr_cache, lens, num_splits: int
         _ptr(v_new, "v_new", dt, (d.batch, d.n_groups, d.d_v)),
         _ptr(kr_new, "kr_new", dt, (d.batch, d.d_r)),
         S,
+        int(split_rows),
         _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
         _stream(stream))
@@ -185,7 +186,7 @@ def gva_combine(dims: GvaDims, o_part, lse_part, num_splits: int, o, lse=None, s
 
 
 def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int, o_part,
-                             lse_part, stream=None):
+                             lse_part, split_rows: int = 0, stream=None):
     """The matched-GQA baseline; ``q`` is [B, H, q_stride] with the query's
     first d_v entries used."""
     d = dims
@@ -201,20 +202,31 @@ def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_split
         _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
         _ptr(lens, "lens", torch.int32, (d.batch,)),
         S,
+        int(split_rows),
         _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
         _stream(stream))
     _check("gva_gqa_decode_attention", st)
 
 
-def gva_pick_splits(dims: GvaDims, max_len: int = 0, total_len: int = 0, n_cu: int = 0) -> int:
-    return int(lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(total_len), int(n_cu)))
+def gva_pick_splits(dims: GvaDims, max_len: int = 0, total_len: int = 0, n_cu: int = 0,
+                    chunked: bool = True) -> Tuple[int, int]:
+    """(num_splits, split_rows); ``chunked=False`` asks for even splits only."""
+    rows = ctypes.c_int32(-1)
+    S = lib().gva_pick_splits(ctypes.byref(dims), int(max_len), int(total_len), int(n_cu),
+                              ctypes.byref(rows) if chunked else None)
+    return int(S), (int(rows.value) if chunked else 0)
+
+
+def plan_for(dims: GvaDims, lens: torch.Tensor, n_cu: int = 0, chunked: bool = True) -> Tuple[int, int]:
+    """gva_pick_splits for the lengths in ``lens`` (host copy)."""
+    L = lens.detach().to("cpu", torch.int64).clamp(0, dims.t_max)
+    return gva_pick_splits(dims, int(L.max()) if L.numel() else 0, int(L.sum()), n_cu, chunked)
 
 
 def splits_for(dims: GvaDims, lens: torch.Tensor, n_cu: int = 0) -> int:
-    """gva_pick_splits for the lengths in ``lens`` (host copy)."""
-    L = lens.detach().to("cpu", torch.int64).clamp(0, dims.t_max)
-    return gva_pick_splits(dims, int(L.max()) if L.numel() else 0, int(L.sum()), n_cu)
+    """The even-split count gva_pick_splits picks for ``lens``."""
+    return plan_for(dims, lens, n_cu, chunked=False)[0]
 
 
 def prefer_fused(num_splits: int) -> bool:
@@ -264,7 +276,8 @@ class DecodeBuffers:
 
 def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
            bufs: Optional[DecodeBuffers] = None, fused: Optional[bool] = None,
-           v_new=None, kr_new=None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+           v_new=None, kr_new=None, split_rows: int = 0,
+           stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Absorb + attention + combine for one step; returns (o, lse) fp32.
 
     ``fused`` runs the absorption inside the attention kernel; otherwise
@@ -278,7 +291,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
         fused = prefer_fused(S)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
-    pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None)
+    pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)
     if fused:
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
                              q=q, m=m, stream=stream, **pend)
@@ -295,12 +308,14 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
 
 
 def gqa_decode(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int,
-               bufs: Optional[DecodeBuffers] = None, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+               bufs: Optional[DecodeBuffers] = None, split_rows: int = 0,
+               stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
     """Matched-GQA attention + combine for one step; returns (o, lse) fp32."""
     S = int(num_splits)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
-    gva_gqa_decode_attention(dims, q, k_cache, v_cache, lens, S, bufs.o_part, bufs.lse_part, stream=stream)
+    gva_gqa_decode_attention(dims, q, k_cache, v_cache, lens, S, bufs.o_part, bufs.lse_part,
+                             split_rows=split_rows, stream=stream)
     if S == 1:
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)

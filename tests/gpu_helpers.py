@@ -34,13 +34,15 @@ def upload(inp: Dict[str, torch.Tensor]) -> Dict[str, torch.Tensor]:
     return out
 
 
-def run_decode(w, dev: Dict[str, torch.Tensor], S: int, fused: bool = True, lens=None):
+def run_decode(w, dev: Dict[str, torch.Tensor], S: int, fused: bool = True, lens=None,
+               split_rows: int = 0):
     """Absorb + attention + combine on the GPU; returns CPU tensors
     (o, lse, o_part, lse_part)."""
     d = dims_of(w)
     L = dev["lens"] if lens is None else lens
     bufs = gva.DecodeBuffers(d, S)
-    o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], L, S, bufs=bufs, fused=fused)
+    o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], L, S, bufs=bufs, fused=fused,
+                        split_rows=split_rows)
     torch.cuda.synchronize()
     return o.cpu(), lse.cpu(), bufs.o_part.cpu(), bufs.lse_part.cpu()
 

@@ -34,7 +34,7 @@ def test_library_exports_every_declared_symbol():
     lib = gva.lib()
     for name in declared_functions():
         assert hasattr(lib, name), name
-    assert gva.gva_version() == 10300
+    assert gva.gva_version() == 10400
 
 
 def test_status_strings():
@@ -52,8 +52,10 @@ def dims(**kw):
     return gva.make_dims(**base)
 
 
-def decode_status(d, S=4, q=A, m=A, qa=None, qr=None, v=A, kr=A, lens=A, op=A, lp=A, vn=None, kn=None):
-    return gva.lib().gva_decode_attention(ctypes.byref(d), q, m, qa, qr, v, kr, lens, vn, kn, S, op, lp, None)
+def decode_status(d, S=4, q=A, m=A, qa=None, qr=None, v=A, kr=A, lens=A, op=A, lp=A, vn=None, kn=None,
+                  rows=0):
+    return gva.lib().gva_decode_attention(ctypes.byref(d), q, m, qa, qr, v, kr, lens, vn, kn, S, rows,
+                                          op, lp, None)
 
 
 @pytest.mark.parametrize("kw", [
@@ -71,6 +73,8 @@ def test_bad_split_counts_rejected():
     d = dims()
     assert decode_status(d, S=0) == gva.GVA_ERR_INVALID_ARG
     assert decode_status(d, S=gva.GVA_MAX_SPLITS + 1) == gva.GVA_ERR_INVALID_ARG
+    assert decode_status(d, rows=-32) == gva.GVA_ERR_INVALID_ARG          # split_rows < 0
+    assert decode_status(d, rows=48) == gva.GVA_ERR_INVALID_ARG           # not whole 32-row tiles
     lib = gva.lib()
     assert lib.gva_combine(ctypes.byref(d), A, A, 0, A, None, None) == gva.GVA_ERR_INVALID_ARG
 
@@ -128,17 +132,33 @@ def test_absorb_validation():
 
 def test_pick_splits_is_host_only_and_bounded():
     d = dims(batch=32, n_heads=32, n_groups=8, t_max=8192)
-    assert gva.gva_pick_splits(d, 8192, 0, 256) == 1       # 256 streams fill 256 CUs
-    assert gva.gva_pick_splits(d, 100, 0, 256) == 1        # short sequences: no split
+    assert gva.gva_pick_splits(d, 8192, 0, 256) == (1, 0)       # 256 streams fill 256 CUs
+    assert gva.gva_pick_splits(d, 100, 0, 256) == (1, 0)        # short sequences: no split
     d3 = dims(batch=4, n_heads=32, n_groups=8, t_max=131072, d_r=32)
-    assert gva.gva_pick_splits(d3, 131072, 0, 256) == 8    # few long streams
+    assert gva.gva_pick_splits(d3, 131072, 0, 256) == (8, 0)    # few long streams
     d4 = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
-    even = gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)
-    spread = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256)
-    assert spread == 2 * even                              # widely spread lengths
+    even, _ = gva.gva_pick_splits(d4, 32768, 64 * 32768, 256, chunked=False)
+    spread, _ = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256, chunked=False)
+    assert spread == 2 * even                                   # widely spread lengths
     for S in (even, spread):
         assert 1 <= S <= gva.GVA_MAX_SPLITS
     assert not gva.prefer_fused(4) and gva.prefer_fused(1)
+
+
+def test_pick_splits_fixed_chunks_for_ragged_lengths():
+    d4 = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
+    S, rows = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256)
+    assert rows > 0 and rows % 32 == 0
+    assert S == -(-32768 // rows) and S <= gva.GVA_MAX_SPLITS  # every row of the longest covered
+    # chunks of about two per CU, none under 128 KiB of value rows
+    assert rows * 128 * 2 >= 128 << 10
+    assert rows <= 2 * (64 * 6000 * 2) // (2 * 256) + 32
+    # uniform lengths keep even splits
+    assert gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)[1] == 0
+    # a very long, very ragged batch stays within GVA_MAX_SPLITS
+    d5 = dims(batch=256, n_heads=8, n_groups=8, t_max=1 << 20, d_v=64)
+    S5, rows5 = gva.gva_pick_splits(d5, 1 << 20, 256 * 1000, 256)
+    assert 1 <= S5 <= gva.GVA_MAX_SPLITS and S5 * rows5 >= 1 << 20
 
 
 def test_tiled_layout_matches_header_formula():
@@ -156,9 +176,10 @@ def test_tiled_layout_matches_header_formula():
     assert torch.equal(gva.untiled(gva.tiled(z)), z)
 
 
-def gqa_status(d, q=A, stride=None, k=A, v=A, lens=A, S=2, op=A, lp=A):
+def gqa_status(d, q=A, stride=None, k=A, v=A, lens=A, S=2, op=A, lp=A, rows=0):
     stride = d.d_v + 16 if stride is None else stride
-    return gva.lib().gva_gqa_decode_attention(ctypes.byref(d), q, stride, k, v, lens, S, op, lp, None)
+    return gva.lib().gva_gqa_decode_attention(ctypes.byref(d), q, stride, k, v, lens, S, rows, op, lp,
+                                              None)
 
 
 def test_gqa_validation():
@@ -166,7 +187,7 @@ def test_gqa_validation():
     assert gqa_status(dims(batch=0)) == gva.GVA_ERR_INVALID_ARG
     for kw in (dict(q=None), dict(k=None), dict(v=None), dict(lens=None), dict(op=None),
                dict(lp=None), dict(k=A + 2), dict(op=A + 4), dict(S=0),
-               dict(S=gva.GVA_MAX_SPLITS + 1), dict(stride=64)):
+               dict(S=gva.GVA_MAX_SPLITS + 1), dict(stride=64), dict(rows=-32), dict(rows=40)):
         assert gqa_status(d, **kw) == gva.GVA_ERR_INVALID_ARG, kw
     assert gqa_status(dims(dtype="f32")) == gva.GVA_ERR_UNSUPPORTED          # bf16 only
     assert gqa_status(dims(d_v=96), stride=96) == gva.GVA_ERR_UNSUPPORTED

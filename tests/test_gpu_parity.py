@@ -55,15 +55,17 @@ def test_split_partials_match_oracle(name):
     w = gva_inputs.workload(name)
     inp = gva_inputs.make_inputs(w, 5, lens=torch.tensor([w.t_max - 7] + [w.t_max // 3] * (w.batch - 1)))
     dev = upload(inp)
-    for S in (2, 7):
-        note(f"{name} partials S={S}")
-        _, _, o_part, lse_part = run_decode(w, dev, S)
-        begins, ends = oracle.split_bounds(inp["lens"], S, tile=32)
+    for S, rows in ((2, 0), (7, 0), (5, 64), (3, 96)):
+        note(f"{name} partials S={S} split_rows={rows}")
+        _, _, o_part, lse_part = run_decode(w, dev, S, split_rows=rows)
+        begins, ends = oracle.split_bounds(inp["lens"], S, tile=32, split_rows=rows)
         for s in range(S):
             o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
                                            t_begin=begins[s], t_end=ends[s])
-            err = max_abs(o_part[:, :, s], o_ref)
-            assert err <= QUALITY[w.dtype], (S, s, err)
+            # an empty split past the first writes only its lse
+            live = (ends[s] > begins[s]) | (s == 0)
+            err = max_abs(o_part[live][:, :, s], o_ref[live])
+            assert err <= QUALITY[w.dtype], (S, rows, s, err)
             assert lse_err(lse_part[:, :, s], lse_ref) <= 1e-3
 
 
@@ -254,10 +256,10 @@ def test_full_size_sampled(name):
     note(f"{name}: drawing inputs")
     inp = gva_inputs.make_inputs(w, 0)
     d = dims_of(w)
-    S = gva.splits_for(d, inp["lens"])
+    S, rows = gva.plan_for(d, inp["lens"])     # the launch configuration bench.py times
     dev = upload({k: inp[k] for k in ("q", "m", "v", "kr", "lens")})
-    note(f"{name}: decode S={S}")
-    o, lse, _, _ = run_decode(w, dev, S)
+    note(f"{name}: decode S={S} split_rows={rows}")
+    o, lse, _, _ = run_decode(w, dev, S, fused=gva.prefer_fused(S), split_rows=rows)
     del dev
     torch.cuda.empty_cache()
     # the oracle on a sample of sequences: first, last, longest, shortest
@@ -341,11 +343,11 @@ def test_gqa_baseline_matches_oracle(hpg, dv):
     o_ref, lse_ref = oracle.gqa_decode(inp["q"], inp["k_gqa"], inp["v"], inp["lens"], d_k=dv)
     dev = upload(inp)
     d = dims_of(w)
-    for S in (1, 3, 8):
-        note(f"gqa hpg={hpg} dv={dv} S={S}")
-        o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S)
+    for S, rows in ((1, 0), (3, 0), (8, 0), (10, 32), (3, 64)):
+        note(f"gqa hpg={hpg} dv={dv} S={S} split_rows={rows}")
+        o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S, split_rows=rows)
         torch.cuda.synchronize()
-        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"gqa/hpg{hpg}/dv{dv}/S{S}")
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"gqa/hpg{hpg}/dv{dv}/S{S}/rows{rows}")
 
 
 def test_gqa_baseline_partials_and_untouched_caches():
@@ -367,7 +369,9 @@ def test_gqa_baseline_partials_and_untouched_caches():
         for b in range(w.batch):
             a, e = int(lo[b]), int(hi[b])
             if a >= e:
-                assert torch.all(op[b, :, s] == 0) and torch.all(lp[b, :, s] == float("-inf"))
+                assert torch.all(lp[b, :, s] == float("-inf"))
+                if s == 0:
+                    assert torch.all(op[b, :, s] == 0)
                 continue
             sl = slice(b, b + 1)
             o_ref, lse_ref = oracle.gqa_decode(inp["q"][sl], inp["k_gqa"][sl, :, a:e].contiguous(),
@@ -383,10 +387,10 @@ def test_gqa_baseline_full_size_sampled():
     note("ragged_b64 gqa: drawing inputs")
     inp = gva_inputs.make_inputs(w, 0)
     d = dims_of(w)
-    S = gva.splits_for(d, inp["lens"])
+    S, rows = gva.plan_for(d, inp["lens"])
     dev = upload({k: inp[k] for k in ("q", "v", "k_gqa", "lens")})
-    note(f"ragged_b64 gqa: decode S={S}")
-    o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S)
+    note(f"ragged_b64 gqa: decode S={S} split_rows={rows}")
+    o, lse = gva.gqa_decode(d, dev["q"], dev["k_gqa"], dev["v"], dev["lens"], S, split_rows=rows)
     o, lse = o.cpu(), lse.cpu()
     del dev
     torch.cuda.empty_cache()
@@ -398,3 +402,69 @@ def test_gqa_baseline_full_size_sampled():
     idx = torch.tensor(picks)
     _check(w, o[idx], lse[idx], o_ref, lse_ref, "ragged_b64 gqa/sampled")
     assert torch.isfinite(o).all()
+
+
+
+# ------------------------------------------- fixed-chunk splits (ragged batches)
+@pytest.mark.parametrize("dtype", ["bf16", "f32"])
+@pytest.mark.parametrize("fused", [True, False])
+def test_fixed_chunk_splits_match_oracle(dtype, fused):
+    # every split of every sequence gets split_rows rows; too few splits
+    # leave the remainder to the last one; empty splits write only their lse
+    w = gva_inputs.Workload("chunks", 6, 1024, 16, 2, 128 if dtype == "bf16" else 64, 64, 16,
+                            dtype=dtype)
+    lens = torch.tensor([1024, 1, 0, 333, 64, 700], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 21, lens=lens)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"])
+    dev = upload(inp)
+    plan = gva.plan_for(dims_of(w), inp["lens"])
+    for S, rows in sorted({(32, 32), (8, 128), (2, 128), (1, 64), plan}):
+        note(f"chunks {dtype} fused={fused} S={S} split_rows={rows}")
+        o, lse, _, _ = run_decode(w, dev, S, fused=fused, split_rows=rows)
+        _check(w, o, lse, o_ref, lse_ref, f"chunks/{dtype}/fused={fused}/S{S}/rows{rows}")
+
+
+def test_fixed_chunks_with_current_row():
+    # the append folded into the attention launch, with fixed chunks: the
+    # chunk holding row len-1 appends it
+    w = gva_inputs.Workload("chunks_pending", 4, 512, 8, 2, 128, 128, 16)
+    lens = torch.tensor([512, 97, 1, 256], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 23, lens=lens)
+    seq = torch.arange(w.batch, dtype=torch.int32)
+    pos = (lens - 1).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"])
+    d = dims_of(w)
+    for S, rows in ((16, 32), (3, 96)):
+        note(f"chunks + current row S={S} split_rows={rows}")
+        dev = upload(inp)
+        o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S,
+                            v_new=dev["v_new"], kr_new=dev["kr_new"], split_rows=rows)
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"chunks+current/S{S}/rows{rows}")
+        assert torch.equal(gva.untiled(dev["v"].cpu()).view(torch.int16), v_ref.view(torch.int16))
+        assert torch.equal(gva.untiled(dev["kr"].cpu()).view(torch.int16), k_ref.view(torch.int16))
+
+
+def test_combine_never_reads_empty_partials():
+    # partials of empty splits hold NaN: a combine that read them would
+    # return NaN
+    g = torch.Generator().manual_seed(9)
+    B, H, S, dv = 3, 4, 70, 128
+    o_part = torch.randn(B, H, S, dv, generator=g)
+    lse_part = torch.randn(B, H, S, generator=g) * 3
+    lse_part[0, :, 5:] = -math.inf
+    lse_part[1, :, ::3] = -math.inf
+    lse_part[2, 1, :] = -math.inf
+    o_ref, lse_ref = oracle.combine(o_part, lse_part)
+    o_part[torch.isneginf(lse_part)] = float("nan")
+    w = gva_inputs.Workload("combine", B, 64, H, 1, dv, 64, 0)
+    o = torch.empty(B, H, dv, device="cuda")
+    lse = torch.empty(B, H, device="cuda")
+    note("combine, NaN in empty partials")
+    gva.gva_combine(dims_of(w), o_part.cuda(), lse_part.cuda(), S, o, lse)
+    torch.cuda.synchronize()
+    assert torch.isfinite(o.cpu()).all()
+    assert max_abs(o.cpu(), o_ref) <= 1e-5
+    assert lse_err(lse.cpu(), lse_ref) <= 1e-5

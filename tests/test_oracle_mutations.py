@@ -35,7 +35,8 @@ PIN_TESTS = [
     lambda o: pins.test_two_rows_closed_form(o),
     lambda o: pins.test_rope_matches_complex_form_and_invariants(o),
     lambda o: pins.test_position_shift_leaves_output_unchanged(o),
-    lambda o: pins.test_split_and_combine_equals_unsplit(o, 3),
+    lambda o: pins.test_split_and_combine_equals_unsplit(o, 3, 0),
+    lambda o: pins.test_split_and_combine_equals_unsplit(o, 5, 32),
     lambda o: pins.test_round_bf16_single_rounding(o),
     lambda o: pins.test_zero_query_gives_mean_value(o),
 ]

@@ -258,11 +258,14 @@ def test_position_shift_leaves_output_unchanged(orc):
 
 
 # ----------------------------------------------------------- split/combine
-@pytest.mark.parametrize("S", [1, 2, 3, 7, 64])
-def test_split_and_combine_equals_unsplit(orc, S):
+@pytest.mark.parametrize("S,rows", [(1, 0), (2, 0), (3, 0), (7, 0), (64, 0),
+                                    (5, 32), (2, 32), (20, 8), (1, 64)])
+def test_split_and_combine_equals_unsplit(orc, S, rows):
+    # even splits, and fixed chunks (including too few splits, where the
+    # last split takes every remaining row)
     q, m, v, kr, lens = tiny_inputs(47, T=150, lens=[150, 61])
     o, lse = orc.decode(q, m, v, kr, lens)
-    begins, ends = orc.split_bounds(lens, S, tile=8)
+    begins, ends = orc.split_bounds(lens, S, tile=8, split_rows=rows)
     parts = [orc.decode(q, m, v, kr, lens, t_begin=bg, t_end=en) for bg, en in zip(begins, ends)]
     o_part = torch.stack([p[0] for p in parts], dim=2)     # [B,H,S,dv]
     lse_part = torch.stack([p[1] for p in parts], dim=2)   # [B,H,S]
@@ -271,15 +274,18 @@ def test_split_and_combine_equals_unsplit(orc, S):
     assert torch.allclose(lc, lse, rtol=0, atol=1e-12)
 
 
-def test_split_bounds_cover_each_sequence(orc):
+@pytest.mark.parametrize("rows", [0, 32, 256])
+def test_split_bounds_cover_each_sequence(orc, rows):
     lens = torch.tensor([0, 1, 31, 32, 33, 1000, 8192], dtype=torch.int32)
     for S in (1, 2, 5, 16):
-        begins, ends = orc.split_bounds(lens, S, tile=32)
+        begins, ends = orc.split_bounds(lens, S, tile=32, split_rows=rows)
         for b in range(lens.numel()):
             covered = []
             for s in range(S):
                 bg, en = int(begins[s][b]), int(ends[s][b])
                 assert bg % 32 == 0 or bg == int(lens[b])
+                if rows and s < S - 1:
+                    assert en - bg <= rows          # fixed chunks, the last takes the rest
                 covered.extend(range(bg, en))
             assert covered == list(range(int(lens[b])))
 
