@@ -150,7 +150,16 @@ def cpu_baseline(w, inp, seq, pos, budget_s: float = 20.0, min_s: float = 10.0):
                 t_used += dt
                 nbytes += nb
             passes += 1
+    # the same oracle on one thread, one sequence (the longest), for scale
+    b1 = int(inp["lens"].argmax())
+    sl = slice(b1, b1 + 1)
+    t0 = time.perf_counter()
+    oracle.decode(inp["q"][sl], inp["m"], v[sl], kr[sl], inp["lens"][sl], rope_base=w.rope_base,
+                  n_threads=1)
+    t1 = time.perf_counter() - t0
+    nb1 = traffic.decode_bytes(inp["lens"][sl], 1, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, esize)
     rec = {"value": nbytes / t_used / 1e9, "unit": "GB/s", "cores": threads, "kind": "oracle",
+           "value_1_thread": nb1 / t1 / 1e9,
            "seconds": round(t_used, 3),
            "sample": f"fp64 oracle decode of {len(done)} of {w.batch} sequences "
                      f"(all {w.n_heads} heads, full length) after the step's append"
@@ -332,6 +341,7 @@ def main():
     torch.cuda.synchronize()
     kt = sorted(a.elapsed_time(b) for a, b in evs)
     decode_ms = sum(kt) / len(kt)
+    achievable, probe_wg = gva.probe_read_bandwidth(stream=stream)
 
     step_b = traffic.step_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
                                 appended_rows=w.batch)
@@ -369,7 +379,11 @@ def main():
             "traffic": measured_traffic(w.name, S),
             "algorithmic_bytes_per_launch": dec_b,
             "avg_launch_ms": round(decode_ms, 5),
+            "median_launch_ms": round(kt[len(kt) // 2], 5),
             "p10_p90_launch_ms": [round(kt[len(kt) // 10], 5), round(kt[(9 * len(kt)) // 10], 5)],
+            "achievable_read_GBps": round(achievable, 1),
+            "frac_of_achievable": round(achieved / achievable, 4),
+            "achievable_probe": f"gva_probe_read, 2 GiB, {probe_wg} workgroups",
         },
         "cpu_baseline": None,
     }

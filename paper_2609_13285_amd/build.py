@@ -1,6 +1,7 @@
 """Build libgva.so (HIP, gfx950) in-tree with hipcc.
 
-``python -m paper_2609_13285_amd.build`` compiles ``csrc/gva.hip`` into
+``python -m paper_2609_13285_amd.build`` compiles ``csrc/gva.hip`` (the
+decode path) and ``csrc/probe.hip`` (the read-bandwidth probe) into
 ``paper_2609_13285_amd/libgva.so``.  Packed-FP32 instructions are disabled
 for the device code (``-packed-fp32-ops``); hipcc's host pass warns that it
 does not know that feature, which is harmless.
@@ -15,7 +16,7 @@ import sys
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 ROOT = os.path.dirname(HERE)
-SRC = os.path.join(HERE, "csrc", "gva.hip")
+SRCS = [os.path.join(HERE, "csrc", "gva.hip"), os.path.join(HERE, "csrc", "probe.hip")]
 LIB = os.path.join(HERE, "libgva.so")
 ARCH = "gfx950"
 
@@ -32,7 +33,7 @@ def build(verbose: bool = False) -> str:
     cmd = [hipcc(), f"--offload-arch={ARCH}", "-O3", "-std=c++17", "-fPIC", "-shared",
            "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
            "-Wno-unused-command-line-argument",
-           "-I", os.path.join(ROOT, "include"), SRC, "-o", tmp]
+           "-I", os.path.join(ROOT, "include"), *SRCS, "-o", tmp]
     res = subprocess.run(cmd, capture_output=True, text=True)
     if res.returncode != 0:
         sys.stderr.write(res.stdout + res.stderr)

@@ -22,6 +22,7 @@ GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
            "gva_gqa_decode_attention", "gva_pick_splits", "gva_status_string", "gva_version")
+PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
 
 class GvaError(RuntimeError):
@@ -66,8 +67,9 @@ def lib() -> ctypes.CDLL:
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
+        L.gva_probe_read.argtypes = [P, ctypes.c_int64, I32, P, P]
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
-                     "gva_gqa_decode_attention", "gva_pick_splits", "gva_version"):
+                     "gva_gqa_decode_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -320,3 +322,30 @@ def gqa_decode(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int,
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
     return bufs.o, bufs.lse
+
+
+def probe_read_bandwidth(nbytes: int = 2 << 30, reps: int = 10, stream=None) -> Tuple[float, int]:
+    """Achievable HBM streaming-read GB/s (gva_probe_read): the best of a few
+    workgroup counts over a ``nbytes`` buffer (larger than the 256 MB
+    last-level cache).  Returns (GB/s, workgroups of the best run)."""
+    buf = torch.empty(nbytes // 4, dtype=torch.int32, device="cuda").fill_(1)
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = _stream(stream)
+    n_cu = torch.cuda.get_device_properties(buf.device).multi_processor_count
+    best = (0.0, 0)
+    for per_cu in (2, 4, 8, 16):
+        wg = per_cu * n_cu
+        _check("gva_probe_read", lib().gva_probe_read(ctypes.c_void_p(buf.data_ptr()), nbytes, wg,
+                                                      ctypes.c_void_p(sink.data_ptr()), st))
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        a.record()
+        for _ in range(reps):
+            lib().gva_probe_read(ctypes.c_void_p(buf.data_ptr()), nbytes, wg,
+                                 ctypes.c_void_p(sink.data_ptr()), st)
+        b.record()
+        torch.cuda.synchronize()
+        gbs = nbytes * reps / (a.elapsed_time(b) * 1e-3) / 1e9
+        if gbs > best[0]:
+            best = (gbs, wg)
+    del buf
+    return best

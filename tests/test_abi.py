@@ -17,8 +17,8 @@ HEADER = os.path.join(ROOT, "include", "gva.h")
 A = 0x10000
 
 
-def declared_functions():
-    text = open(HEADER).read()
+def declared_functions(header=HEADER):
+    text = open(header).read()
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"^\s*(?:const\s+)?\w+\s*\*?\s*(gva_\w+)\s*\(", text, flags=re.M)))
 
@@ -32,8 +32,12 @@ def test_header_declares_the_four_calls():
 
 def test_library_exports_every_declared_symbol():
     lib = gva.lib()
-    for name in declared_functions():
+    probe_header = os.path.join(ROOT, "include", "gva_probe.h")
+    assert set(declared_functions(probe_header)) == set(gva.PROBE_EXPORTS)
+    for name in declared_functions() + declared_functions(probe_header):
         assert hasattr(lib, name), name
+    # every header under include/ is one of the two
+    assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["gva.h", "gva_probe.h"]
     assert gva.gva_version() == 10400
 
 
@@ -194,3 +198,11 @@ def test_gqa_validation():
     assert gqa_status(dims(n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED   # H/G = 16
     assert gqa_status(d, stride=132) == gva.GVA_ERR_UNSUPPORTED             # 16-byte query rows
     assert gqa_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED
+
+
+def test_probe_validation():
+    lib = gva.lib()
+    assert lib.gva_probe_read(None, 1 << 20, 8, A, None) == 1
+    assert lib.gva_probe_read(A, 8, 8, A, None) == 1            # under one 16-byte piece
+    assert lib.gva_probe_read(A, 1 << 20, 0, A, None) == 1
+    assert lib.gva_probe_read(A + 4, 1 << 20, 8, A, None) == 1
