@@ -184,6 +184,65 @@ def timed(step, steps: int, stream) -> float:
     return t_start.elapsed_time(t_end) / steps
 
 
+def layer_stack(args, w, inp, d, S, split_rows, fused, dec_b):
+    """An N-layer decode step (the step of one token through N attention
+    layers, each with its own caches, query and maps), timed eagerly and as
+    one captured HIP graph.  The library allocates, synchronises and clears
+    nothing, so its launches are captured as they are.  Sets of layer caches
+    rotate like the single-layer caches so no step finds its rows in the
+    MALL."""
+    n = args.layers
+    n_sets = min(8, max(2, math.ceil(2 * MALL_BYTES / (n * dec_b))))
+    v_t, kr_t = gva.tiled(inp["v"]), gva.tiled(inp["kr"])
+    small = {k: inp[k].cuda() for k in ("q", "m", "lens", "v_new", "kr_new")}
+    layers = []
+    for _ in range(n):
+        layer = {k: t.clone() for k, t in small.items()}
+        layer["caches"] = [(v_t.cuda(), kr_t.cuda()) for _ in range(n_sets)]
+        layer["bufs"] = gva.DecodeBuffers(d, S)
+        layer["q_abs"] = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+        layer["q_rot"] = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+        layers.append(layer)
+    del v_t, kr_t
+
+    def run(i):
+        st = torch.cuda.current_stream()      # the capture stream while capturing
+        for L in layers:
+            vc, kc = L["caches"][i % n_sets]
+            pend = dict(v_new=L["v_new"], kr_new=L["kr_new"] if w.d_r > 0 else None,
+                        split_rows=split_rows)
+            if fused:
+                gva.gva_decode_attention(d, vc, kc, L["lens"], S, L["bufs"].o_part, L["bufs"].lse_part,
+                                         q=L["q"], m=L["m"], stream=st, **pend)
+            else:
+                gva.gva_absorb_query(d, L["q"], L["m"], L["lens"], L["q_abs"], L["q_rot"], st)
+                gva.gva_decode_attention(d, vc, kc, L["lens"], S, L["bufs"].o_part, L["bufs"].lse_part,
+                                         q_abs=L["q_abs"], q_rot=L["q_rot"] if w.d_r > 0 else None,
+                                         stream=st, **pend)
+            if S > 1:
+                gva.gva_combine(d, L["bufs"].o_part, L["bufs"].lse_part, S, L["bufs"].o, L["bufs"].lse, st)
+
+    stream = torch.cuda.current_stream()
+    for i in range(args.warmup):
+        run(i)
+    eager_ms = timed(run, args.steps, stream)
+    graphs = []
+    for c in range(n_sets):
+        g = torch.cuda.CUDAGraph()
+        with torch.cuda.graph(g):
+            run(c)
+        graphs.append(g)
+    for i in range(args.warmup):
+        graphs[i % n_sets].replay()
+    graph_ms = timed(lambda i: graphs[i % n_sets].replay(), args.steps, stream)
+    launches = n * ((0 if fused else 1) + 1 + (1 if S > 1 else 0))
+    return {"n_layers": n, "launches_per_step": launches, "cache_sets": n_sets,
+            "eager_ms_per_step": round(eager_ms, 5), "graph_ms_per_step": round(graph_ms, 5),
+            "eager_us_per_layer": round(eager_ms * 1000 / n, 2),
+            "graph_us_per_layer": round(graph_ms * 1000 / n, 2),
+            "graph_GBps": round(n * dec_b / (graph_ms * 1e-3) / 1e9, 1)}
+
+
 def gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches, stream):
     """Attention only (the caches as stored, no append), GVA against the
     matched GQA baseline on the same values, lengths and query content
@@ -257,6 +316,9 @@ def main():
     ap.add_argument("--cache-copies", type=int, default=0,
                     help="cache copies the steps rotate through (0: enough that the bytes one "
                          "rotation streams exceed twice the 256 MB last-level cache, at least 2)")
+    ap.add_argument("--layers", type=int, default=0,
+                    help="also time an N-layer decode step (each layer its own caches, query "
+                         "and maps) eagerly and as one HIP graph replay")
     ap.add_argument("--no-gqa", action="store_true",
                     help="skip the matched-GQA comparison on workloads that carry a GQA key cache")
     args = ap.parse_args()
@@ -300,7 +362,7 @@ def main():
     seq = torch.arange(w.batch, dtype=torch.int32)
     pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
     bufs = gva.DecodeBuffers(d, S)
-    fused = gva.prefer_fused(S) if args.absorb == "auto" else args.absorb == "fused"
+    fused = gva.prefer_fused(d, S) if args.absorb == "auto" else args.absorb == "fused"
     q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
     q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()
@@ -389,6 +451,8 @@ def main():
     }
 
     o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
+    if args.layers > 0:
+        out["layer_stack"] = layer_stack(args, w, inp, d, S, split_rows, fused, dec_b)
     if w.gqa and not args.no_gqa:
         out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches,
                                                stream)

@@ -153,6 +153,10 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
  * kernel absorbs and rotates it itself ahead of the attention loop (the
  * fused path) -- or pre-absorbed by gva_absorb_query: q/m NULL, q_abs
  * [B][H][d_v] fp32 and (if d_r > 0) q_rot [B][H][d_r] fp32 non-NULL.
+ * In the fused path every workgroup absorbs its group's heads itself: it
+ * suits launches of at most one workgroup per CU (B * G * num_splits) and
+ * few splits; otherwise one gva_absorb_query call and the pre-absorbed
+ * path cost less than every workgroup absorbing the same heads again.
  * The current token, appended and attended in one launch (optional):
  * v_new [B][G][d_v] and kr_new [B][d_r] (unrotated, storage dtype, as for
  * gva_append_kv) are the rows of position lens[b]-1 of every sequence with

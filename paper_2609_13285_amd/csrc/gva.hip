@@ -89,7 +89,7 @@ struct AbsorbParams {
   double inv_freq[kMaxPairs];
 };
 
-struct DecodeParams {
+struct DecodeArgs {
   const void* q;          // fused path: raw query and maps
   const void* m;
   const float* q_abs;     // pre-absorbed path
@@ -107,6 +107,10 @@ struct DecodeParams {
   int32_t split_rows;     // fixed rows per split (0: the even rule)
   float scale_log2;       // score scale * log2(e): softmax runs in base 2
   int32_t fused;
+};
+
+struct DecodeParams {
+  DecodeArgs a;           // scalars and pointers: read into registers at once
   double inv_freq[kMaxPairs];
 };
 
@@ -207,21 +211,33 @@ __device__ __forceinline__ int xcd_remap(int x, int n) {
 //    by b: the XCDs get near-equal shares of a ragged batch.  The grid is
 //    B * S8 * G with S8 = S rounded up to 8; workgroups whose s >= S are
 //    padding and return false.
-__device__ __forceinline__ bool work_item(const DecodeParams& p, int& b, int& s, int& g) {
-  if (p.split_rows > 0) {
-    const int x = blockIdx.x, xcd = x & 7, slot = x >> 3;
-    g = slot % p.G;
-    const int t = slot / p.G;
-    b = t % p.B;
-    s = 8 * (t / p.B) + ((xcd - (b & 7)) & 7);
-    return s < p.S;
-  }
-  const int item = xcd_remap(blockIdx.x, gridDim.x);
-  g = item % p.G;
-  const int bs = item / p.G;
-  s = bs % p.S;
-  b = bs / p.S;
-  return true;
+// Every scalar argument the decode prologue needs, requested here in one
+// round trip: left to itself the compiler fetches them where first used,
+// several dependent kernel-argument round trips deep.  The memory clobber
+// keeps the loads that follow after this point.
+template <bool RAW_QUERY>
+__device__ __forceinline__ void request_args(const DecodeArgs& a) {
+  asm volatile("" ::"s"(a.B), "s"(a.H), "s"(a.G), "s"(a.S), "s"(a.t_max), "s"(a.split_rows), "s"(a.d_r),
+               "s"(a.d_c), "s"(a.lens), "s"(a.v_new), "s"(a.kr_new),
+               "s"(RAW_QUERY ? static_cast<const void*>(a.q) : static_cast<const void*>(a.q_abs)),
+               "s"(RAW_QUERY ? a.m : static_cast<const void*>(a.q_rot)), "s"(gridDim.x)
+               : "memory");
+}
+
+// Both orders are computed and one is selected, so no branch waits on the
+// split mode before the other kernel arguments are requested.
+__device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g) {
+  const int x = blockIdx.x, xcd = x & 7, slot = x >> 3;
+  const int gc = slot % p.G, t = slot / p.G;
+  const int bc = t % p.B;
+  const int sc = 8 * (t / p.B) + ((xcd - (bc & 7)) & 7);
+  const int item = xcd_remap(x, gridDim.x);
+  const int ge = item % p.G, bs = item / p.G;
+  const bool chunked = p.split_rows > 0;
+  g = chunked ? gc : ge;
+  b = chunked ? bc : bs / p.S;
+  s = chunked ? sc : bs % p.S;
+  return !chunked || sc < p.S;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -467,36 +483,130 @@ struct Tile {
 // stream per group instead of the value rows, with no positional term and
 // the raw query; P.V, the softmax, the splits and the layout are shared, so
 // the two kernels differ only in the bytes they must stream.
-template <int HPG, int DV, int NRC, bool GQA = false>
+template <int HPG, int DV, int NRC, bool GQA, bool FUSED>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
+  static_assert(!(GQA && FUSED), "the GQA baseline takes the raw query");
+  const DecodeArgs a = p.a;
+  request_args<FUSED || GQA>(a);
   using Cfg = DecodeCfg<HPG, DV, NRC>;
   using TileT = Tile<DV, NRC, GQA>;
   constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
   int b, s, g;
-  if (!work_item(p, b, s, g)) return;          // grid padding (fixed chunks)
+  if (!work_item(a, b, s, g)) return;          // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform (SGPR)
   const int n = lane & 15, qd = lane >> 4;     // MFMA column / row slot and 16-lane row
   const int h0 = g * HPG;
-  const int L = clamp_len(p.lens, b, p.t_max);
-  int r0, r1;
-  split_rows(L, p.S, p.split_rows, s, r0, r1);
-  if (r0 >= r1 && s > 0) {                     // an empty split past the first: lse only
-    if (tid < HPG) p.lse_part[((int64_t)b * p.H + h0 + tid) * p.S + s] = -INFINITY;
-    return;
-  }
-  // With the current token's rows given, the split holding row L-1 takes
-  // that row from them and streams only the rows before it from the cache.
-  const bool pending = !GQA && p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
-  if (pending) r1 = L - 1;
-  const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
-
   // Column roles: [hi_0 .. hi_{HPG-1}, lo_{HPG-1} .. lo_0, zero padding].
   const bool active = n < 2 * HPG;
   const bool is_lo = n >= HPG;
   const int col_head = !active ? 0 : (is_lo ? 2 * HPG - 1 - n : n);
+  const int hq = h0 + col_head;
+  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+  __shared__ __attribute__((aligned(16))) uint16_t prow[DV + 32 * (NRC > 0 ? NRC : 1)];
+
+  // The rows of this split are settled once the query loads are on their
+  // way (they do not depend on the length), which takes a memory round trip
+  // off the prologue.  The length is a scalar load through the constant
+  // address space, requested here and waited for at first use.
+  const int len_b = *(const __attribute__((address_space(4))) int32_t*)(a.lens + b);
+  int L = 0, r0 = 0, r1 = 0;
+  auto settle_rows = [&]() {
+    L = len_b < 0 ? 0 : (len_b > a.t_max ? a.t_max : len_b);
+    split_rows(L, a.S, a.split_rows, s, r0, r1);
+    return r0 < r1 || s == 0;
+  };
+  auto write_empty = [&]() {                   // an empty split past the first: lse only
+    if (tid < HPG) a.lse_part[((int64_t)b * a.H + h0 + tid) * a.S + s] = -INFINITY;
+  };
+  if (a.split_rows > 0 && s > 0) {
+    // Fixed chunks of a ragged batch leave many splits empty: those return
+    // before any load.  (A volatile load of its own, so the compiler cannot
+    // merge it with the length used below and wait for that one up here.)
+    const int lc = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const volatile int32_t*>(a.lens + b));
+    const int Lc = lc < 0 ? 0 : (lc > a.t_max ? a.t_max : lc);
+    if ((long long)a.split_rows * s >= Lc) {
+      write_empty();
+      return;
+    }
+  }
+
+  // ---- loads that do not depend on the length, oldest first: the current
+  // token's rows (staged first, below), then the query.  Loads retire in
+  // order, so waiting for them never waits for the tiles requested later.
+  // (kept as loaded bits: converting them here would wait for them here)
+  u32x4 pend_piece = {0u, 0u, 0u, 0u};
+  uint32_t pend_kbits = 0u;
+  if (!GQA && a.v_new != nullptr) {
+    if (tid < DV / 8)
+      pend_piece = *(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_new) + ((int64_t)b * a.G + g) * DV) + tid);
+    if (tid < a.d_r / 2)
+      pend_kbits = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(a.kr_new) + (int64_t)b * a.d_r + 2 * tid);
+  }
+  // The query: raw bf16 (GQA baseline); pre-absorbed fp32 (q_abs, q_rot);
+  // or, fused, the raw positional pair and the first round of q / M_h
+  // chunks for this wave's first head.
+  u32x4 xqg[GQA ? NC : 1];
+  f32x4 xa[GQA ? 1 : NC][2];
+  f32x4 xr[NRC > 0 ? NRC : 1][2];
+  bf16x8 am[CR][NB];
+  bf16x8 xqf[CR];
+  const int W = a.d_c + a.d_r;
+  const int nck = a.d_c / 32;
+  const int npair = a.d_r / 2;
+  const bool has_pair = FUSED && tid < HPG * npair;
+  const int pair_h = npair > 0 ? tid / npair : 0, pair_i = npair > 0 ? tid % npair : 0;
+  uint32_t rq_bits = 0u;                       // the raw positional pair (bf16 x 2)
+  auto load_round = [&](int hl, int c0) {      // q chunks and M_h rows of one absorption round
+    const int h = h0 + hl;
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + h) * W;
+    const uint16_t* mh = static_cast<const uint16_t*>(a.m) + (int64_t)h * DV * a.d_c;
+#pragma unroll
+    for (int cr = 0; cr < CR; ++cr) {
+      const int c = min(c0 + cr, nck - 1);
+      xqf[cr] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
+#pragma unroll
+      for (int ib = 0; ib < NB; ++ib)
+        am[cr][ib] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * a.d_c + 32 * c + 8 * qd));
+    }
+  };
+  if constexpr (GQA) {
+    const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + hq) * a.q_stride + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) xqg[c] = *reinterpret_cast<const u32x4*>(qrow + 32 * c);
+  } else if constexpr (!FUSED) {
+    const float* qa = a.q_abs + ((int64_t)b * a.H + hq) * DV + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      xa[c][0] = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      xa[c][1] = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const int j0 = min(32 * rc + 8 * qd, a.d_r - 8);    // lanes past d_r: any valid piece
+      const float* qr = a.q_rot + ((int64_t)b * a.H + hq) * a.d_r + j0;
+      xr[rc][0] = *reinterpret_cast<const f32x4*>(qr);
+      xr[rc][1] = *reinterpret_cast<const f32x4*>(qr + 4);
+    }
+  } else {
+    if (has_pair)
+      rq_bits = *reinterpret_cast<const uint32_t*>(
+          static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + h0 + pair_h) * W + a.d_c + 2 * pair_i);
+    if (w < HPG) load_round(w, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+  if (!settle_rows()) {
+    write_empty();
+    return;
+  }
+
+  // With the current token's rows given, the split holding row L-1 takes
+  // that row from them and streams only the rows before it from the cache.
+  const bool pending = !GQA && a.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
+  if (pending) r1 = L - 1;
+  const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
 
   // ---- streaming setup.  Rows are read through buffer descriptors that end
   // at the split's last layout tile: a tile past the end reads as zeros
@@ -505,24 +615,24 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   // a loop-invariant per-lane offset plus the tile base in a scalar
   // register.  Rows past the split inside its last layout tile may hold
   // never-written data; the tail tile zeroes them before use.
-  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
-  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + ((int64_t)b * a.G + g) * a.t_max * DV;
+  const uint16_t* kbase = static_cast<const uint16_t*>(a.kr) + (int64_t)b * a.t_max * a.d_r;
   const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(vbase), (short)0, r1c * DV * 2, kBufferWord3);
   const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(kbase), (short)0, r1c * p.d_r * 2, kBufferWord3);
+      const_cast<uint16_t*>(kbase), (short)0, r1c * a.d_r * 2, kBufferWord3);
   const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
-                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
+      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(a.k_gqa) +
+                                                       ((int64_t)b * a.G + g) * a.t_max * DV)
                             : static_cast<const void*>(vbase)),
       (short)0, r1c * DV * 2, kBufferWord3);
-  const int kpieces = p.d_r / 8;              // 16-byte pieces per key row
+  const int kpieces = a.d_r / 8;              // 16-byte pieces per key row
   const int v_lane = qd * 256 + n * 16;       // piece qd of row n (of a 32-column chunk)
   int k_lane[NRC > 0 ? NRC : 1];
 #pragma unroll
   for (int rc = 0; rc < NRC; ++rc)            // lanes past d_r re-read a valid piece (weight 0)
     k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
-  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
+  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * a.d_r * 2;
 
   const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
   const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
@@ -547,181 +657,128 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     }
   };
   TileT buf[DEPTH];
-
-  // The pending row's raw values: one 16-byte value piece per thread of the
-  // first DV/8 threads, one positional pair per thread of the first d_r/2.
-  u32x4 pend_piece = {0u, 0u, 0u, 0u};
-  float pend_k0 = 0.f, pend_k1 = 0.f;
-  if (pending) {
-    if (tid < DV / 8)
-      pend_piece = *(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(p.v_new) + ((int64_t)b * p.G + g) * DV) + tid);
-    if (tid < p.d_r / 2) {
-      const uint32_t two = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(p.kr_new) + (int64_t)b * p.d_r + 2 * tid);
-      pend_k0 = bf16_bits_to_f32(two & 0xFFFFu);
-      pend_k1 = bf16_bits_to_f32(two >> 16);
-    }
+#pragma unroll
+  for (int d = 0; d < DEPTH - 1; ++d) {
+    load_tile(buf[d], tile_row(d));
+    __builtin_amdgcn_sched_barrier(0);
   }
 
-  // ---- prologue: absorbed, rotated, scaled queries as MFMA B operands.
-  // The query loads are issued before the V prefetch: loads retire in order,
-  // so waiting for the query does not wait for the prefetched tiles.
+  // ---- the current token's rows (Algorithm 1's append): wave 0 rotates
+  // the positional pair (fp64 angle, one rounding, exactly as append_kernel
+  // does), stages the row in LDS for the epilogue and stores it into the
+  // caches.  This workgroup is the only reader of row L-1 of stream (b, g)
+  // in this launch; the shared positional key is stored once, by group 0.
+  // Other workgroups may load the layout tile holding it, but only as rows
+  // past their split, which are zeroed.  Run while the query loads land
+  // (pre-absorbed path) or after the absorption (fused path, whose M_h
+  // round holds too many registers to overlap it).
+  auto stage_current_row = [&]() {
+    if (!(pending && w == 0)) return;
+    uint16_t* vcache = static_cast<uint16_t*>(a.v) + ((int64_t)b * a.G + g) * a.t_max * DV;
+    uint16_t* kcache = static_cast<uint16_t*>(a.kr) + (int64_t)b * a.t_max * a.d_r;
+    if (tid < DV / 8) {
+      *(reinterpret_cast<u32x4*>(prow) + tid) = pend_piece;
+      *reinterpret_cast<u32x4*>(vcache + tiled_off<uint16_t>(L - 1, 8 * tid, DV)) = pend_piece;
+    }
+    if (tid < 16 * NRC) {
+      uint16_t y0b = 0, y1b = 0;
+      if (tid < a.d_r / 2) {
+        double y0, y1;
+        rotate_pair(bf16_bits_to_f32(pend_kbits & 0xFFFFu), bf16_bits_to_f32(pend_kbits >> 16),
+                    (double)(L - 1) * p.inv_freq[tid], y0, y1);
+        y0b = f64_to_bf16_rne(y0);
+        y1b = f64_to_bf16_rne(y1);
+        if (g == 0) {
+          const int64_t o = tiled_off<uint16_t>(L - 1, 2 * tid, a.d_r);
+          kcache[o] = y0b;
+          kcache[o + 1] = y1b;
+        }
+      }
+      prow[DV + 2 * tid] = y0b;
+      prow[DV + 2 * tid + 1] = y1b;
+    }
+  };
+
+  // ---- the query as MFMA B operands: absorbed, rotated and scaled, each
+  // head's values split into bf16 high and low columns.
   bf16x8 bq[NC];
   bf16x8 bk[NRC > 0 ? NRC : 1];
   if constexpr (GQA) {
-    // the raw query's first DV entries, scaled, split hi + lo
-    const int hq = h0 + col_head;
-    const uint16_t* qrow = static_cast<const uint16_t*>(p.q) + ((int64_t)b * p.H + hq) * p.q_stride + 8 * qd;
-    u32x4 xq[NC];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) xq[c] = *reinterpret_cast<const u32x4*>(qrow + 32 * c);
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int d = 0; d < DEPTH - 1; ++d) {
-      load_tile(buf[d], tile_row(d));
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       float x[8];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[2 * j] = bf16_bits_to_f32(xq[c][j] & 0xFFFFu) * p.scale_log2;
-        x[2 * j + 1] = bf16_bits_to_f32(xq[c][j] >> 16) * p.scale_log2;
+        x[2 * j] = bf16_bits_to_f32(xqg[c][j] & 0xFFFFu) * a.scale_log2;
+        x[2 * j + 1] = bf16_bits_to_f32(xqg[c][j] >> 16) * a.scale_log2;
       }
       bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
     }
-  } else if (!p.fused) {
-    const int hq = h0 + col_head;
-    const float* qa = p.q_abs + ((int64_t)b * p.H + hq) * DV + 8 * qd;
-    f32x4 xa[NC][2];
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      xa[c][0] = *reinterpret_cast<const f32x4*>(qa + 32 * c);
-      xa[c][1] = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
-    }
-    f32x4 xr[NRC > 0 ? NRC : 1][2];
-#pragma unroll
-    for (int rc = 0; rc < NRC; ++rc) {
-      const int j0 = min(32 * rc + 8 * qd, p.d_r - 8);    // lanes past d_r: any valid piece
-      const float* qr = p.q_rot + ((int64_t)b * p.H + hq) * p.d_r + j0;
-      xr[rc][0] = *reinterpret_cast<const f32x4*>(qr);
-      xr[rc][1] = *reinterpret_cast<const f32x4*>(qr + 4);
-    }
-    __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-    for (int d = 0; d < DEPTH - 1; ++d) {
-      load_tile(buf[d], tile_row(d));
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+  } else if constexpr (!FUSED) {
+    stage_current_row();
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       float x[8];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] = xa[c][0][j] * p.scale_log2;
-        x[4 + j] = xa[c][1][j] * p.scale_log2;
+        x[j] = xa[c][0][j] * a.scale_log2;
+        x[4 + j] = xa[c][1][j] * a.scale_log2;
       }
       bq[c] = active ? split_hi_lo(x, is_lo) : zero8;
     }
 #pragma unroll
     for (int rc = 0; rc < NRC; ++rc) {
-      const bool in_range = 32 * rc + 8 * qd < p.d_r;
+      const bool in_range = 32 * rc + 8 * qd < a.d_r;
       float x[8];
 #pragma unroll
       for (int j = 0; j < 4; ++j) {
-        x[j] = xr[rc][0][j] * p.scale_log2;
-        x[4 + j] = xr[rc][1][j] * p.scale_log2;
+        x[j] = xr[rc][0][j] * a.scale_log2;
+        x[4 + j] = xr[rc][1][j] * a.scale_log2;
       }
       bk[rc] = (active && in_range) ? split_hi_lo(x, is_lo) : zero8;
     }
   } else {
     // Fused absorption: q~_h = q^nope_h M_h^T on the matrix cores, wave w
     // taking heads w, w+4, ...; A = rows i of M_h (K = d_c), B = the query
-    // chunk broadcast to all 16 columns.  The first round of M/q loads and
-    // the raw positional query go out before the V prefetch.
+    // chunk broadcast to all 16 columns.  The first round was loaded above.
     float* qs = lds;                                  // [HPG][QS_STRIDE]
     float* qrs = lds + HPG * Cfg::QS_STRIDE;          // [HPG][QR_STRIDE]
-    const uint16_t* qg = static_cast<const uint16_t*>(p.q);
-    const uint16_t* mg = static_cast<const uint16_t*>(p.m);
-    const int W = p.d_c + p.d_r;
-    const int nck = p.d_c / 32;
-    // raw positional query pairs, one pair per thread
-    const int npair = p.d_r / 2;
-    const bool has_pair = tid < HPG * npair;
-    float rq0 = 0.f, rq1 = 0.f;
-    int pair_h = 0, pair_i = 0;
-    if (has_pair) {
-      pair_h = tid / npair;
-      pair_i = tid % npair;
-      const uint16_t* qrow = qg + ((int64_t)b * p.H + h0 + pair_h) * W + p.d_c + 2 * pair_i;
-      const uint32_t two = *reinterpret_cast<const uint32_t*>(qrow);
-      rq0 = bf16_bits_to_f32(two & 0xFFFFu);
-      rq1 = bf16_bits_to_f32(two >> 16);
-    }
-    bool prefetched = false;
     for (int hl = w; hl < HPG; hl += kWaves) {
-      const int h = h0 + hl;
-      const uint16_t* qrow = qg + ((int64_t)b * p.H + h) * W;
-      const uint16_t* mh = mg + (int64_t)h * DV * p.d_c;
       f32x4 acc[NB];
 #pragma unroll
       for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
       for (int c0 = 0; c0 < nck; c0 += CR) {
-        bf16x8 am[CR][NB];
-        bf16x8 xq[CR];
-#pragma unroll
-        for (int cr = 0; cr < CR; ++cr) {
-          const int c = min(c0 + cr, nck - 1);
-          xq[cr] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
-#pragma unroll
-          for (int ib = 0; ib < NB; ++ib)
-            am[cr][ib] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
-        }
-        if (!prefetched) {
-          __builtin_amdgcn_sched_barrier(0);
-#pragma unroll
-          for (int d = 0; d < DEPTH - 1; ++d) {
-            load_tile(buf[d], tile_row(d));
-            __builtin_amdgcn_sched_barrier(0);
-          }
-          prefetched = true;
-        }
+        if (hl != w || c0 != 0) load_round(hl, c0);
 #pragma unroll
         for (int cr = 0; cr < CR; ++cr)
           if (c0 + cr < nck)
 #pragma unroll
-            for (int ib = 0; ib < NB; ++ib) acc[ib] = mfma16(am[cr][ib], xq[cr], acc[ib]);
+            for (int ib = 0; ib < NB; ++ib) acc[ib] = mfma16(am[cr][ib], xqf[cr], acc[ib]);
       }
       if (n == 0) {
 #pragma unroll
         for (int ib = 0; ib < NB; ++ib)
-          *reinterpret_cast<f32x4*>(qs + hl * Cfg::QS_STRIDE + 16 * ib + 4 * qd) = acc[ib] * p.scale_log2;
+          *reinterpret_cast<f32x4*>(qs + hl * Cfg::QS_STRIDE + 16 * ib + 4 * qd) = acc[ib] * a.scale_log2;
       }
     }
-    if (!prefetched) {       // waves without a head of their own
-#pragma unroll
-      for (int d = 0; d < DEPTH - 1; ++d) {
-        load_tile(buf[d], tile_row(d));
-        __builtin_amdgcn_sched_barrier(0);
-      }
-    }
+    stage_current_row();
     // rotate the positional query at position L-1 (fp64 angle, reduced
     // exactly, fp32 rotation); the padding past d_r is written as zeros in
     // the same phase, so one barrier covers both
     if (has_pair) {
       float y0, y1;
-      rotate_query_pair(rq0, rq1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], p.scale_log2, y0, y1);
+      rotate_query_pair(bf16_bits_to_f32(rq_bits & 0xFFFFu), bf16_bits_to_f32(rq_bits >> 16),
+                        (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], a.scale_log2, y0, y1);
       qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i] = y0;
       qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = y1;
     }
-    for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads) {
-      const int j = idx % (32 * NRC);
-      if (j >= p.d_r) qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + j] = 0.f;
+    if constexpr (NRC > 0) {
+      for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads) {
+        const int j = idx % (32 * NRC);
+        if (j >= a.d_r) qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + j] = 0.f;
+      }
     }
     __syncthreads();
-    const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 #pragma unroll
     for (int c = 0; c < NC; ++c) {
       const float* src = qs + col_head * Cfg::QS_STRIDE + 32 * c + 8 * qd;
@@ -756,7 +813,6 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   f32x4 acc[NB];
 #pragma unroll
   for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
-  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
 
   auto compute_tile = [&](TileT& t, int row0, int row_end) {
     if (row0 + kTileRows > row_end) {        // ragged tail: clear rows past the end
@@ -852,53 +908,22 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     }
   }
 
-  // ---- the pending row (current token): staged through LDS, then wave 0
-  // scores it as a one-row tile, exactly as if it had been read from the
-  // cache after gva_append_kv (same rotation and rounding)
-  if (pending) {
-    __syncthreads();                        // prologue LDS no longer needed
-    uint16_t* prow = reinterpret_cast<uint16_t*>(lds);          // [DV] value, then [32*NRC] key
-    // the append: this workgroup is the only reader of row L-1 of stream
-    // (b, g) in this launch, so it also stores the row into the caches (the
-    // shared positional key once, by group 0)
-    uint16_t* vcache = static_cast<uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
-    uint16_t* kcache = static_cast<uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
-    if (tid < DV / 8) {
-      *(reinterpret_cast<u32x4*>(prow) + tid) = pend_piece;
-      *reinterpret_cast<u32x4*>(vcache + tiled_off<uint16_t>(L - 1, 8 * tid, DV)) = pend_piece;
-    }
-    for (int idx = tid; idx < 16 * NRC; idx += kThreads) {
-      uint16_t y0b = 0, y1b = 0;
-      if (idx < p.d_r / 2) {
-        double y0, y1;
-        rotate_pair(pend_k0, pend_k1, (double)(L - 1) * p.inv_freq[idx], y0, y1);
-        y0b = f64_to_bf16_rne(y0);
-        y1b = f64_to_bf16_rne(y1);
-        if (g == 0) {
-          const int64_t o = tiled_off<uint16_t>(L - 1, 2 * idx, p.d_r);
-          kcache[o] = y0b;
-          kcache[o + 1] = y1b;
-        }
-      }
-      prow[DV + 2 * idx] = y0b;
-      prow[DV + 2 * idx + 1] = y1b;
-    }
-    __syncthreads();
-    if (w == 0) {
-      TileT t;
-      const u32x4* pv = reinterpret_cast<const u32x4*>(prow);
+  // ---- the current token's row, staged in LDS by wave 0 in the prologue,
+  // scored by wave 0 as a one-row tile
+  if (pending && w == 0) {
+    TileT t;
+    const u32x4* pv = reinterpret_cast<const u32x4*>(prow);
 #pragma unroll
-      for (int c = 0; c < NC; ++c) {
-        t.v[0][c] = n == 0 ? as_bf16x8(pv[4 * c + qd]) : zero8;
-        t.v[1][c] = zero8;
-      }
-#pragma unroll
-      for (int rc = 0; rc < NRC; ++rc) {
-        t.k[0][rc] = n == 0 ? as_bf16x8(pv[DV / 8 + 4 * rc + qd]) : zero8;
-        t.k[1][rc] = zero8;
-      }
-      compute_tile(t, L - 1, L);
+    for (int c = 0; c < NC; ++c) {
+      t.v[0][c] = n == 0 ? as_bf16x8(pv[4 * c + qd]) : zero8;
+      t.v[1][c] = zero8;
     }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      t.k[0][rc] = n == 0 ? as_bf16x8(pv[DV / 8 + 4 * rc + qd]) : zero8;
+      t.k[1][rc] = zero8;
+    }
+    compute_tile(t, L - 1, L);
   }
 
   // ---- merge the waves and write this split's partial
@@ -939,9 +964,9 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       }
       o /= lsum;
     }
-    const int64_t prow = ((int64_t)b * p.H + h0 + hl) * p.S + s;
-    p.o_part[prow * DV + i] = o;
-    if (i == 0) p.lse_part[prow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
+    const int64_t prow = ((int64_t)b * a.H + h0 + hl) * a.S + s;
+    a.o_part[prow * DV + i] = o;
+    if (i == 0) a.lse_part[prow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
   }
 }
 
@@ -961,55 +986,55 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
   __shared__ float red_o[kWaves][kF32MaxHpg][kF32MaxDv];
 
   int b, s, g;
-  if (!work_item(p, b, s, g)) return;          // grid padding (fixed chunks)
+  if (!work_item(p.a, b, s, g)) return;          // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
-  const int hpg = p.H / p.G, h0 = g * hpg;
-  const int DV = p.d_v, DR = p.d_r;
-  const int L = clamp_len(p.lens, b, p.t_max);
+  const int hpg = p.a.H / p.a.G, h0 = g * hpg;
+  const int DV = p.a.d_v, DR = p.a.d_r;
+  const int L = clamp_len(p.a.lens, b, p.a.t_max);
   int r0, r1;
-  split_rows(L, p.S, p.split_rows, s, r0, r1);
+  split_rows(L, p.a.S, p.a.split_rows, s, r0, r1);
   if (r0 >= r1 && s > 0) {                     // an empty split past the first: lse only
-    if (tid < hpg) p.lse_part[((int64_t)b * p.H + h0 + tid) * p.S + s] = -INFINITY;
+    if (tid < hpg) p.a.lse_part[((int64_t)b * p.a.H + h0 + tid) * p.a.S + s] = -INFINITY;
     return;
   }
-  const bool pending = p.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
+  const bool pending = p.a.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
   if (pending) r1 = L - 1;
 
-  if (p.fused) {
-    const float* qg = static_cast<const float*>(p.q);
-    const float* mg = static_cast<const float*>(p.m);
-    const int W = p.d_c + DR;
+  if (p.a.fused) {
+    const float* qg = static_cast<const float*>(p.a.q);
+    const float* mg = static_cast<const float*>(p.a.m);
+    const int W = p.a.d_c + DR;
     for (int idx = tid; idx < hpg * DV; idx += kThreads) {
       const int hl = idx / DV, i = idx % DV;
-      const float* qrow = qg + ((int64_t)b * p.H + h0 + hl) * W;
-      const float* mrow = mg + ((int64_t)(h0 + hl) * DV + i) * p.d_c;
+      const float* qrow = qg + ((int64_t)b * p.a.H + h0 + hl) * W;
+      const float* mrow = mg + ((int64_t)(h0 + hl) * DV + i) * p.a.d_c;
       float a = 0.f;
-      for (int k = 0; k < p.d_c; ++k) a = fmaf(qrow[k], mrow[k], a);
-      qs[hl][i] = a * p.scale_log2;
+      for (int k = 0; k < p.a.d_c; ++k) a = fmaf(qrow[k], mrow[k], a);
+      qs[hl][i] = a * p.a.scale_log2;
     }
     const int L1 = L > 0 ? L - 1 : 0;
     for (int idx = tid; idx < hpg * (DR / 2); idx += kThreads) {
       const int hl = idx / (DR / 2), i = idx % (DR / 2);
-      const float* qrow = qg + ((int64_t)b * p.H + h0 + hl) * W + p.d_c;
+      const float* qrow = qg + ((int64_t)b * p.a.H + h0 + hl) * W + p.a.d_c;
       double y0, y1;
       rotate_pair(qrow[2 * i], qrow[2 * i + 1], (double)L1 * p.inv_freq[i], y0, y1);
-      qr[hl][2 * i] = (float)(y0 * (double)p.scale_log2);
-      qr[hl][2 * i + 1] = (float)(y1 * (double)p.scale_log2);
+      qr[hl][2 * i] = (float)(y0 * (double)p.a.scale_log2);
+      qr[hl][2 * i + 1] = (float)(y1 * (double)p.a.scale_log2);
     }
   } else {
     for (int idx = tid; idx < hpg * DV; idx += kThreads) {
       const int hl = idx / DV, i = idx % DV;
-      qs[hl][i] = p.q_abs[((int64_t)b * p.H + h0 + hl) * DV + i] * p.scale_log2;
+      qs[hl][i] = p.a.q_abs[((int64_t)b * p.a.H + h0 + hl) * DV + i] * p.a.scale_log2;
     }
     for (int idx = tid; idx < hpg * DR; idx += kThreads) {
       const int hl = idx / DR, j = idx % DR;
-      qr[hl][j] = p.q_rot[((int64_t)b * p.H + h0 + hl) * DR + j] * p.scale_log2;
+      qr[hl][j] = p.a.q_rot[((int64_t)b * p.a.H + h0 + hl) * DR + j] * p.a.scale_log2;
     }
   }
   __syncthreads();
 
-  const float* vb = static_cast<const float*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
-  const float* kb = static_cast<const float*>(p.kr) + (int64_t)b * p.t_max * DR;
+  const float* vb = static_cast<const float*>(p.a.v) + ((int64_t)b * p.a.G + g) * p.a.t_max * DV;
+  const float* kb = static_cast<const float*>(p.a.kr) + (int64_t)b * p.a.t_max * DR;
   float m_run[kF32MaxHpg], l_run[kF32MaxHpg], acc[kF32MaxHpg][4];
 #pragma unroll
   for (int h = 0; h < kF32MaxHpg; ++h) {
@@ -1082,25 +1107,25 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
   // the pending row (current token), taken from v_new / kr_new with the
   // rotation and rounding gva_append_kv would store, added by wave 0
   if (pending && w == 0) {
-    const float* vn = static_cast<const float*>(p.v_new) + ((int64_t)b * p.G + g) * DV;
+    const float* vn = static_cast<const float*>(p.a.v_new) + ((int64_t)b * p.a.G + g) * DV;
     float vv[4];
 #pragma unroll
     for (int u = 0; u < 4; ++u) vv[u] = lane + 64 * u < DV ? vn[lane + 64 * u] : 0.f;
     float kk = 0.f;
     if (lane < DR) {
-      const float* kn = static_cast<const float*>(p.kr_new) + (int64_t)b * DR;
+      const float* kn = static_cast<const float*>(p.a.kr_new) + (int64_t)b * DR;
       double y0, y1;
       const int pi = lane / 2;
       rotate_pair(kn[2 * pi], kn[2 * pi + 1], (double)(L - 1) * p.inv_freq[pi], y0, y1);
       kk = (float)((lane & 1) ? y1 : y0);
     }
     // the append of row L-1 (this wave is its only reader in this launch)
-    float* vcache = static_cast<float*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+    float* vcache = static_cast<float*>(p.a.v) + ((int64_t)b * p.a.G + g) * p.a.t_max * DV;
 #pragma unroll
     for (int u = 0; u < 4; ++u)
       if (lane + 64 * u < DV) vcache[tiled_off<float>(L - 1, lane + 64 * u, DV)] = vv[u];
     if (g == 0 && lane < DR)
-      (static_cast<float*>(p.kr) + (int64_t)b * p.t_max * DR)[tiled_off<float>(L - 1, lane, DR)] = kk;
+      (static_cast<float*>(p.a.kr) + (int64_t)b * p.a.t_max * DR)[tiled_off<float>(L - 1, lane, DR)] = kk;
 #pragma unroll
     for (int h = 0; h < kF32MaxHpg; ++h) {
       if (h < hpg) {
@@ -1149,9 +1174,9 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
       }
       o /= lsum;
     }
-    const int64_t prow = ((int64_t)b * p.H + h0 + hl) * p.S + s;
-    p.o_part[prow * DV + i] = o;
-    if (i == 0) p.lse_part[prow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
+    const int64_t prow = ((int64_t)b * p.a.H + h0 + hl) * p.a.S + s;
+    p.a.o_part[prow * DV + i] = o;
+    if (i == 0) p.a.lse_part[prow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
   }
 }
 
@@ -1284,21 +1309,21 @@ int launch_status() {
 
 using DecodeFn = void (*)(DecodeParams);
 
-template <int HPG, int DV>
+template <int HPG, int DV, bool FUSED>
 DecodeFn pick_nrc(int nrc) {
   switch (nrc) {
-    case 0: return decode_bf16_kernel<HPG, DV, 0>;
-    case 1: return decode_bf16_kernel<HPG, DV, 1>;
-    case 2: return decode_bf16_kernel<HPG, DV, 2>;
+    case 0: return decode_bf16_kernel<HPG, DV, 0, false, FUSED>;
+    case 1: return decode_bf16_kernel<HPG, DV, 1, false, FUSED>;
+    case 2: return decode_bf16_kernel<HPG, DV, 2, false, FUSED>;
   }
   return nullptr;
 }
 
 template <int HPG>
-DecodeFn pick_dv(int dv, int nrc) {
+DecodeFn pick_dv(int dv, int nrc, bool fused) {
   switch (dv) {
-    case 64: return pick_nrc<HPG, 64>(nrc);
-    case 128: return pick_nrc<HPG, 128>(nrc);
+    case 64: return fused ? pick_nrc<HPG, 64, true>(nrc) : pick_nrc<HPG, 64, false>(nrc);
+    case 128: return fused ? pick_nrc<HPG, 128, true>(nrc) : pick_nrc<HPG, 128, false>(nrc);
   }
   return nullptr;
 }
@@ -1306,10 +1331,10 @@ DecodeFn pick_dv(int dv, int nrc) {
 template <int DV>
 DecodeFn pick_gqa_hpg(int hpg) {
   switch (hpg) {
-    case 1: return decode_bf16_kernel<1, DV, 0, true>;
-    case 2: return decode_bf16_kernel<2, DV, 0, true>;
-    case 4: return decode_bf16_kernel<4, DV, 0, true>;
-    case 8: return decode_bf16_kernel<8, DV, 0, true>;
+    case 1: return decode_bf16_kernel<1, DV, 0, true, false>;
+    case 2: return decode_bf16_kernel<2, DV, 0, true, false>;
+    case 4: return decode_bf16_kernel<4, DV, 0, true, false>;
+    case 8: return decode_bf16_kernel<8, DV, 0, true, false>;
   }
   return nullptr;
 }
@@ -1322,12 +1347,12 @@ DecodeFn pick_gqa_decode(int hpg, int dv) {
   return nullptr;
 }
 
-DecodeFn pick_bf16_decode(int hpg, int dv, int nrc) {
+DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused) {
   switch (hpg) {
-    case 1: return pick_dv<1>(dv, nrc);
-    case 2: return pick_dv<2>(dv, nrc);
-    case 4: return pick_dv<4>(dv, nrc);
-    case 8: return pick_dv<8>(dv, nrc);
+    case 1: return pick_dv<1>(dv, nrc, fused);
+    case 2: return pick_dv<2>(dv, nrc, fused);
+    case 4: return pick_dv<4>(dv, nrc, fused);
+    case 8: return pick_dv<8>(dv, nrc, fused);
   }
   return nullptr;
 }
@@ -1451,30 +1476,30 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p;
-  p.q = q;
-  p.m = m;
-  p.q_abs = q_abs;
-  p.q_rot = q_rot;
-  p.v = v_cache;
-  p.kr = kr_cache;
-  p.lens = lens;
-  p.o_part = o_part;
-  p.lse_part = lse_part;
-  p.v_new = v_new;
-  p.kr_new = kr_new;
-  p.k_gqa = nullptr;
-  p.q_stride = 0;
-  p.B = dims->batch;
-  p.H = dims->n_heads;
-  p.G = dims->n_groups;
-  p.d_v = dims->d_v;
-  p.d_c = dims->d_c;
-  p.d_r = dims->d_r;
-  p.t_max = dims->t_max;
-  p.S = num_splits;
-  p.split_rows = split_rows;
-  p.scale_log2 = scale_log2(dims);
-  p.fused = fused ? 1 : 0;
+  p.a.q = q;
+  p.a.m = m;
+  p.a.q_abs = q_abs;
+  p.a.q_rot = q_rot;
+  p.a.v = v_cache;
+  p.a.kr = kr_cache;
+  p.a.lens = lens;
+  p.a.o_part = o_part;
+  p.a.lse_part = lse_part;
+  p.a.v_new = v_new;
+  p.a.kr_new = kr_new;
+  p.a.k_gqa = nullptr;
+  p.a.q_stride = 0;
+  p.a.B = dims->batch;
+  p.a.H = dims->n_heads;
+  p.a.G = dims->n_groups;
+  p.a.d_v = dims->d_v;
+  p.a.d_c = dims->d_c;
+  p.a.d_r = dims->d_r;
+  p.a.t_max = dims->t_max;
+  p.a.S = num_splits;
+  p.a.split_rows = split_rows;
+  p.a.scale_log2 = scale_log2(dims);
+  p.a.fused = fused ? 1 : 0;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -1482,7 +1507,7 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
     if (dims->d_c % 32 != 0 || dims->d_c > 512 || dims->d_r % 8 != 0 || dims->d_r > 64)
       return GVA_ERR_UNSUPPORTED;
     const int nrc = (dims->d_r + 31) / 32;
-    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc);
+    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused);
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   } else {
@@ -1517,24 +1542,24 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
 
   DecodeParams p;
   memset(&p, 0, sizeof(p));
-  p.q = q;
-  p.v = const_cast<void*>(v_cache);       // read only: the GQA kernel never appends
-  p.k_gqa = k_cache;
-  p.q_stride = q_stride;
-  p.lens = lens;
-  p.o_part = o_part;
-  p.lse_part = lse_part;
-  p.B = dims->batch;
-  p.H = dims->n_heads;
-  p.G = dims->n_groups;
-  p.d_v = dims->d_v;
-  p.d_c = dims->d_v;
-  p.d_r = 0;
-  p.t_max = dims->t_max;
-  p.S = num_splits;
-  p.split_rows = split_rows;
+  p.a.q = q;
+  p.a.v = const_cast<void*>(v_cache);       // read only: the GQA kernel never appends
+  p.a.k_gqa = k_cache;
+  p.a.q_stride = q_stride;
+  p.a.lens = lens;
+  p.a.o_part = o_part;
+  p.a.lse_part = lse_part;
+  p.a.B = dims->batch;
+  p.a.H = dims->n_heads;
+  p.a.G = dims->n_groups;
+  p.a.d_v = dims->d_v;
+  p.a.d_c = dims->d_v;
+  p.a.d_r = 0;
+  p.a.t_max = dims->t_max;
+  p.a.S = num_splits;
+  p.a.split_rows = split_rows;
   const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
-  p.scale_log2 = (float)(sc * kLog2e);
+  p.a.scale_log2 = (float)(sc * kLog2e);
   hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
 }

@@ -231,11 +231,19 @@ def splits_for(dims: GvaDims, lens: torch.Tensor, n_cu: int = 0) -> int:
     return plan_for(dims, lens, n_cu, chunked=False)[0]
 
 
-def prefer_fused(num_splits: int) -> bool:
-    """Fuse the absorption into the attention kernel when each (sequence,
-    group) has at most two splits; with more splits every workgroup would
-    redo the absorption, so a separate absorb launch is cheaper."""
-    return int(num_splits) <= 2
+def device_cu_count(device=None) -> int:
+    """Compute units of the current (or given) GPU."""
+    return int(torch.cuda.get_device_properties(device if device is not None else
+                                                torch.cuda.current_device()).multi_processor_count)
+
+
+def prefer_fused(dims: GvaDims, num_splits: int, n_cu: int = 0) -> bool:
+    """Fuse the absorption into the attention kernel when the grid fits one
+    workgroup per CU (B * G * S workgroups) with at most two splits per
+    sequence: every fused workgroup absorbs its group's heads again, so
+    with more workgroups one gva_absorb_query launch is cheaper."""
+    n_cu = int(n_cu) or device_cu_count()
+    return int(num_splits) <= 2 and dims.batch * dims.n_groups * int(num_splits) <= n_cu
 
 
 def gva_version() -> int:
@@ -290,7 +298,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
     """
     S = int(num_splits)
     if fused is None:
-        fused = prefer_fused(S)
+        fused = prefer_fused(dims, S)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
     pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)

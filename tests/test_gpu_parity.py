@@ -259,7 +259,7 @@ def test_full_size_sampled(name):
     S, rows = gva.plan_for(d, inp["lens"])     # the launch configuration bench.py times
     dev = upload({k: inp[k] for k in ("q", "m", "v", "kr", "lens")})
     note(f"{name}: decode S={S} split_rows={rows}")
-    o, lse, _, _ = run_decode(w, dev, S, fused=gva.prefer_fused(S), split_rows=rows)
+    o, lse, _, _ = run_decode(w, dev, S, fused=gva.prefer_fused(d, S), split_rows=rows)
     del dev
     torch.cuda.empty_cache()
     # the oracle on a sample of sequences: first, last, longest, shortest
@@ -468,3 +468,56 @@ def test_combine_never_reads_empty_partials():
     assert torch.isfinite(o.cpu()).all()
     assert max_abs(o.cpu(), o_ref) <= 1e-5
     assert lse_err(lse.cpu(), lse_ref) <= 1e-5
+
+
+# ------------------------------------------------- HIP graph capture of steps
+@pytest.mark.parametrize("S,fused", [(1, True), (3, False)])
+def test_graph_capture_of_layer_steps(S, fused):
+    # Several layers' decode steps (absorb, attention with the current row
+    # appended in the same launch, combine) captured in one HIP graph.  The
+    # library allocates, synchronises and clears nothing, so its launches
+    # are capturable as they are.  Each replay, with eager work and
+    # synchronisation between replays, must equal the eager result bit for
+    # bit and match the oracle.
+    w = gva_inputs.workload("gva350m_b8_t2k")
+    d = dims_of(w)
+    n_layers = 3
+    layers = []
+    for layer in range(n_layers):
+        inp = gva_inputs.make_inputs(w, 100 + layer)
+        seq = torch.arange(w.batch, dtype=torch.int32)
+        pos = (inp["lens"] - 1).to(torch.int32)
+        v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+        oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+        o_ref, _ = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"])
+        layers.append((upload(inp), gva.DecodeBuffers(d, S), o_ref))
+
+    def run_layers():
+        outs = []
+        for dev, bufs, _ in layers:
+            o, _ = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S, bufs=bufs,
+                              fused=fused, v_new=dev["v_new"], kr_new=dev["kr_new"])
+            outs.append(o)
+        return outs
+
+    note(f"graph capture S={S} fused={fused}: eager")
+    eager = [o.clone() for o in run_layers()]
+    torch.cuda.synchronize()
+    for o, (_, _, o_ref) in zip(eager, layers):
+        assert max_abs(o.cpu(), o_ref) <= 1e-4
+    run_layers()                                  # warm the capture stream's allocator state
+    torch.cuda.synchronize()
+    g = torch.cuda.CUDAGraph()
+    with torch.cuda.graph(g):
+        graphed = run_layers()
+    for rep in range(3):
+        for o in graphed:
+            o.zero_()
+        scratch = torch.randn(1 << 16, device="cuda").sum()     # eager work between replays
+        torch.cuda.synchronize()
+        note(f"graph replay {rep}")
+        g.replay()
+        torch.cuda.synchronize()
+        assert float(scratch) == float(scratch)
+        for o, e in zip(graphed, eager):
+            assert torch.equal(o, e), f"replay {rep} differs from eager"
