@@ -316,6 +316,9 @@ def main():
     ap.add_argument("--cache-copies", type=int, default=0,
                     help="cache copies the steps rotate through (0: enough that the bytes one "
                          "rotation streams exceed twice the 256 MB last-level cache, at least 2)")
+    ap.add_argument("--paged", type=int, default=0, metavar="PAGE_ROWS",
+                    help="read the caches from page pools of PAGE_ROWS rows through a block table "
+                         "(pages in random pool order)")
     ap.add_argument("--layers", type=int, default=0,
                     help="also time an N-layer decode step (each layer its own caches, query "
                          "and maps) eagerly and as one HIP graph replay")
@@ -357,6 +360,15 @@ def main():
     n_copies = args.cache_copies or min(64, max(2, math.ceil(2 * MALL_BYTES / dec_b)))
     dev = {k: inp[k].cuda() for k in ("q", "m", "lens", "v_new", "kr_new")}
     v_tiled, kr_tiled = gva.tiled(inp["v"]), gva.tiled(inp["kr"])   # the library's cache layout
+    paging = None
+    if args.paged:
+        # every sequence's pages drawn in random order from one pool
+        paging = gva.make_paging(d, args.paged, w.batch * (w.t_max // args.paged))
+        gen = torch.Generator().manual_seed(args.seed + 7)
+        block_table = torch.randperm(paging.n_pages, generator=gen).reshape(w.batch, paging.max_pages)
+        block_table = block_table.to(torch.int32)
+        v_tiled, kr_tiled = gva.to_pages(v_tiled, kr_tiled, block_table, paging)
+        dev["block_table"] = block_table.cuda()
     caches = [(v_tiled.cuda(), kr_tiled.cuda()) for _ in range(n_copies)]
     del v_tiled, kr_tiled
     seq = torch.arange(w.batch, dtype=torch.int32)
@@ -377,13 +389,14 @@ def main():
             gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
         if ev_a is not None:
             ev_a.record(stream)
-        if fused:
-            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part,
-                                     bufs.lse_part, q=dev["q"], m=dev["m"], stream=stream, **pend)
+        qkw = dict(q=dev["q"], m=dev["m"]) if fused else \
+            dict(q_abs=q_abs, q_rot=q_rot if w.d_r > 0 else None)
+        if paging is not None:
+            gva.gva_paged_decode_attention(d, paging, vc, kc, dev["block_table"], dev["lens"], S,
+                                           bufs.o_part, bufs.lse_part, stream=stream, **qkw, **pend)
         else:
-            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part,
-                                     bufs.lse_part, q_abs=q_abs,
-                                     q_rot=q_rot if w.d_r > 0 else None, stream=stream, **pend)
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
+                                     stream=stream, **qkw, **pend)
         if ev_b is not None:
             ev_b.record(stream)
         if S > 1:   # with one split the attention kernel's partial is the output
@@ -426,6 +439,7 @@ def main():
         "config": {"workload": w.name, "batch": w.batch, "t_max": w.t_max,
                    "n_heads": w.n_heads, "n_groups": w.n_groups, "d_v": w.d_v, "d_c": w.d_c,
                    "d_r": w.d_r, "num_splits": S, "split_rows": split_rows, "fused_absorb": fused,
+                   "page_rows": args.paged or None,
                    "total_cached_rows": int(lens.clamp(min=0).sum()), "cache_copies": n_copies,
                    "parallelism": "none"},
         "frac_of_hbm_peak": round(value / HBM_PEAK_GBS, 4),
@@ -451,6 +465,8 @@ def main():
     }
 
     o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
+    if paging is not None and (args.layers > 0 or (w.gqa and not args.no_gqa)):
+        raise SystemExit("--paged times the decode step only")
     if args.layers > 0:
         out["layer_stack"] = layer_stack(args, w, inp, d, S, split_rows, fused, dec_b)
     if w.gqa and not args.no_gqa:

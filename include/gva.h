@@ -16,6 +16,9 @@
  *                         steps of Algorithm 1)
  *   gva_combine           log-sum-exp merge of the split partials
  *
+ * Paged caches (a block table over page pools) have their own append and
+ * attention calls, gva_paged_append_kv and gva_paged_decode_attention.
+ *
  * The matched grouped-query baseline the paper measures GVA against
  * (explicit key stream per group) has its own attention call,
  * gva_gqa_decode_attention, sharing the layout, splits and gva_combine.
@@ -98,6 +101,31 @@ typedef struct gva_dims {
   double scale;       /* score scale; 0 selects 1/sqrt(d_c + d_r) */
 } gva_dims;
 
+/*
+ * Paged caches (for ragged serving: a sequence's rows live in fixed-size
+ * pages drawn from shared pools, found through a block table).
+ *   v_pool  [n_pages][G][page_rows][d_v]   each (page, g) block in the
+ *                                           tiled layout of a stream
+ *   kr_pool [n_pages][page_rows][d_r]      each page block tiled likewise
+ *   block_table [B][max_pages] int32       row t of sequence b is row
+ *           t % page_rows of page block_table[b][t / page_rows]
+ * page_rows is a positive multiple of 32; dims->t_max must equal
+ * max_pages * page_rows (the capacity of a sequence); max_pages <=
+ * GVA_MAX_PAGES.  Entries a call needs (the pages of rows below lens[b], or
+ * of an appended position) must name pages in [0, n_pages): the attention
+ * kernel clamps other ids into the pool (it reads some page, never outside
+ * the pool) and the append skips rows whose page is out of range.  bf16
+ * storage only.
+ */
+typedef struct {
+  int32_t page_rows;
+  int32_t max_pages;
+  int32_t n_pages;
+} gva_paging;
+
+/* Largest max_pages accepted by the paged calls. */
+#define GVA_MAX_PAGES 4096
+
 /* Largest num_splits accepted by gva_decode_attention / gva_combine. */
 #define GVA_MAX_SPLITS 256
 
@@ -179,6 +207,30 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m,
                          const int32_t* lens, const void* v_new, const void* kr_new,
                          int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
                          void* stream);
+
+/*
+ * gva_paged_append_kv -- gva_append_kv on paged caches: row pos[r] of
+ * sequence seq[r] is written to row pos % page_rows of page
+ * block_table[seq][pos / page_rows] of both pools, with the same rotation
+ * and rounding.  Pools 16-byte aligned, block_table 4-byte aligned.
+ */
+int gva_paged_append_kv(const gva_dims* dims, const gva_paging* paging, void* v_pool, void* kr_pool,
+                        const int32_t* block_table, const void* v_new, const void* kr_new,
+                        const int32_t* seq, const int32_t* pos, int32_t n_rows, void* stream);
+
+/*
+ * gva_paged_decode_attention -- gva_decode_attention on paged caches: the
+ * same scores, softmax, splits, partials and current-row append (into the
+ * current row's page), every cache row read through the block table.
+ * A split's page ids are read once into LDS; each 32-row tile lies in one
+ * page.  Arguments as for gva_decode_attention, plus the paging and
+ * block_table (device int32 [B][max_pages]).
+ */
+int gva_paged_decode_attention(const gva_dims* dims, const gva_paging* paging, const void* q,
+                               const void* m, const float* q_abs, const float* q_rot, void* v_pool,
+                               void* kr_pool, const int32_t* block_table, const int32_t* lens,
+                               const void* v_new, const void* kr_new, int32_t num_splits,
+                               int32_t split_rows, float* o_part, float* lse_part, void* stream);
 
 /*
  * gva_gqa_decode_attention -- the matched grouped-query attention baseline

@@ -66,6 +66,7 @@ constexpr float kLn2 = 0.693147180559945309417f;
 constexpr double kLog2e = 1.44269504088896340736;
 constexpr int kBufferWord3 = 0x00020000;   // raw buffer descriptor, 32-bit data format
 constexpr int kAuxNT = 2;                  // non-temporal: the V stream is read once
+constexpr int kMaxPages = 4096;            // paged caches: block-table entries per sequence
 
 // ------------------------------------------------------------ parameters
 struct AppendParams {
@@ -76,6 +77,8 @@ struct AppendParams {
   const int32_t* seq;
   const int32_t* pos;
   int32_t B, G, t_max, d_v, d_r, n_rows;
+  const int32_t* block_table;   // paged caches (NULL: contiguous streams)
+  int32_t page_rows, max_pages, n_pages;
   double inv_freq[kMaxPairs];
 };
 
@@ -107,6 +110,8 @@ struct DecodeArgs {
   int32_t split_rows;     // fixed rows per split (0: the even rule)
   float scale_log2;       // score scale * log2(e): softmax runs in base 2
   int32_t fused;
+  const int32_t* block_table;   // paged caches: [B][max_pages] page ids
+  int32_t page_rows, max_pages, n_pages;
 };
 
 struct DecodeParams {
@@ -358,18 +363,35 @@ __global__ void __launch_bounds__(256) append_kernel(AppendParams p) {
   }
   const int b = p.seq[r], ps = p.pos[r];
   if (b < 0 || b >= p.B || ps < 0 || ps >= p.t_max) return;
+  // the stream holding row ps: a contiguous (b, g) stream, or, paged, the
+  // page block_table[b][ps / page_rows] (rows naming a page outside the pool
+  // are skipped)
+  int64_t vstream0, kstream0, vstride;
+  int row = ps;
+  if (p.block_table != nullptr) {
+    const int page = p.block_table[(int64_t)b * p.max_pages + ps / p.page_rows];
+    if (page < 0 || page >= p.n_pages) return;
+    row = ps % p.page_rows;
+    vstride = (int64_t)p.page_rows * p.d_v;
+    vstream0 = (int64_t)page * p.G * vstride;
+    kstream0 = (int64_t)page * p.page_rows * p.d_r;
+  } else {
+    vstride = (int64_t)p.t_max * p.d_v;
+    vstream0 = (int64_t)b * p.G * vstride;
+    kstream0 = (int64_t)b * p.t_max * p.d_r;
+  }
   for (int idx = tid; idx < n_pieces; idx += blockDim.x) {
     if (idx != tid) piece = src[idx];
     const int g = idx / pieces_per_row, c = idx % pieces_per_row;
-    T* stream = static_cast<T*>(p.v_cache) + ((int64_t)b * p.G + g) * p.t_max * p.d_v;
-    *reinterpret_cast<u32x4*>(stream + tiled_off<T>(ps, c * P, p.d_v)) = piece;
+    T* stream = static_cast<T*>(p.v_cache) + vstream0 + g * vstride;
+    *reinterpret_cast<u32x4*>(stream + tiled_off<T>(row, c * P, p.d_v)) = piece;
   }
   // positional key: rotate pair i at position ps in fp64 (eq. krope)
   if (has_pair) {
-    T* kstream = static_cast<T*>(p.kr_cache) + (int64_t)b * p.t_max * p.d_r;
+    T* kstream = static_cast<T*>(p.kr_cache) + kstream0;
     double y0, y1;
     rotate_pair(k0, k1, (double)ps * p.inv_freq[tid], y0, y1);
-    const int64_t o = tiled_off<T>(ps, 2 * tid, p.d_r);   // the pair shares a piece
+    const int64_t o = tiled_off<T>(row, 2 * tid, p.d_r);  // the pair shares a piece
     store_from_f64<T>(kstream, o, y0);
     store_from_f64<T>(kstream, o + 1, y1);
   }
@@ -483,9 +505,12 @@ struct Tile {
 // stream per group instead of the value rows, with no positional term and
 // the raw query; P.V, the softmax, the splits and the layout are shared, so
 // the two kernels differ only in the bytes they must stream.
-template <int HPG, int DV, int NRC, bool GQA, bool FUSED>
+// PAGED reads the caches from page pools through a block table: only the
+// addressing of a tile (and of the current row) changes.
+template <int HPG, int DV, int NRC, bool GQA, bool FUSED, bool PAGED>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
   static_assert(!(GQA && FUSED), "the GQA baseline takes the raw query");
+  static_assert(!(GQA && PAGED), "the GQA baseline reads contiguous caches");
   const DecodeArgs a = p.a;
   request_args<FUSED || GQA>(a);
   using Cfg = DecodeCfg<HPG, DV, NRC>;
@@ -506,6 +531,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int hq = h0 + col_head;
   const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
   __shared__ __attribute__((aligned(16))) uint16_t prow[DV + 32 * (NRC > 0 ? NRC : 1)];
+  __shared__ int32_t split_pages[PAGED ? kMaxPages : 1];   // paged: this split's page ids
 
   // The rows of this split are settled once the query loads are on their
   // way (they do not depend on the length), which takes a memory round trip
@@ -602,6 +628,20 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     return;
   }
 
+  // Paged: the page ids of the split's rows [r0, r1), clamped into the pool
+  // (an id outside it reads some page's data but never outside the pool).
+  const int PR = PAGED ? a.page_rows : 1;
+  const int pg0 = r0 / PR;
+  if constexpr (PAGED) {
+    const int npg = (r1 + PR - 1) / PR - pg0;
+    const int32_t* bt = a.block_table + (int64_t)b * a.max_pages + pg0;
+    for (int i = tid; i < npg; i += kThreads) {
+      const int id = bt[i];
+      split_pages[i] = id < 0 ? 0 : (id >= a.n_pages ? a.n_pages - 1 : id);
+    }
+    __syncthreads();
+  }
+
   // With the current token's rows given, the split holding row L-1 takes
   // that row from them and streams only the rows before it from the cache.
   const bool pending = !GQA && a.v_new != nullptr && L > 0 && r0 <= L - 1 && L - 1 < r1;
@@ -637,8 +677,24 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
   const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
   auto tile_row = [&](int j) { return r0 + (w + kWaves * j) * kTileRows; };
+  // Paged: the descriptors of the page holding a tile (a tile never spans
+  // pages: pages are whole multiples of 32 rows), ending at the split's last
+  // layout tile like the contiguous ones; a tile past it gets empty ones.
+  auto page_res = [&](int row0, __amdgpu_buffer_rsrc_t& vr, __amdgpu_buffer_rsrc_t& kr, int& lt) {
+    const int pg = row0 / PR;
+    const bool live = row0 < r1c;
+    const int page = live ? __builtin_amdgcn_readfirstlane(split_pages[pg - pg0]) : 0;
+    const int rows = live ? min(PR, r1c - pg * PR) : 0;
+    const uint16_t* vp = static_cast<const uint16_t*>(a.v) + ((int64_t)page * a.G + g) * PR * DV;
+    const uint16_t* kp = static_cast<const uint16_t*>(a.kr) + (int64_t)page * PR * a.d_r;
+    vr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(vp), (short)0, rows * DV * 2, kBufferWord3);
+    kr = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint16_t*>(kp), (short)0, rows * a.d_r * 2, kBufferWord3);
+    lt = (row0 - pg * PR) / kLayoutRows;
+  };
   auto load_tile = [&](TileT& t, int row0) {
-    const int lt = row0 / kLayoutRows;         // first layout tile (uniform)
+    int lt = row0 / kLayoutRows;               // first layout tile (uniform)
+    __amdgpu_buffer_rsrc_t tv = vres, tk = kres;
+    if constexpr (PAGED) page_res(row0, tv, tk, lt);
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int vsoff = (lt + hf) * v_tile_bytes;
@@ -649,11 +705,11 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       }
 #pragma unroll
       for (int c = 0; c < NC; ++c)
-        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, kAuxNT));
+        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(tv, v_lane + 1024 * c, vsoff, kAuxNT));
       const int ksoff = (lt + hf) * k_tile_bytes;
 #pragma unroll
       for (int rc = 0; rc < NRC; ++rc)
-        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], ksoff, 0));
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(tk, k_lane[rc], ksoff, 0));
     }
   };
   TileT buf[DEPTH];
@@ -674,11 +730,20 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   // round holds too many registers to overlap it).
   auto stage_current_row = [&]() {
     if (!(pending && w == 0)) return;
-    uint16_t* vcache = static_cast<uint16_t*>(a.v) + ((int64_t)b * a.G + g) * a.t_max * DV;
-    uint16_t* kcache = static_cast<uint16_t*>(a.kr) + (int64_t)b * a.t_max * a.d_r;
+    // row L-1 of stream (b, g), or, paged, row (L-1) mod page_rows of its page
+    int64_t vs = ((int64_t)b * a.G + g) * a.t_max * DV, ks = (int64_t)b * a.t_max * a.d_r;
+    int crow = L - 1;
+    if constexpr (PAGED) {
+      const int page = split_pages[(L - 1) / PR - pg0];
+      vs = ((int64_t)page * a.G + g) * PR * DV;
+      ks = (int64_t)page * PR * a.d_r;
+      crow = (L - 1) % PR;
+    }
+    uint16_t* vcache = static_cast<uint16_t*>(a.v) + vs;
+    uint16_t* kcache = static_cast<uint16_t*>(a.kr) + ks;
     if (tid < DV / 8) {
       *(reinterpret_cast<u32x4*>(prow) + tid) = pend_piece;
-      *reinterpret_cast<u32x4*>(vcache + tiled_off<uint16_t>(L - 1, 8 * tid, DV)) = pend_piece;
+      *reinterpret_cast<u32x4*>(vcache + tiled_off<uint16_t>(crow, 8 * tid, DV)) = pend_piece;
     }
     if (tid < 16 * NRC) {
       uint16_t y0b = 0, y1b = 0;
@@ -689,7 +754,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
         y0b = f64_to_bf16_rne(y0);
         y1b = f64_to_bf16_rne(y1);
         if (g == 0) {
-          const int64_t o = tiled_off<uint16_t>(L - 1, 2 * tid, a.d_r);
+          const int64_t o = tiled_off<uint16_t>(crow, 2 * tid, a.d_r);
           kcache[o] = y0b;
           kcache[o + 1] = y1b;
         }
@@ -1309,21 +1374,27 @@ int launch_status() {
 
 using DecodeFn = void (*)(DecodeParams);
 
-template <int HPG, int DV, bool FUSED>
+template <int HPG, int DV, bool FUSED, bool PAGED>
 DecodeFn pick_nrc(int nrc) {
   switch (nrc) {
-    case 0: return decode_bf16_kernel<HPG, DV, 0, false, FUSED>;
-    case 1: return decode_bf16_kernel<HPG, DV, 1, false, FUSED>;
-    case 2: return decode_bf16_kernel<HPG, DV, 2, false, FUSED>;
+    case 0: return decode_bf16_kernel<HPG, DV, 0, false, FUSED, PAGED>;
+    case 1: return decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED>;
+    case 2: return decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED>;
   }
   return nullptr;
 }
 
+template <int HPG, int DV>
+DecodeFn pick_mode(int nrc, bool fused, bool paged) {
+  if (paged) return fused ? pick_nrc<HPG, DV, true, true>(nrc) : pick_nrc<HPG, DV, false, true>(nrc);
+  return fused ? pick_nrc<HPG, DV, true, false>(nrc) : pick_nrc<HPG, DV, false, false>(nrc);
+}
+
 template <int HPG>
-DecodeFn pick_dv(int dv, int nrc, bool fused) {
+DecodeFn pick_dv(int dv, int nrc, bool fused, bool paged) {
   switch (dv) {
-    case 64: return fused ? pick_nrc<HPG, 64, true>(nrc) : pick_nrc<HPG, 64, false>(nrc);
-    case 128: return fused ? pick_nrc<HPG, 128, true>(nrc) : pick_nrc<HPG, 128, false>(nrc);
+    case 64: return pick_mode<HPG, 64>(nrc, fused, paged);
+    case 128: return pick_mode<HPG, 128>(nrc, fused, paged);
   }
   return nullptr;
 }
@@ -1331,10 +1402,10 @@ DecodeFn pick_dv(int dv, int nrc, bool fused) {
 template <int DV>
 DecodeFn pick_gqa_hpg(int hpg) {
   switch (hpg) {
-    case 1: return decode_bf16_kernel<1, DV, 0, true, false>;
-    case 2: return decode_bf16_kernel<2, DV, 0, true, false>;
-    case 4: return decode_bf16_kernel<4, DV, 0, true, false>;
-    case 8: return decode_bf16_kernel<8, DV, 0, true, false>;
+    case 1: return decode_bf16_kernel<1, DV, 0, true, false, false>;
+    case 2: return decode_bf16_kernel<2, DV, 0, true, false, false>;
+    case 4: return decode_bf16_kernel<4, DV, 0, true, false, false>;
+    case 8: return decode_bf16_kernel<8, DV, 0, true, false, false>;
   }
   return nullptr;
 }
@@ -1347,35 +1418,20 @@ DecodeFn pick_gqa_decode(int hpg, int dv) {
   return nullptr;
 }
 
-DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused) {
+DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged) {
   switch (hpg) {
-    case 1: return pick_dv<1>(dv, nrc, fused);
-    case 2: return pick_dv<2>(dv, nrc, fused);
-    case 4: return pick_dv<4>(dv, nrc, fused);
-    case 8: return pick_dv<8>(dv, nrc, fused);
+    case 1: return pick_dv<1>(dv, nrc, fused, paged);
+    case 2: return pick_dv<2>(dv, nrc, fused, paged);
+    case 4: return pick_dv<4>(dv, nrc, fused, paged);
+    case 8: return pick_dv<8>(dv, nrc, fused, paged);
   }
   return nullptr;
 }
 
-}  // namespace
-
-extern "C" {
-
-int gva_version(void) { return 10400; }
-
-const char* gva_status_string(int status) {
-  switch (status) {
-    case GVA_OK: return "ok";
-    case GVA_ERR_INVALID_ARG: return "invalid argument";
-    case GVA_ERR_UNSUPPORTED: return "unsupported shape";
-    case GVA_ERR_HIP: return "HIP runtime error";
-  }
-  return "unknown status";
-}
-
-int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const void* v_new,
-                  const void* kr_new, const int32_t* seq, const int32_t* pos, int32_t n_rows,
-                  void* stream) {
+// The append behind gva_append_kv and, with paging given, gva_paged_append_kv.
+int append_impl(const gva_dims* dims, const gva_paging* paging, const int32_t* block_table, void* v_cache,
+                void* kr_cache, const void* v_new, const void* kr_new, const int32_t* seq, const int32_t* pos,
+                int32_t n_rows, void* stream) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (n_rows < 0) return GVA_ERR_INVALID_ARG;
@@ -1400,6 +1456,10 @@ int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const voi
   p.d_v = dims->d_v;
   p.d_r = dims->d_r;
   p.n_rows = n_rows;
+  p.block_table = block_table;
+  p.page_rows = paging ? paging->page_rows : 0;
+  p.max_pages = paging ? paging->max_pages : 0;
+  p.n_pages = paging ? paging->n_pages : 0;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dims->dtype == GVA_DTYPE_BF16)
@@ -1409,45 +1469,26 @@ int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const voi
   return launch_status();
 }
 
-int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const int32_t* lens,
-                     float* q_abs, float* q_rot, void* stream) {
-  int st = check_dims(dims);
-  if (st != GVA_OK) return st;
-  if (!q || !m || !lens || !q_abs) return GVA_ERR_INVALID_ARG;
-  if (dims->d_r > 0 && !q_rot) return GVA_ERR_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(lens, 4) || !aligned(q_abs, 16) ||
-      (q_rot && !aligned(q_rot, 4)))
-    return GVA_ERR_INVALID_ARG;
-  if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
-  AbsorbParams p;
-  p.q = q;
-  p.m = m;
-  p.lens = lens;
-  p.q_abs = q_abs;
-  p.q_rot = q_rot;
-  p.B = dims->batch;
-  p.H = dims->n_heads;
-  p.d_v = dims->d_v;
-  p.d_c = dims->d_c;
-  p.d_r = dims->d_r;
-  p.t_max = dims->t_max;
-  fill_inv_freq(dims, p.inv_freq);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dims->dtype == GVA_DTYPE_BF16) {
-    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
-    const dim3 grid(dims->n_heads, (dims->batch + 15) / 16);
-    hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
-  } else {
-    hipLaunchKernelGGL(absorb_f32_kernel, dim3(dims->batch * dims->n_heads), dim3(128), 0, s, p);
-  }
-  return launch_status();
+// A paging description consistent with dims: pages of whole 32-row tiles,
+// a block-table row covering the capacity exactly, ids for at most
+// kMaxPages pages per sequence.
+int check_paging(const gva_dims* dims, const gva_paging* pg, const int32_t* block_table) {
+  if (pg == nullptr || block_table == nullptr || !aligned(block_table, 4)) return GVA_ERR_INVALID_ARG;
+  if (pg->page_rows < kTileRows || pg->page_rows % kTileRows != 0) return GVA_ERR_INVALID_ARG;
+  if (pg->max_pages < 1 || pg->n_pages < 1) return GVA_ERR_INVALID_ARG;
+  if ((long long)pg->max_pages * pg->page_rows != dims->t_max) return GVA_ERR_INVALID_ARG;
+  if (pg->max_pages > kMaxPages) return GVA_ERR_UNSUPPORTED;
+  if (dims->dtype != GVA_DTYPE_BF16) return GVA_ERR_UNSUPPORTED;
+  return GVA_OK;
 }
 
-int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, const float* q_abs,
-                         const float* q_rot, void* v_cache, void* kr_cache,
-                         const int32_t* lens, const void* v_new, const void* kr_new,
-                         int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
-                         void* stream) {
+// The attention launch behind gva_decode_attention and, with paging given,
+// gva_paged_decode_attention (v_cache / kr_cache are then the page pools).
+int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const int32_t* block_table,
+                          const void* q, const void* m, const float* q_abs, const float* q_rot,
+                          void* v_cache, void* kr_cache, const int32_t* lens, const void* v_new,
+                          const void* kr_new, int32_t num_splits, int32_t split_rows, float* o_part,
+                          float* lse_part, void* stream) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
@@ -1500,6 +1541,10 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
   p.a.split_rows = split_rows;
   p.a.scale_log2 = scale_log2(dims);
   p.a.fused = fused ? 1 : 0;
+  p.a.block_table = block_table;
+  p.a.page_rows = paging ? paging->page_rows : 0;
+  p.a.max_pages = paging ? paging->max_pages : 0;
+  p.a.n_pages = paging ? paging->n_pages : 0;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
 
@@ -1507,15 +1552,105 @@ int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, con
     if (dims->d_c % 32 != 0 || dims->d_c > 512 || dims->d_r % 8 != 0 || dims->d_r > 64)
       return GVA_ERR_UNSUPPORTED;
     const int nrc = (dims->d_r + 31) / 32;
-    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused);
+    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr);
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   } else {
+    if (paging != nullptr) return GVA_ERR_UNSUPPORTED;       // paged caches: bf16 only
     if (dims->d_v > kF32MaxDv || dims->d_c > 512 || dims->d_r > kF32MaxDr || hpg > kF32MaxHpg)
       return GVA_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(decode_f32_kernel, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   }
   return launch_status();
+}
+
+}  // namespace
+
+extern "C" {
+
+int gva_version(void) { return 10500; }
+
+const char* gva_status_string(int status) {
+  switch (status) {
+    case GVA_OK: return "ok";
+    case GVA_ERR_INVALID_ARG: return "invalid argument";
+    case GVA_ERR_UNSUPPORTED: return "unsupported shape";
+    case GVA_ERR_HIP: return "HIP runtime error";
+  }
+  return "unknown status";
+}
+
+int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const void* v_new,
+                  const void* kr_new, const int32_t* seq, const int32_t* pos, int32_t n_rows,
+                  void* stream) {
+  return append_impl(dims, nullptr, nullptr, v_cache, kr_cache, v_new, kr_new, seq, pos, n_rows, stream);
+}
+
+int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const int32_t* lens,
+                     float* q_abs, float* q_rot, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  if (!q || !m || !lens || !q_abs) return GVA_ERR_INVALID_ARG;
+  if (dims->d_r > 0 && !q_rot) return GVA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(lens, 4) || !aligned(q_abs, 16) ||
+      (q_rot && !aligned(q_rot, 4)))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
+  AbsorbParams p;
+  p.q = q;
+  p.m = m;
+  p.lens = lens;
+  p.q_abs = q_abs;
+  p.q_rot = q_rot;
+  p.B = dims->batch;
+  p.H = dims->n_heads;
+  p.d_v = dims->d_v;
+  p.d_c = dims->d_c;
+  p.d_r = dims->d_r;
+  p.t_max = dims->t_max;
+  fill_inv_freq(dims, p.inv_freq);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dims->dtype == GVA_DTYPE_BF16) {
+    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
+    const dim3 grid(dims->n_heads, (dims->batch + 15) / 16);
+    hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(absorb_f32_kernel, dim3(dims->batch * dims->n_heads), dim3(128), 0, s, p);
+  }
+  return launch_status();
+}
+
+
+int gva_decode_attention(const gva_dims* dims, const void* q, const void* m, const float* q_abs,
+                         const float* q_rot, void* v_cache, void* kr_cache,
+                         const int32_t* lens, const void* v_new, const void* kr_new,
+                         int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
+                         void* stream) {
+  return decode_attention_impl(dims, nullptr, nullptr, q, m, q_abs, q_rot, v_cache, kr_cache, lens, v_new,
+                               kr_new, num_splits, split_rows, o_part, lse_part, stream);
+}
+
+int gva_paged_decode_attention(const gva_dims* dims, const gva_paging* paging, const void* q, const void* m,
+                               const float* q_abs, const float* q_rot, void* v_pool, void* kr_pool,
+                               const int32_t* block_table, const int32_t* lens, const void* v_new,
+                               const void* kr_new, int32_t num_splits, int32_t split_rows, float* o_part,
+                               float* lse_part, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  st = check_paging(dims, paging, block_table);
+  if (st != GVA_OK) return st;
+  return decode_attention_impl(dims, paging, block_table, q, m, q_abs, q_rot, v_pool, kr_pool, lens, v_new,
+                               kr_new, num_splits, split_rows, o_part, lse_part, stream);
+}
+
+int gva_paged_append_kv(const gva_dims* dims, const gva_paging* paging, void* v_pool, void* kr_pool,
+                        const int32_t* block_table, const void* v_new, const void* kr_new, const int32_t* seq,
+                        const int32_t* pos, int32_t n_rows, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  st = check_paging(dims, paging, block_table);
+  if (st != GVA_OK) return st;
+  return append_impl(dims, paging, block_table, v_pool, kr_pool, v_new, kr_new, seq, pos, n_rows, stream);
 }
 
 int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stride,

@@ -21,7 +21,9 @@ GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, 1, 2, 3
 GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
-           "gva_gqa_decode_attention", "gva_pick_splits", "gva_status_string", "gva_version")
+           "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
+           "gva_pick_splits", "gva_status_string", "gva_version")
+GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
 
@@ -46,6 +48,11 @@ class GvaDims(ctypes.Structure):
         return ("GvaDims(" + ", ".join(f"{k}={getattr(self, k)}" for k, _ in self._fields_) + ")")
 
 
+class GvaPaging(ctypes.Structure):
+    _fields_ = [("page_rows", ctypes.c_int32), ("max_pages", ctypes.c_int32),
+                ("n_pages", ctypes.c_int32)]
+
+
 _lib = None
 
 
@@ -63,13 +70,17 @@ def lib() -> ctypes.CDLL:
         L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
         L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, I32, P, P, P]
+        PG = ctypes.POINTER(GvaPaging)
+        L.gva_paged_append_kv.argtypes = [D, PG, P, P, P, P, P, P, P, I32, P]
+        L.gva_paged_decode_attention.argtypes = [D, PG, P, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32, ctypes.POINTER(I32)]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
         L.gva_probe_read.argtypes = [P, ctypes.c_int64, I32, P, P]
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
-                     "gva_gqa_decode_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
+                     "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
+                     "gva_pick_splits", "gva_version", "gva_probe_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -209,6 +220,88 @@ def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_split
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
         _stream(stream))
     _check("gva_gqa_decode_attention", st)
+
+
+def gva_paged_append_kv(dims: GvaDims, paging: GvaPaging, v_pool, kr_pool, block_table, v_new, kr_new,
+                        seq, pos, stream=None):
+    d, pg = dims, paging
+    dt = d.torch_dtype
+    n = int(seq.numel())
+    st = lib().gva_paged_append_kv(
+        ctypes.byref(d), ctypes.byref(pg),
+        _ptr(v_pool, "v_pool", dt, (pg.n_pages, d.n_groups, pg.page_rows, d.d_v)),
+        _ptr(kr_pool, "kr_pool", dt, (pg.n_pages, pg.page_rows, d.d_r)),
+        _ptr(block_table, "block_table", torch.int32, (d.batch, pg.max_pages)),
+        _ptr(v_new, "v_new", dt, (n, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (n, d.d_r)),
+        _ptr(seq, "seq", torch.int32, (n,)),
+        _ptr(pos, "pos", torch.int32, (n,)),
+        n, _stream(stream))
+    _check("gva_paged_append_kv", st)
+
+
+def gva_paged_decode_attention(dims: GvaDims, paging: GvaPaging, v_pool, kr_pool, block_table, lens,
+                               num_splits: int, o_part, lse_part, q=None, m=None, q_abs=None, q_rot=None,
+                               v_new=None, kr_new=None, split_rows: int = 0, stream=None):
+    d, pg = dims, paging
+    dt = d.torch_dtype
+    S = int(num_splits)
+    st = lib().gva_paged_decode_attention(
+        ctypes.byref(d), ctypes.byref(pg),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(q_abs, "q_abs", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(q_rot, "q_rot", torch.float32, (d.batch, d.n_heads, d.d_r)),
+        _ptr(v_pool, "v_pool", dt, (pg.n_pages, d.n_groups, pg.page_rows, d.d_v)),
+        _ptr(kr_pool, "kr_pool", dt, (pg.n_pages, pg.page_rows, d.d_r)),
+        _ptr(block_table, "block_table", torch.int32, (d.batch, pg.max_pages)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(v_new, "v_new", dt, (d.batch, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (d.batch, d.d_r)),
+        S, int(split_rows),
+        _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
+        _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
+        _stream(stream))
+    _check("gva_paged_decode_attention", st)
+
+
+def make_paging(dims: GvaDims, page_rows: int, n_pages: int) -> GvaPaging:
+    if dims.t_max % page_rows:
+        raise ValueError("t_max must be a whole number of pages")
+    return GvaPaging(int(page_rows), dims.t_max // int(page_rows), int(n_pages))
+
+
+def to_pages(v_tiled: torch.Tensor, kr_tiled: torch.Tensor, block_table: torch.Tensor, paging: GvaPaging,
+             fill=0.0):
+    """Page pools holding tiled contiguous caches [B,G,T,d_v] / [B,T,d_r]
+    (library layout) at the pages the block table names: page block (p, g)
+    of the pool is the page_rows-row slice of stream (b, g) that
+    block_table[b][t / page_rows] = p maps there.  Pages no entry names
+    hold ``fill``.  Storage plumbing: a page boundary is a layout-tile
+    boundary, so the slices move as they are."""
+    B, G, T, dv = v_tiled.shape
+    PR, MP = paging.page_rows, paging.max_pages
+    v_pool = torch.full((paging.n_pages, G, PR, dv), fill, dtype=v_tiled.dtype, device=v_tiled.device)
+    kr_pool = torch.full((paging.n_pages, PR, kr_tiled.shape[-1]), fill, dtype=kr_tiled.dtype,
+                         device=kr_tiled.device)
+    bt = block_table.to(torch.long).to(v_tiled.device)
+    vb = v_tiled.reshape(B, G, MP, PR, dv).permute(0, 2, 1, 3, 4)      # [B, MP, G, PR, dv]
+    kb = kr_tiled.reshape(B, MP, PR, kr_tiled.shape[-1])
+    valid = (bt >= 0) & (bt < paging.n_pages)
+    v_pool[bt[valid]] = vb[valid]
+    kr_pool[bt[valid]] = kb[valid]
+    return v_pool, kr_pool
+
+
+def from_pages(v_pool: torch.Tensor, kr_pool: torch.Tensor, block_table: torch.Tensor, paging: GvaPaging):
+    """Inverse of :func:`to_pages` for every block-table entry: the tiled
+    contiguous caches [B,G,T,d_v] / [B,T,d_r] the pools hold."""
+    n_pages, G, PR, dv = v_pool.shape
+    B, MP = block_table.shape
+    bt = block_table.to(torch.long).to(v_pool.device).clamp(0, n_pages - 1)
+    v = v_pool[bt].permute(0, 2, 1, 3, 4).reshape(B, G, MP * PR, dv)
+    kr = kr_pool[bt].reshape(B, MP * PR, kr_pool.shape[-1])
+    return v.contiguous(), kr.contiguous()
 
 
 def gva_pick_splits(dims: GvaDims, max_len: int = 0, total_len: int = 0, n_cu: int = 0,
@@ -357,3 +450,29 @@ def probe_read_bandwidth(nbytes: int = 2 << 30, reps: int = 10, stream=None) -> 
             best = (gbs, wg)
     del buf
     return best
+
+
+def paged_decode(dims: GvaDims, paging: GvaPaging, q, m, v_pool, kr_pool, block_table, lens, num_splits: int,
+                 bufs: Optional[DecodeBuffers] = None, fused: Optional[bool] = None, v_new=None, kr_new=None,
+                 split_rows: int = 0, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """decode() on paged caches."""
+    S = int(num_splits)
+    if fused is None:
+        fused = prefer_fused(dims, S)
+    if bufs is None or bufs.num_splits != S:
+        bufs = DecodeBuffers(dims, S, device=v_pool.device)
+    pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)
+    if fused:
+        gva_paged_decode_attention(dims, paging, v_pool, kr_pool, block_table, lens, S, bufs.o_part,
+                                   bufs.lse_part, q=q, m=m, stream=stream, **pend)
+    else:
+        q_abs = torch.empty(dims.batch, dims.n_heads, dims.d_v, dtype=torch.float32, device=v_pool.device)
+        q_rot = torch.empty(dims.batch, dims.n_heads, dims.d_r, dtype=torch.float32, device=v_pool.device)
+        gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
+        gva_paged_decode_attention(dims, paging, v_pool, kr_pool, block_table, lens, S, bufs.o_part,
+                                   bufs.lse_part, q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None,
+                                   stream=stream, **pend)
+    if S == 1:
+        return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
+    gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
+    return bufs.o, bufs.lse

@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
     # every header under include/ is one of the two
     assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["gva.h", "gva_probe.h"]
-    assert gva.gva_version() == 10400
+    assert gva.gva_version() == 10500
 
 
 def test_status_strings():
@@ -208,3 +208,46 @@ def test_probe_validation():
     assert lib.gva_probe_read(A, 8, 8, A, None) == 1            # under one 16-byte piece
     assert lib.gva_probe_read(A, 1 << 20, 0, A, None) == 1
     assert lib.gva_probe_read(A + 4, 1 << 20, 8, A, None) == 1
+
+
+def paged_status(d, pg, v=A, kr=A, bt=A, lens=A, S=2, rows=0, op=A, lp=A):
+    return gva.lib().gva_paged_decode_attention(ctypes.byref(d), ctypes.byref(pg) if pg is not None else None,
+                                                A, A, None, None, v, kr, bt, lens, None, None, S, rows, op,
+                                                lp, None)
+
+
+def test_paged_validation():
+    d = dims(t_max=256)
+    ok = gva.GvaPaging(64, 4, 10)
+    for pg in (gva.GvaPaging(48, 4, 10),        # not whole 32-row tiles
+               gva.GvaPaging(0, 4, 10), gva.GvaPaging(64, 0, 10), gva.GvaPaging(64, 4, 0),
+               gva.GvaPaging(64, 3, 10)):       # capacity != t_max
+        assert paged_status(d, pg) == gva.GVA_ERR_INVALID_ARG, (pg.page_rows, pg.max_pages, pg.n_pages)
+    assert paged_status(d, None) == gva.GVA_ERR_INVALID_ARG
+    assert paged_status(d, ok, bt=None) == gva.GVA_ERR_INVALID_ARG
+    assert paged_status(d, ok, bt=A + 2) == gva.GVA_ERR_INVALID_ARG
+    assert paged_status(d, ok, v=A + 2) == gva.GVA_ERR_INVALID_ARG
+    assert paged_status(dims(t_max=256, dtype="f32"), ok) == gva.GVA_ERR_UNSUPPORTED
+    big = dims(t_max=32 * (gva.GVA_MAX_PAGES + 1))
+    assert paged_status(big, gva.GvaPaging(32, gva.GVA_MAX_PAGES + 1, 10)) == gva.GVA_ERR_UNSUPPORTED
+    lib = gva.lib()
+    assert lib.gva_paged_append_kv(ctypes.byref(d), ctypes.byref(ok), A, A, A, A, A, A, A, 0, None) == gva.GVA_OK
+    assert lib.gva_paged_append_kv(ctypes.byref(d), ctypes.byref(gva.GvaPaging(64, 3, 10)), A, A, A, A, A, A,
+                                   A, 2, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_paged_append_kv(ctypes.byref(d), ctypes.byref(ok), A, A, None, A, A, A, A, 2,
+                                   None) == gva.GVA_ERR_INVALID_ARG
+
+
+def test_page_plumbing_round_trip():
+    import torch
+    d = gva.make_dims(3, 8, 2, 64, 64, 16, 256, "bf16")
+    pg = gva.make_paging(d, 64, 14)
+    bt = torch.randperm(14, generator=torch.Generator().manual_seed(1))[:12].reshape(3, 4).to(torch.int32)
+    v = torch.randn(3, 2, 256, 64).to(torch.bfloat16)
+    kr = torch.randn(3, 256, 16).to(torch.bfloat16)
+    vp, kp = gva.to_pages(gva.tiled(v), gva.tiled(kr), bt, pg)
+    v2, k2 = gva.from_pages(vp, kp, bt, pg)
+    assert torch.equal(gva.untiled(v2), v) and torch.equal(gva.untiled(k2), kr)
+    # a page block is the tiled layout of that page's rows
+    page = int(bt[1, 2])
+    assert torch.equal(gva.untiled(vp[page]), v[1, :, 128:192])

@@ -521,3 +521,72 @@ def test_graph_capture_of_layer_steps(S, fused):
         assert float(scratch) == float(scratch)
         for o, e in zip(graphed, eager):
             assert torch.equal(o, e), f"replay {rep} differs from eager"
+
+
+
+# ------------------------------------------------------------ paged caches
+def _paged_setup(w, seed, lens, page_rows, extra_pages=5):
+    inp = gva_inputs.make_inputs(w, seed, lens=lens)
+    d = dims_of(w)
+    max_pages = w.t_max // page_rows
+    n_pages = w.batch * max_pages + extra_pages
+    g = torch.Generator().manual_seed(seed + 1)
+    bt = torch.randperm(n_pages, generator=g)[: w.batch * max_pages].reshape(w.batch, max_pages).to(torch.int32)
+    pg = gva.make_paging(d, page_rows, n_pages)
+    return inp, d, pg, bt
+
+
+@pytest.mark.parametrize("page_rows", [32, 64, 256])
+def test_paged_decode_matches_oracle(page_rows):
+    # the caches scattered over a pool in random page order; unused pages
+    # hold NaN, so reading a wrong page poisons the output
+    w = gva_inputs.Workload("paged", 6, 512, 16, 4, 128, 128, 16)
+    lens = torch.tensor([512, 0, 1, page_rows - 1, page_rows + 1, 300], dtype=torch.int32)
+    inp, d, pg, bt = _paged_setup(w, 31, lens, page_rows)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"])
+    vp, kp = gva.to_pages(gva.tiled(inp["v"]), gva.tiled(inp["kr"]), bt, pg, fill=float("nan"))
+    dev = upload({k: inp[k] for k in ("q", "m", "lens")})
+    vp, kp, btd = vp.cuda(), kp.cuda(), bt.cuda()
+    for S, rows, fused in ((1, 0, True), (3, 0, False), (12, 64, False), (2, 0, True)):
+        note(f"paged page_rows={page_rows} S={S} split_rows={rows} fused={fused}")
+        o, lse = gva.paged_decode(d, pg, dev["q"], dev["m"], vp, kp, btd, dev["lens"], S, fused=fused,
+                                  split_rows=rows)
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"paged/{page_rows}/S{S}/rows{rows}/fused={fused}")
+
+
+def test_paged_append_and_current_row():
+    # the paged append and the current row appended in the attention launch
+    # write exactly what the contiguous append writes, at the right pages
+    page_rows = 64
+    w = gva_inputs.Workload("paged", 4, 256, 8, 2, 128, 128, 16)
+    lens = torch.tensor([256, 65, 1, 128], dtype=torch.int32)
+    inp, d, pg, bt = _paged_setup(w, 37, lens, page_rows)
+    seq = torch.arange(w.batch, dtype=torch.int32)
+    pos = (lens - 1).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"])
+    vp0, kp0 = gva.to_pages(gva.tiled(inp["v"]), gva.tiled(inp["kr"]), bt, pg)
+    dev = upload({k: inp[k] for k in ("q", "m", "lens", "v_new", "kr_new")})
+    btd = bt.cuda()
+    itype = torch.int16
+    # 1) the paged append call
+    vp, kp = vp0.clone().cuda(), kp0.clone().cuda()
+    note("paged append")
+    gva.gva_paged_append_kv(d, pg, vp, kp, btd, dev["v_new"], dev["kr_new"], seq.cuda(), pos.cuda())
+    torch.cuda.synchronize()
+    v2, k2 = gva.from_pages(vp.cpu(), kp.cpu(), bt, pg)
+    assert torch.equal(gva.untiled(v2).view(itype), v_ref.view(itype))
+    assert torch.equal(gva.untiled(k2).view(itype), k_ref.view(itype))
+    # 2) appended and attended in one launch
+    for S, fused in ((1, True), (3, False)):
+        vp, kp = vp0.clone().cuda(), kp0.clone().cuda()
+        note(f"paged current row S={S} fused={fused}")
+        o, lse = gva.paged_decode(d, pg, dev["q"], dev["m"], vp, kp, btd, dev["lens"], S, fused=fused,
+                                  v_new=dev["v_new"], kr_new=dev["kr_new"])
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"paged current row S{S}")
+        v2, k2 = gva.from_pages(vp.cpu(), kp.cpu(), bt, pg)
+        assert torch.equal(gva.untiled(v2).view(itype), v_ref.view(itype))
+        assert torch.equal(gva.untiled(k2).view(itype), k_ref.view(itype))
