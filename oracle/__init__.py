@@ -59,6 +59,9 @@ def _load():
         lib.gva_oracle_combine.restype = None
         lib.gva_oracle_gqa_decode.argtypes = [I, I, I, I, I, I, I, P, I, P, P, I, P, D, I, P, P]
         lib.gva_oracle_gqa_decode.restype = None
+        lib.gva_oracle_rope_decode.argtypes = [I, I, I, I, I, I, P, I, P, I, P, I, P, D, D,
+                                               ctypes.c_int64, I, P, P]
+        lib.gva_oracle_rope_decode.restype = None
         lib.gva_oracle_max_threads.argtypes = []
         lib.gva_oracle_max_threads.restype = I
         _lib = lib
@@ -194,6 +197,22 @@ def gqa_decode(q: torch.Tensor, k: torch.Tensor, v: torch.Tensor, lens: torch.Te
     _load().gva_oracle_gqa_decode(B, H, G, T, dv, dk, qc.shape[-1], _ptr(qc), _code(qc),
                                   _ptr(kc), _ptr(vc), _code(vc), _ptr(lc), float(scale),
                                   int(n_threads), _ptr(o), _ptr(lse))
+    return o, lse
+
+
+def rope_decode(q: torch.Tensor, m: torch.Tensor, v: torch.Tensor, lens: torch.Tensor,
+                rope_base: float = 10000.0, scale: float = 0.0, shift: int = 0, n_threads: int = 0):
+    """GVA without decoupled RoPE in fp64: keys reconstructed (v M_h) and
+    rotated over their full width d_c, query rotated at L-1.  q [B,H,d_c]."""
+    B, G, T, dv = v.shape
+    H, dc = q.shape[1], q.shape[2]
+    qc, mc, vc = _cpu(q), _cpu(m), _cpu(v)
+    lc = _cpu(lens.to(torch.int32))
+    o = torch.empty(B, H, dv, dtype=torch.float64)
+    lse = torch.empty(B, H, dtype=torch.float64)
+    _load().gva_oracle_rope_decode(B, H, G, T, dv, dc, _ptr(qc), _code(qc), _ptr(mc), _code(mc),
+                                   _ptr(vc), _code(vc), _ptr(lc), float(scale), float(rope_base),
+                                   int(shift), int(n_threads), _ptr(o), _ptr(lse))
     return o, lse
 
 

@@ -233,6 +233,69 @@ void gva_oracle_decode(int B, int H, int G, int T_max, int d_v, int d_c, int d_r
   }
 }
 
+/* GVA without decoupled RoPE (Section 3.2: the ordinary-RoPE variants the
+ * paper evaluates, which cannot absorb M_h at decode), for every (b, h):
+ *   k_t = RoPE(V[b, g(h), t, :] M_h, t + shift)        (key reconstructed,
+ *                                                        rotated over d_c)
+ *   q'  = RoPE(q[b, h, :], L-1 + shift)
+ *   s[t] = scale * q' . k_t,   o = sum_t softmax(s)[t] V[b, g(h), t, :]
+ * RoPE here acts on the whole d_c-wide key (theta_i = base^(-2i/d_c)).
+ * scale <= 0 selects 1/sqrt(d_c).  q is [B][H][d_c].  shift moves every
+ * position by the same amount (the scores depend only on differences). */
+void gva_oracle_rope_decode(int B, int H, int G, int T_max, int d_v, int d_c,
+                            const void* q, int dt_q, const void* m, int dt_m,
+                            const void* v_cache, int dt_cache, const int32_t* lens,
+                            double scale, double rope_base, int64_t shift, int n_threads,
+                            double* o, double* lse) {
+  if (scale <= 0.0) scale = 1.0 / sqrt((double)d_c);
+  const int hpg = H / G;
+  const int n_pairs = B * H;
+#ifdef _OPENMP
+  if (n_threads > 0) omp_set_num_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int bh = 0; bh < n_pairs; ++bh) {
+    const int b = bh / H, h = bh % H, g = h / hpg;
+    int L = lens[b];
+    if (L < 0) L = 0;
+    if (L > T_max) L = T_max;
+    double* out = o + (int64_t)bh * d_v;
+    for (int i = 0; i < d_v; ++i) out[i] = 0.0;
+    if (L == 0) { lse[bh] = -INFINITY; continue; }
+    double* qraw = (double*)malloc(sizeof(double) * (size_t)d_c);
+    double* qrot = (double*)malloc(sizeof(double) * (size_t)d_c);
+    double* k = (double*)malloc(sizeof(double) * (size_t)d_c);
+    double* krot = (double*)malloc(sizeof(double) * (size_t)d_c);
+    double* s = (double*)malloc(sizeof(double) * (size_t)L);
+    for (int c = 0; c < d_c; ++c) qraw[c] = ld(q, (int64_t)bh * d_c + c, dt_q);
+    gva_oracle_rope(qraw, d_c, (int64_t)(L - 1) + shift, rope_base, qrot);
+    const int64_t vbase = ((int64_t)b * G + g) * T_max;
+    for (int t = 0; t < L; ++t) {
+      for (int c = 0; c < d_c; ++c) {         /* k = v M_h: k[c] = sum_i v[i] M_h[i][c] */
+        double acc = 0.0;
+        for (int i = 0; i < d_v; ++i)
+          acc += ld(v_cache, (vbase + t) * d_v + i, dt_cache) * ld(m, ((int64_t)h * d_v + i) * d_c + c, dt_m);
+        k[c] = acc;
+      }
+      gva_oracle_rope(k, d_c, (int64_t)t + shift, rope_base, krot);
+      double dot = 0.0;
+      for (int c = 0; c < d_c; ++c) dot += qrot[c] * krot[c];
+      s[t] = scale * dot;
+    }
+    double mx = -INFINITY;
+    for (int t = 0; t < L; ++t) mx = s[t] > mx ? s[t] : mx;
+    double z = 0.0;
+    for (int t = 0; t < L; ++t) {
+      double w = exp(s[t] - mx);
+      z += w;
+      for (int i = 0; i < d_v; ++i) out[i] += w * ld(v_cache, (vbase + t) * d_v + i, dt_cache);
+    }
+    for (int i = 0; i < d_v; ++i) out[i] /= z;
+    lse[bh] = mx + log(z);
+    free(qraw); free(qrot); free(k); free(krot); free(s);
+  }
+}
+
 /* Log-sum-exp merge of partial results over disjoint row ranges:
  *   LSE = log sum_s exp(lse_s),  o = sum_s exp(lse_s - LSE) o_s.
  * Partials with lse_s = -inf carry no rows and are skipped; if all are, the

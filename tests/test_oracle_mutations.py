@@ -24,6 +24,12 @@ MUTANTS = [
     ("query position", "const int64_t p = L > 0 ? L - 1 : 0;", "const int64_t p = L;"),
     ("combine weight", "double w = exp(x - big);", "double w = exp(x - mx);"),
     ("double rounding", "double n = nearbyint(scaled);", "double n = nearbyint((double)(float)scaled);"),
+    ("rope-decode key position", "gva_oracle_rope(k, d_c, (int64_t)t + shift, rope_base, krot);",
+     "gva_oracle_rope(k, d_c, (int64_t)(L - 1 - t) + shift, rope_base, krot);"),
+    ("rope-decode scale", "if (scale <= 0.0) scale = 1.0 / sqrt((double)d_c);",
+     "if (scale <= 0.0) scale = 1.0 / sqrt((double)d_v);"),
+    ("rope-decode transposed M", "ld(m, ((int64_t)h * d_v + i) * d_c + c, dt_m)",
+     "ld(m, ((int64_t)h * d_c + c) * d_v + i, dt_m)"),
     ("last row dropped", "for (int t = 0; t < n; ++t) {\n      double w", "for (int t = 0; t < n - 1; ++t) {\n      double w"),
 ]
 
@@ -39,6 +45,9 @@ PIN_TESTS = [
     lambda o: pins.test_split_and_combine_equals_unsplit(o, 5, 32),
     lambda o: pins.test_round_bf16_single_rounding(o),
     lambda o: pins.test_zero_query_gives_mean_value(o),
+    lambda o: pins.test_rope_decode_matches_explicit_construction(o, 4, 2),
+    lambda o: pins.test_rope_decode_scores_are_a_relative_rotation(o),
+    lambda o: pins.test_rope_decode_shift_and_edge_cases(o),
 ]
 
 

@@ -379,6 +379,100 @@ def test_gqa_oracle_is_textbook_sdpa(orc):
             assert torch.allclose(o[b, h], ref, rtol=0, atol=1e-13)
 
 
+# ------------------------------------- GVA without decoupled RoPE (Sec. 3.2)
+def explicit_rope_decode(q, m, v, lens, scale=None, base=10000.0, shift=0):
+    """Keys materialised as k_t = v_t M_h and rotated at t + shift over their
+    whole width, the query rotated at L-1+shift, textbook SDPA in float64."""
+    q, m, v = (t.to(torch.float64) for t in (q, m, v))
+    B, G, T, dv = v.shape
+    H, dc = q.shape[1], q.shape[2]
+    hpg = H // G
+    scale = 1.0 / math.sqrt(dc) if scale is None else scale
+    o = torch.zeros(B, H, dv, dtype=torch.float64)
+    lse = torch.full((B, H), -math.inf, dtype=torch.float64)
+    for b in range(B):
+        L = int(lens[b])
+        if L == 0:
+            continue
+        for h in range(H):
+            g = h // hpg
+            K = (v[b, g, :L] @ m[h]).numpy()
+            Kr = np.stack([rope_complex(K[t], t + shift, base) for t in range(L)])
+            qr = rope_complex(q[b, h].numpy(), L - 1 + shift, base)
+            Kt = torch.from_numpy(Kr)
+            qt = torch.from_numpy(qr)
+            o[b, h] = F.scaled_dot_product_attention(
+                qt.view(1, 1, 1, dc), Kt.view(1, 1, L, dc),
+                v[b, g, :L].reshape(1, 1, L, dv), scale=scale).view(dv)
+            lse[b, h] = torch.logsumexp((Kt @ qt) * scale, dim=0)
+    return o, lse
+
+
+def rope_tiny_inputs(seed, B=2, H=4, G=2, T=29, dv=16, dc=12, lens=None):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(B, H, dc, generator=g, dtype=torch.float64)
+    v = torch.randn(B, G, T, dv, generator=g, dtype=torch.float64)
+    m = torch.randn(H, dv, dc, generator=g, dtype=torch.float64) / math.sqrt(dv)
+    if lens is None:
+        lens = torch.randint(1, T + 1, (B,), generator=g, dtype=torch.int32)
+    return q, m, v, torch.as_tensor(lens, dtype=torch.int32)
+
+
+@pytest.mark.parametrize("H,G", [(4, 2), (4, 1), (6, 3)])
+def test_rope_decode_matches_explicit_construction(orc, H, G):
+    # non-square M (d_v=16, d_c=12): a transposed map cannot pass
+    q, m, v, lens = rope_tiny_inputs(71 + H + G, H=H, G=G, lens=[29, 9])
+    o, lse = orc.rope_decode(q, m, v, lens)
+    o_ref, lse_ref = explicit_rope_decode(q, m, v, lens)
+    assert torch.allclose(o, o_ref, rtol=0, atol=1e-12)
+    assert torch.allclose(lse, lse_ref, rtol=0, atol=1e-12)
+
+
+def test_rope_decode_scores_are_a_relative_rotation(orc):
+    # With pairs as complex numbers, RoPE(x, P) . RoPE(y, t) = Re(x conj(y)
+    # e^{-i theta d}), d = t - P; per pair that is a cos(theta d) + b sin(theta d)
+    # with a = x_2i y_2i + x_2i+1 y_2i+1 and b = x_2i+1 y_2i - x_2i y_2i+1.
+    # A two-row cache with one zero row makes the weights that closed form.
+    dc, dv, L = 8, 8, 2
+    g = torch.Generator().manual_seed(73)
+    q = torch.randn(1, 1, dc, generator=g, dtype=torch.float64)
+    m = torch.eye(dv, dtype=torch.float64).view(1, dv, dc)
+    v = torch.zeros(1, 1, L, dv, dtype=torch.float64)
+    v[0, 0, 1] = torch.randn(dv, generator=g, dtype=torch.float64)
+    o, lse = orc.rope_decode(q, m, v, torch.tensor([L], dtype=torch.int32))
+    # row 1 is the query's own position: d = 0, the score is plain q . v_1
+    s1 = float(q[0, 0] @ v[0, 0, 1]) / math.sqrt(dc)
+    w1 = 1.0 / (1.0 + math.exp(-s1))              # row 0 scores 0
+    assert torch.allclose(o[0, 0], w1 * v[0, 0, 1], rtol=0, atol=1e-14)
+    assert abs(float(lse[0, 0]) - math.log(1.0 + math.exp(s1))) < 1e-14
+    # move the nonzero row to position 0: d = -1 rotates each pair by -theta_i
+    v2 = v.flip(2).contiguous()
+    o2, _ = orc.rope_decode(q, m, v2, torch.tensor([L], dtype=torch.int32))
+    x, y = q[0, 0].numpy(), v2[0, 0, 0].numpy()
+    theta = 10000.0 ** (-np.arange(0, dc, 2, dtype=np.float64) / dc)
+    dot = x[0::2] * y[0::2] + x[1::2] * y[1::2]
+    cross = x[1::2] * y[0::2] - x[0::2] * y[1::2]
+    s0 = float(np.sum(dot * np.cos(-theta) + cross * np.sin(-theta))) / math.sqrt(dc)
+    w0 = 1.0 / (1.0 + math.exp(-s0))
+    assert torch.allclose(o2[0, 0], w0 * v2[0, 0, 0], rtol=0, atol=1e-14)
+
+
+def test_rope_decode_shift_and_edge_cases(orc):
+    q, m, v, lens = rope_tiny_inputs(79, lens=[29, 1])
+    o, lse = orc.rope_decode(q, m, v, lens)
+    o2, lse2 = orc.rope_decode(q, m, v, lens, shift=4321)
+    assert torch.allclose(o, o2, rtol=0, atol=1e-10)
+    assert torch.allclose(lse, lse2, rtol=0, atol=1e-10)
+    for h in range(4):                            # one row: its value, any query
+        assert torch.allclose(o[1, h], v[1, h // 2, 0], rtol=0, atol=1e-15)
+    o0, lse0 = orc.rope_decode(q, m, v, torch.tensor([0, 3], dtype=torch.int32))
+    assert torch.all(o0[0] == 0) and torch.all(torch.isneginf(lse0[0]))
+    # the rotation is not absorbable: the decoupled-RoPE decode with d_r = 0
+    # (no rotation anywhere) gives a different result on the same inputs
+    oa, _ = orc.decode(q, m, v, torch.zeros(2, v.shape[2], 0, dtype=torch.float64), lens)
+    assert (oa[0] - o[0]).abs().max() > 1e-3
+
+
 # ------------------------------------------------- figures the paper prints
 def _golden_rows(name):
     rows = []
