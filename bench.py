@@ -38,6 +38,7 @@ from paper_2609_13285_amd import gva, traffic  # noqa: E402
 
 METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s, B=32 T=8K bf16"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD's published figure
+MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, AMD's published figure
 KERNEL_SRC = os.path.join(ROOT, "paper_2609_13285_amd", "csrc", "gva.hip")
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_b32_t8k.json")
 
@@ -294,6 +295,73 @@ def gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches, stream):
             "gqa_GBps": round(b_gqa / (t_gqa * 1e-3) / 1e9, 1)}
 
 
+def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
+    """GVA with ordinary RoPE (keys reconstructed and rotated per position,
+    the variant that cannot absorb M_h) against absorbed GVA without a
+    positional slice, on the same values, lengths, query content slice and
+    maps: attention + combine, caches as stored, same split plan.  The
+    contrast kernel is bound by the matrix cores, not by HBM: its roofline
+    is priced in bf16 MFMA flops."""
+    n = len(caches)
+    d0 = gva.make_dims(w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, 0, w.t_max, w.dtype, w.rope_base)
+    q0 = dev["q"][..., :w.d_c].contiguous()
+    bufs = gva.DecodeBuffers(d0, S)
+    fused0 = gva.prefer_fused(d0, S)
+    q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+
+    def combine():
+        if S > 1:
+            gva.gva_combine(d0, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
+
+    def absorbed(i):
+        vc = caches[i % n][0]
+        if fused0:
+            gva.gva_decode_attention(d0, vc, None, dev["lens"], S, bufs.o_part, bufs.lse_part,
+                                     q=q0, m=dev["m"], split_rows=split_rows, stream=stream)
+        else:
+            gva.gva_absorb_query(d0, q0, dev["m"], dev["lens"], q_abs, None, stream)
+            gva.gva_decode_attention(d0, vc, None, dev["lens"], S, bufs.o_part, bufs.lse_part,
+                                     q_abs=q_abs, split_rows=split_rows, stream=stream)
+        combine()
+
+    def rope(i, ev_a=None, ev_b=None):
+        if ev_a is not None:
+            ev_a.record(stream)
+        gva.gva_rope_decode_attention(d0, q0, dev["m"], caches[i % n][0], dev["lens"], S,
+                                      bufs.o_part, bufs.lse_part, split_rows=split_rows, stream=stream)
+        if ev_b is not None:
+            ev_b.record(stream)
+        combine()
+
+    for i in range(args.warmup):
+        absorbed(i)
+        rope(i)
+    t_abs = timed(absorbed, args.steps, stream)
+    t_rope = timed(rope, args.steps, stream)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+           for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        rope(i, a, b)
+    torch.cuda.synchronize()
+    kt = sorted(a.elapsed_time(b) for a, b in evs)
+    k_ms = sum(kt) / len(kt)
+    rows = int(inp["lens"].clamp(min=0).sum())
+    flops = traffic.rope_decode_flops(rows, w.n_heads, w.d_v, w.d_c)
+    bytes_ = traffic.decode_bytes(inp["lens"], w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, 0, 2)
+    tflops = flops / (k_ms * 1e-3) / 1e12
+    return {"what": "attention only (caches as stored): GVA with ordinary RoPE (per-position key "
+                    "reconstruction) vs absorbed GVA with d_r = 0, same inputs and split plan",
+            "absorbed_ms": round(t_abs, 5), "rope_ms": round(t_rope, 5),
+            "time_ratio_rope_over_absorbed": round(t_rope / t_abs, 4),
+            "absorbed_GBps": round(bytes_ / (t_abs * 1e-3) / 1e9, 1),
+            "roofline": {"kernel": "rope_decode_kernel", "bound": "mfma", "achieved": round(tflops, 2),
+                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                         "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(k_ms, 5),
+                         "median_launch_ms": round(kt[len(kt) // 2], 5)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -322,6 +390,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0,
                     help="also time an N-layer decode step (each layer its own caches, query "
                          "and maps) eagerly and as one HIP graph replay")
+    ap.add_argument("--no-rope", action="store_true",
+                    help="skip the ordinary-RoPE contrast timing (bf16 workloads)")
     ap.add_argument("--no-gqa", action="store_true",
                     help="skip the matched-GQA comparison on workloads that carry a GQA key cache")
     args = ap.parse_args()
@@ -472,6 +542,8 @@ def main():
     if w.gqa and not args.no_gqa:
         out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches,
                                                stream)
+    if w.dtype == "bf16" and not args.no_rope and paging is None:
+        out["rope_comparison"] = rope_comparison(args, w, inp, S, split_rows, dev, caches, stream)
     if not args.no_cpu_baseline:
         rec, o_ref = cpu_baseline(w, inp, seq, pos)
         errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]

@@ -22,6 +22,9 @@
  * The matched grouped-query baseline the paper measures GVA against
  * (explicit key stream per group) has its own attention call,
  * gva_gqa_decode_attention, sharing the layout, splits and gva_combine.
+ * GVA with ordinary RoPE (keys reconstructed and rotated per position, the
+ * variant that cannot absorb M_h) has gva_rope_decode_attention, as a
+ * contrast workload.
  *
  * Conventions shared by every call
  * --------------------------------
@@ -255,6 +258,39 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
                              const void* k_cache, const void* v_cache, const int32_t* lens,
                              int32_t num_splits, int32_t split_rows, float* o_part, float* lse_part,
                              void* stream);
+
+/*
+ * gva_rope_decode_attention -- the contrast workload: GVA with ordinary
+ * RoPE instead of decoupled RoPE (Section 3.2, the variant whose key map
+ * cannot be absorbed at decode).  Content keys are reconstructed per
+ * position and rotated over their whole width d_c at their own position;
+ * there is no shared positional key.  For every (b, h, s), with L the
+ * clamped length and P = L - 1 the query's position:
+ *   rows    as in gva_decode_attention (same split rule and split_rows)
+ *   key     k_t = RoPE(v_cache[b][g(h)][t] M_h, t)       (width d_c)
+ *   score   x_t = scale * RoPE(q[b][h], P) . k_t
+ *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
+ *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)
+ * RoPE rotates interleaved pairs (2i, 2i+1) by t * rope_base^(-2i/d_c);
+ * scale = dims->scale, or 1/sqrt(d_c) when it is 0.  The kernel evaluates
+ * the scores through the equivalent per-pair form
+ *   sum_i (v_t . W_h[:, 2i]) cos(theta_i (t-P)) + (v_t . W_h[:, 2i+1]) sin(theta_i (t-P))
+ * with W_h built from q and M_h once per workgroup and rounded to bf16, so
+ * every position still costs d_v * d_c multiply-adds per head; this
+ * rounding and the fp32 cos/sin make it less exact than the absorbed path.
+ * Empty splits and S == 1 behave as in gva_decode_attention; gva_combine
+ * merges the partials.  The current token's value row must already be in
+ * the cache (gva_append_kv with d_r = 0); the caches are only read.
+ * dims->d_r must be 0 and d_c even: else GVA_ERR_INVALID_ARG.
+ * q [B][H][d_c] and M [H][d_v][d_c] in bf16; v_cache B*G streams of
+ * T rows x d_v in the tiled layout.
+ * Supported: bf16, d_v and d_c in {64, 128}, H/G in {1, 2, 4, 8} with
+ * H/G * d_v * d_c * 2 bytes <= 128 KiB; other valid shapes:
+ * GVA_ERR_UNSUPPORTED.  Pointers: 16-byte aligned (lens 4).
+ */
+int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m, const void* v_cache,
+                              const int32_t* lens, int32_t num_splits, int32_t split_rows,
+                              float* o_part, float* lse_part, void* stream);
 
 /*
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):

@@ -22,7 +22,7 @@ GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
            "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
-           "gva_pick_splits", "gva_status_string", "gva_version")
+           "gva_rope_decode_attention", "gva_pick_splits", "gva_status_string", "gva_version")
 GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
@@ -70,6 +70,7 @@ def lib() -> ctypes.CDLL:
         L.gva_decode_attention.argtypes = [D, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
         L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, I32, P, P, P]
+        L.gva_rope_decode_attention.argtypes = [D, P, P, P, P, I32, I32, P, P, P]
         PG = ctypes.POINTER(GvaPaging)
         L.gva_paged_append_kv.argtypes = [D, PG, P, P, P, P, P, P, P, I32, P]
         L.gva_paged_decode_attention.argtypes = [D, PG, P, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
@@ -80,7 +81,7 @@ def lib() -> ctypes.CDLL:
         L.gva_probe_read.argtypes = [P, ctypes.c_int64, I32, P, P]
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
                      "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
-                     "gva_pick_splits", "gva_version", "gva_probe_read"):
+                     "gva_rope_decode_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -220,6 +221,27 @@ def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_split
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
         _stream(stream))
     _check("gva_gqa_decode_attention", st)
+
+
+def gva_rope_decode_attention(dims: GvaDims, q, m, v_cache, lens, num_splits: int, o_part, lse_part,
+                              split_rows: int = 0, stream=None):
+    """GVA with ordinary RoPE (keys reconstructed and rotated per position):
+    ``q`` [B, H, d_c], ``m`` [H, d_v, d_c], dims.d_r == 0."""
+    d = dims
+    dt = d.torch_dtype
+    S = int(num_splits)
+    st = lib().gva_rope_decode_attention(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        S,
+        int(split_rows),
+        _ptr(o_part, "o_part", torch.float32, (d.batch, d.n_heads, S, d.d_v)),
+        _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
+        _stream(stream))
+    _check("gva_rope_decode_attention", st)
 
 
 def gva_paged_append_kv(dims: GvaDims, paging: GvaPaging, v_pool, kr_pool, block_table, v_new, kr_new,
@@ -419,6 +441,21 @@ def gqa_decode(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int,
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
     gva_gqa_decode_attention(dims, q, k_cache, v_cache, lens, S, bufs.o_part, bufs.lse_part,
                              split_rows=split_rows, stream=stream)
+    if S == 1:
+        return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
+    gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
+    return bufs.o, bufs.lse
+
+
+def rope_decode(dims: GvaDims, q, m, v_cache, lens, num_splits: int,
+                bufs: Optional[DecodeBuffers] = None, split_rows: int = 0,
+                stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Ordinary-RoPE GVA attention + combine for one step; returns (o, lse) fp32."""
+    S = int(num_splits)
+    if bufs is None or bufs.num_splits != S:
+        bufs = DecodeBuffers(dims, S, device=v_cache.device)
+    gva_rope_decode_attention(dims, q, m, v_cache, lens, S, bufs.o_part, bufs.lse_part,
+                              split_rows=split_rows, stream=stream)
     if S == 1:
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)

@@ -70,3 +70,12 @@ def step_bytes(lens: IntSeq, B: int, H: int, G: int, d_v: int, d_c: int, d_r: in
 def gqa_decode_bytes(lens: IntSeq, B: int, H: int, G: int, d_v: int, elem: int) -> int:
     """Algorithmic bytes of one matched-GQA decode launch (K and V streams)."""
     return _total_len(lens) * 2 * G * d_v * elem + B * H * d_v * elem
+
+
+def rope_decode_flops(total_rows: int, H: int, d_v: int, d_c: int) -> int:
+    """Algorithmic flops of one decode launch of GVA with ordinary RoPE
+    (Section 3.2: the key map is not absorbable), over ``total_rows`` cached
+    rows summed across the batch.  Per row and head: the key reconstruction
+    v_t M_h (2 d_v d_c), the rotated score (2 d_c) and the weighted value
+    sum (2 d_v).  Absorbed GVA needs only 2 d_v + 2 d_v per row and head."""
+    return int(total_rows) * H * 2 * (d_v * d_c + d_c + d_v)

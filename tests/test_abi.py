@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
     # every header under include/ is one of the two
     assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["gva.h", "gva_probe.h"]
-    assert gva.gva_version() == 10500
+    assert gva.gva_version() == 10600
 
 
 def test_status_strings():
@@ -200,6 +200,29 @@ def test_gqa_validation():
     assert gqa_status(dims(n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED   # H/G = 16
     assert gqa_status(d, stride=132) == gva.GVA_ERR_UNSUPPORTED             # 16-byte query rows
     assert gqa_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED
+
+
+def rope_status(d, q=A, m=A, v=A, lens=A, S=2, rows=0, op=A, lp=A):
+    return gva.lib().gva_rope_decode_attention(ctypes.byref(d), q, m, v, lens, S, rows, op, lp, None)
+
+
+def test_rope_decode_validation():
+    d = dims(n_heads=8, n_groups=2, d_r=0)
+    assert rope_status(dims(batch=0, d_r=0)) == gva.GVA_ERR_INVALID_ARG
+    assert rope_status(dims(d_r=16)) == gva.GVA_ERR_INVALID_ARG              # no decoupled slice
+    assert rope_status(dims(d_r=0, rope_base=0.0)) == gva.GVA_ERR_INVALID_ARG
+    assert rope_status(dims(d_r=0, d_c=63)) == gva.GVA_ERR_INVALID_ARG       # whole pairs
+    for kw in (dict(q=None), dict(m=None), dict(v=None), dict(lens=None), dict(op=None),
+               dict(lp=None), dict(q=A + 2), dict(m=A + 8), dict(v=A + 4), dict(lens=A + 2),
+               dict(S=0), dict(S=gva.GVA_MAX_SPLITS + 1), dict(rows=-32), dict(rows=40)):
+        assert rope_status(d, **kw) == gva.GVA_ERR_INVALID_ARG, kw
+    assert rope_status(dims(d_r=0, dtype="f32")) == gva.GVA_ERR_UNSUPPORTED   # bf16 only
+    assert rope_status(dims(d_r=0, d_v=96)) == gva.GVA_ERR_UNSUPPORTED
+    assert rope_status(dims(d_r=0, d_c=96)) == gva.GVA_ERR_UNSUPPORTED
+    assert rope_status(dims(d_r=0, n_heads=32, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED   # H/G = 16
+    # W of 8 heads at d_v = d_c = 128 is 256 KiB: over the LDS budget
+    assert rope_status(dims(d_r=0, n_heads=16, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED
+    assert rope_status(dims(d_r=0, t_max=40)) == gva.GVA_ERR_UNSUPPORTED
 
 
 def test_probe_validation():

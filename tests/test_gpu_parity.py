@@ -590,3 +590,100 @@ def test_paged_append_and_current_row():
         v2, k2 = gva.from_pages(vp.cpu(), kp.cpu(), bt, pg)
         assert torch.equal(gva.untiled(v2).view(itype), v_ref.view(itype))
         assert torch.equal(gva.untiled(k2).view(itype), k_ref.view(itype))
+
+
+# ------------------------------------- GVA with ordinary RoPE (contrast path)
+# W_h = rotation-paired q M_h is rounded to bf16 and the cos/sin weights are
+# fp32, so this path is less exact than the absorbed one (which keeps the
+# query as a bf16 high+low pair); its expected accuracy is pinned separately.
+# A relative rounding of up to 2^-9 on each W entry moves a base-2 logit of
+# rms ~1.4 by ~1.6e-3 rms; with one row dominating a short sequence and
+# |v| up to ~4 that is a few 1e-3 on o (observed: <= 1.9e-3).
+ROPE_QUALITY = 5e-3
+
+
+def _rope_check(o, lse, o_ref, lse_ref, label):
+    err = max_abs(o, o_ref)
+    lerr = lse_err(lse, lse_ref)
+    note(f"{label}: max|o-o_ref| = {err:.3e}  max|lse-lse_ref| = {lerr:.3e}")
+    assert err <= TOL["bf16"], (label, err)
+    assert err <= ROPE_QUALITY, (label, err)
+    assert lerr <= 1e-2, (label, lerr)
+
+
+def _rope_workload(hpg, dv, dc, T, B, G=2):
+    return gva_inputs.Workload("rope", B, T, G * hpg, G, dv, dc, 0, dtype="bf16")
+
+
+@pytest.mark.parametrize("hpg,dv,dc", [(1, 64, 64), (2, 128, 64), (4, 64, 128), (4, 128, 128),
+                                       (8, 64, 64), (8, 64, 128)])
+def test_rope_decode_matches_oracle(hpg, dv, dc):
+    w = _rope_workload(hpg, dv, dc, 304, 5)
+    lens = torch.tensor([304, 0, 1, 45, 263], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 13, lens=lens)
+    for b, L in enumerate(lens.tolist()):       # rows past a length are never read
+        inp["v"][b, :, L:] = float("nan")
+    o_ref, lse_ref = oracle.rope_decode(inp["q"], inp["m"], inp["v"], inp["lens"], rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("q", "m", "v", "lens")})
+    d = dims_of(w)
+    for S, rows in ((1, 0), (3, 0), (8, 0), (10, 32), (3, 64)):
+        note(f"rope hpg={hpg} dv={dv} dc={dc} S={S} split_rows={rows}")
+        o, lse = gva.rope_decode(d, dev["q"], dev["m"], dev["v"], dev["lens"], S, split_rows=rows)
+        torch.cuda.synchronize()
+        _rope_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"rope/hpg{hpg}/dv{dv}/dc{dc}/S{S}/rows{rows}")
+
+
+def test_rope_decode_long_positions_and_read_only_cache():
+    # positions up to 16K: the angle reduction has to hold far from zero
+    w = _rope_workload(4, 128, 128, 16384, 2, G=1)
+    lens = torch.tensor([16384, 9001], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 17, lens=lens)
+    note("rope long positions: oracle")
+    o_ref, lse_ref = oracle.rope_decode(inp["q"], inp["m"], inp["v"], inp["lens"], rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("q", "m", "v", "lens")})
+    v0 = dev["v"].clone()
+    d = dims_of(w)
+    for S in (1, 16):
+        note(f"rope long positions S={S}")
+        o, lse = gva.rope_decode(d, dev["q"], dev["m"], dev["v"], dev["lens"], S)
+        torch.cuda.synchronize()
+        _rope_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"rope long/S{S}")
+    assert torch.equal(dev["v"], v0)
+
+
+def test_rope_decode_differs_from_absorbed_gva():
+    # the same q, M and values through the absorbed (no rotation, d_r = 0)
+    # kernel give a different result: the contrast path is not the GVA path
+    w = _rope_workload(4, 64, 64, 128, 2)
+    inp = gva_inputs.make_inputs(w, 19, lens=torch.tensor([128, 77], dtype=torch.int32))
+    dev = upload({k: inp[k] for k in ("q", "m", "v", "kr", "lens")})
+    d = dims_of(w)
+    note("rope vs absorbed")
+    o_r, _ = gva.rope_decode(d, dev["q"], dev["m"], dev["v"], dev["lens"], 1)
+    o_a, _, _, _ = run_decode(w, dev, 1)
+    torch.cuda.synchronize()
+    assert max_abs(o_r.cpu(), o_a) > 1e-2
+
+
+@pytest.mark.slow
+def test_rope_decode_full_size_sampled():
+    # the bandwidth-headline shape (B32, T8192, H32, G8, d 128/128) with
+    # ordinary RoPE: every output checked for finiteness, two sequences
+    # against the oracle
+    w = gva_inputs.workload("b32_t8k").replace(name="rope_b32_t8k", d_r=0)
+    note("rope b32_t8k: drawing inputs")
+    inp = gva_inputs.make_inputs(w, 0)
+    d = dims_of(w)
+    dev = upload({k: inp[k] for k in ("q", "m", "v", "lens")})
+    note("rope b32_t8k: decode S=1")
+    o, lse = gva.rope_decode(d, dev["q"], dev["m"], dev["v"], dev["lens"], 1)
+    o, lse = o.cpu(), lse.cpu()
+    del dev
+    torch.cuda.empty_cache()
+    picks = [0, w.batch - 1]
+    sub = sub_batch(inp, picks)
+    note(f"rope b32_t8k: oracle on sequences {picks}")
+    o_ref, lse_ref = oracle.rope_decode(sub["q"], sub["m"], sub["v"], sub["lens"], rope_base=w.rope_base)
+    idx = torch.tensor(picks)
+    _rope_check(o[idx], lse[idx], o_ref, lse_ref, "rope b32_t8k/sampled")
+    assert torch.isfinite(o).all()
