@@ -62,6 +62,8 @@ def _load():
         lib.gva_oracle_rope_decode.argtypes = [I, I, I, I, I, I, P, I, P, I, P, I, P, D, D,
                                                ctypes.c_int64, I, P, P]
         lib.gva_oracle_rope_decode.restype = None
+        lib.gva_oracle_prefill.argtypes = [I, I, I, I, I, I, I, I, P, I, P, I, P, P, I, P, D, D, I, P, P]
+        lib.gva_oracle_prefill.restype = None
         lib.gva_oracle_max_threads.argtypes = []
         lib.gva_oracle_max_threads.restype = I
         _lib = lib
@@ -213,6 +215,29 @@ def rope_decode(q: torch.Tensor, m: torch.Tensor, v: torch.Tensor, lens: torch.T
     _load().gva_oracle_rope_decode(B, H, G, T, dv, dc, _ptr(qc), _code(qc), _ptr(mc), _code(mc),
                                    _ptr(vc), _code(vc), _ptr(lc), float(scale), float(rope_base),
                                    int(shift), int(n_threads), _ptr(o), _ptr(lse))
+    return o, lse
+
+
+def prefill(q: torch.Tensor, m: torch.Tensor, v: torch.Tensor, kr: torch.Tensor, lens: torch.Tensor,
+            scale: float = 0.0, rope_base: float = 10000.0, n_threads: int = 0):
+    """Causal prefill in fp64: q [B, N, H, d_c+d_r] holds the queries of each
+    sequence's last N cached rows (query i at position lens-N+i).
+    Returns o [B, N, H, d_v], lse [B, N, H]."""
+    B, N, H, W = q.shape
+    _, G, T, dv = v.shape
+    dr = kr.shape[-1]
+    dc = W - dr
+    if m.shape != (H, dv, dc) or kr.shape[:2] != (B, T) or H % G:
+        raise ValueError("inconsistent shapes")
+    qc, mc, vc, kc = _cpu(q), _cpu(m), _cpu(v), _cpu(kr)
+    if kc.dtype != vc.dtype:
+        raise ValueError("v and kr caches must share a dtype")
+    lc = _cpu(lens.to(torch.int32))
+    o = torch.empty(B, N, H, dv, dtype=torch.float64)
+    lse = torch.empty(B, N, H, dtype=torch.float64)
+    _load().gva_oracle_prefill(B, N, H, G, T, dv, dc, dr, _ptr(qc), _code(qc), _ptr(mc), _code(mc),
+                               _ptr(vc), _ptr(kc), _code(vc), _ptr(lc), float(scale), float(rope_base),
+                               int(n_threads), _ptr(o), _ptr(lse))
     return o, lse
 
 

@@ -233,6 +233,72 @@ void gva_oracle_decode(int B, int H, int G, int T_max, int d_v, int d_c, int d_r
   }
 }
 
+/* Prefill: Algorithm 1's loop run for every prompt position at once, with
+ * causal attention (training uses the same content-position split with
+ * standard causal attention, Section 3.3).  Each sequence's N query rows
+ * are the last N of its L cached rows, so query i sits at position
+ * p = L - N + i and sees rows 0..p.  For every (b, i, h) with p >= 0:
+ *   q~ = q^nope M_h^T,  q^ = RoPE(q^rope, p)
+ *   s[t] = scale * ( q~ . V[b, g(h), t, :] + q^ . kr[b, t, :] ),  t <= p
+ *   o = sum_t softmax(s)[t] V[b, g(h), t, :],  lse = log sum_t exp(s[t]);
+ * rows with p < 0 give o = 0, lse = -inf.  scale <= 0 selects
+ * 1/sqrt(d_c + d_r).  q [B][N][H][d_c+d_r], o [B][N][H][d_v], lse [B][N][H]. */
+void gva_oracle_prefill(int B, int N, int H, int G, int T_max, int d_v, int d_c, int d_r,
+                        const void* q, int dt_q, const void* m, int dt_m,
+                        const void* v_cache, const void* kr_cache, int dt_cache,
+                        const int32_t* lens, double scale, double rope_base, int n_threads,
+                        double* o, double* lse) {
+  if (scale <= 0.0) scale = 1.0 / sqrt((double)(d_c + d_r));
+  const int hpg = H / G;
+  const int64_t n_rows = (int64_t)B * N * H;
+#ifdef _OPENMP
+  if (n_threads > 0) omp_set_num_threads(n_threads);
+#pragma omp parallel for schedule(dynamic, 1)
+#endif
+  for (int64_t r = 0; r < n_rows; ++r) {
+    const int h = (int)(r % H);
+    const int i = (int)((r / H) % N);
+    const int b = (int)(r / ((int64_t)H * N));
+    const int g = h / hpg;
+    int L = lens[b];
+    if (L < 0) L = 0;
+    if (L > T_max) L = T_max;
+    const int64_t p = (int64_t)L - N + i;
+    double* out = o + r * d_v;
+    for (int k = 0; k < d_v; ++k) out[k] = 0.0;
+    if (p < 0) {
+      lse[r] = -INFINITY;
+      continue;
+    }
+    double* qa = (double*)malloc(sizeof(double) * (size_t)d_v);
+    double* qr = (double*)malloc(sizeof(double) * (size_t)(d_r > 0 ? d_r : 1));
+    double* s = (double*)malloc(sizeof(double) * (size_t)(p + 1));
+    /* q is [B*N][H][W]: row (b*N + i) */
+    absorb_one(H, d_v, d_c, d_r, q, dt_q, m, dt_m, b * N + i, h, p, rope_base, qa, qr);
+    const int64_t vbase = ((int64_t)b * G + g) * T_max;
+    for (int64_t t = 0; t <= p; ++t) {
+      double content = 0.0, positional = 0.0;
+      for (int k = 0; k < d_v; ++k) content += qa[k] * ld(v_cache, (vbase + t) * d_v + k, dt_cache);
+      for (int j = 0; j < d_r; ++j)
+        positional += qr[j] * ld(kr_cache, ((int64_t)b * T_max + t) * d_r + j, dt_cache);
+      s[t] = scale * (content + positional);
+    }
+    double mx = -INFINITY;
+    for (int64_t t = 0; t <= p; ++t) mx = s[t] > mx ? s[t] : mx;
+    double z = 0.0;
+    for (int64_t t = 0; t <= p; ++t) {
+      double w = exp(s[t] - mx);
+      z += w;
+      for (int k = 0; k < d_v; ++k) out[k] += w * ld(v_cache, (vbase + t) * d_v + k, dt_cache);
+    }
+    for (int k = 0; k < d_v; ++k) out[k] /= z;
+    lse[r] = mx + log(z);
+    free(qa);
+    free(qr);
+    free(s);
+  }
+}
+
 /* GVA without decoupled RoPE (Section 3.2: the ordinary-RoPE variants the
  * paper evaluates, which cannot absorb M_h at decode), for every (b, h):
  *   k_t = RoPE(V[b, g(h), t, :] M_h, t + shift)        (key reconstructed,

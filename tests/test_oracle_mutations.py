@@ -30,6 +30,10 @@ MUTANTS = [
      "if (scale <= 0.0) scale = 1.0 / sqrt((double)d_v);"),
     ("rope-decode transposed M", "ld(m, ((int64_t)h * d_v + i) * d_c + c, dt_m)",
      "ld(m, ((int64_t)h * d_c + c) * d_v + i, dt_m)"),
+    ("prefill query position", "b * N + i, h, p, rope_base, qa, qr);",
+     "b * N + i, h, p + 1, rope_base, qa, qr);"),
+    ("prefill query row", "b * N + i, h, p, rope_base, qa, qr);",
+     "b * N + (N - 1 - i), h, p, rope_base, qa, qr);"),
     ("last row dropped", "for (int t = 0; t < n; ++t) {\n      double w", "for (int t = 0; t < n - 1; ++t) {\n      double w"),
 ]
 
@@ -48,6 +52,8 @@ PIN_TESTS = [
     lambda o: pins.test_rope_decode_matches_explicit_construction(o, 4, 2),
     lambda o: pins.test_rope_decode_scores_are_a_relative_rotation(o),
     lambda o: pins.test_rope_decode_shift_and_edge_cases(o),
+    lambda o: pins.test_prefill_matches_masked_explicit_attention(o, 4, 2, 8),
+    lambda o: pins.test_prefill_rows_are_decode_steps(o),
 ]
 
 

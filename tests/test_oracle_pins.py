@@ -473,6 +473,67 @@ def test_rope_decode_shift_and_edge_cases(orc):
     assert (oa[0] - o[0]).abs().max() > 1e-3
 
 
+# ------------------------------------------------ prefill (causal, Sec. 3.3)
+def _prefill_inputs(seed, B=2, N=5, H=4, G=2, T=37, dv=16, dc=12, dr=8, lens=(37, 3)):
+    g = torch.Generator().manual_seed(seed)
+    q = torch.randn(B, N, H, dc + dr, generator=g, dtype=torch.float64)
+    v = torch.randn(B, G, T, dv, generator=g, dtype=torch.float64)
+    kr = torch.randn(B, T, dr, generator=g, dtype=torch.float64)
+    m = torch.randn(H, dv, dc, generator=g, dtype=torch.float64) / math.sqrt(dv)
+    return q, m, v, kr, torch.tensor(lens, dtype=torch.int32)
+
+
+@pytest.mark.parametrize("H,G,dr", [(4, 2, 8), (4, 1, 0), (6, 3, 4)])
+def test_prefill_matches_masked_explicit_attention(orc, H, G, dr):
+    # explicit keys [V M_h, kr] over every cached row, a boolean causal mask
+    # (t <= p) and textbook SDPA; rows whose position is negative are empty
+    q, m, v, kr, lens = _prefill_inputs(83 + H + dr, H=H, G=G, dr=dr)
+    B, N, _, W = q.shape
+    dc, hpg = W - dr, H // G
+    o, lse = orc.prefill(q, m, v, kr, lens)
+    for b in range(B):
+        L = int(lens[b])
+        for i in range(N):
+            p = L - N + i
+            for h in range(H):
+                if p < 0:
+                    assert torch.all(o[b, i, h] == 0) and math.isinf(float(lse[b, i, h]))
+                    continue
+                g = h // hpg
+                K = torch.cat([v[b, g, :L] @ m[h], kr[b, :L]], dim=1)
+                qr = torch.from_numpy(rope_complex(q[b, i, h, dc:].numpy(), p))
+                qf = torch.cat([q[b, i, h, :dc], qr])
+                mask = (torch.arange(L) <= p).view(1, 1, 1, L)
+                scale = 1.0 / math.sqrt(W)
+                ref = F.scaled_dot_product_attention(qf.view(1, 1, 1, -1), K.view(1, 1, L, -1),
+                                                     v[b, g, :L].reshape(1, 1, L, -1), attn_mask=mask,
+                                                     scale=scale).view(-1)
+                assert torch.allclose(o[b, i, h], ref, rtol=0, atol=1e-12)
+                lref = torch.logsumexp((K[: p + 1] @ qf) * scale, dim=0)
+                assert abs(float(lse[b, i, h]) - float(lref)) < 1e-12
+
+
+def test_prefill_rows_are_decode_steps(orc):
+    # Algorithm 1 run token by token: query i of the prompt is one decode step
+    # over the first p+1 rows
+    q, m, v, kr, lens = _prefill_inputs(89, lens=(37, 20))
+    o, lse = orc.prefill(q, m, v, kr, lens)
+    N = q.shape[1]
+    for i in range(N):
+        p = lens - N + i
+        od, ld = orc.decode(q[:, i].contiguous(), m, v, kr, p + 1)
+        assert torch.allclose(o[:, i], od, rtol=0, atol=1e-13)
+        assert torch.allclose(lse[:, i], ld, rtol=0, atol=1e-13)
+
+
+def test_prefill_first_prompt_row_is_its_value(orc):
+    # a prompt that fills the cache from row 0: its first query sees one row
+    q, m, v, kr, lens = _prefill_inputs(97, N=6, lens=(6, 6))
+    o, _ = orc.prefill(q, m, v, kr, lens)
+    for h in range(4):
+        assert torch.equal(o[:, 0, h], v[:, h // 2, 0])
+
+
 # ------------------------------------------------- figures the paper prints
 def _golden_rows(name):
     rows = []
