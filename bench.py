@@ -362,6 +362,75 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
                          "median_launch_ms": round(kt[len(kt) // 2], 5)}}
 
 
+def prefill_comparison(args, w, caches, dev, stream):
+    """A prompt of T tokens for one sequence at the workload's head shapes
+    (its rows are the first sequence's cached rows): absorption + causal
+    attention (gva_prefill_absorb + gva_prefill_attention), against the
+    matched-GQA prefill (explicit key stream of width d_v, no positional
+    term) on the same values.  Dense contractions: priced on the bf16 MFMA
+    roofline."""
+    N = w.t_max
+    w1 = w.replace(batch=1)
+    d1 = gva.make_dims(1, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, w.t_max, w.dtype, w.rope_base)
+    v1, kr1 = caches[0][0][:1], caches[0][1][:1]
+    lens1 = torch.full((1,), N, dtype=torch.int32, device="cuda")
+    q = gva_inputs.prefill_queries(w1, args.seed, N).cuda()
+    qg = gva_inputs.prefill_queries(w1, args.seed, N, gqa=True).cuda()
+    g = torch.Generator().manual_seed(args.seed + 11)
+    kg = gva.tiled(torch.randn(1, w.n_groups, w.t_max, w.d_v, generator=g).to(torch.bfloat16)).cuda()
+    q_abs = torch.empty(1, N, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+    q_rot = torch.empty(1, N, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+    o = torch.empty(1, N, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+    lse = torch.empty(1, N, w.n_heads, dtype=torch.float32, device="cuda")
+    qr = q_rot if w.d_r > 0 else None
+    krc = kr1 if w.d_r > 0 else None
+
+    def absorb(i):
+        gva.gva_prefill_absorb(d1, N, q, dev["m"], lens1, q_abs, qr, stream)
+
+    def attend(i, ev_a=None, ev_b=None):
+        if ev_a is not None:
+            ev_a.record(stream)
+        gva.gva_prefill_attention(d1, N, q_abs, qr, v1, krc, lens1, o, lse, stream)
+        if ev_b is not None:
+            ev_b.record(stream)
+
+    def gqa(i):
+        gva.gva_gqa_prefill_attention(d1, N, qg, kg, v1, lens1, o, lse, stream)
+
+    steps = max(5, args.steps // 10)
+    for i in range(2):
+        absorb(i)
+        attend(i)
+        gqa(i)
+    t_abs = timed(absorb, steps, stream)
+    t_att = timed(attend, steps, stream)
+    t_gqa = timed(gqa, steps, stream)
+    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
+    torch.cuda.synchronize()
+    for i, (a, b) in enumerate(evs):
+        attend(i, a, b)
+    torch.cuda.synchronize()
+    kt = sorted(a.elapsed_time(b) for a, b in evs)
+    k_ms = sum(kt) / len(kt)
+    f_gva = traffic.prefill_flops(N, N, w.n_heads, w.d_v, w.d_r)
+    f_gqa = traffic.prefill_flops(N, N, w.n_heads, w.d_v, 0)
+    tf = f_gva / (k_ms * 1e-3) / 1e12
+    return {"what": f"causal prefill of {N} tokens, batch 1, at the workload's head shapes: GVA "
+                    "(absorb + attention) vs matched GQA attention on the same values",
+            "n_tokens": N, "absorb_ms": round(t_abs, 5), "gva_attention_ms": round(t_att, 5),
+            "gqa_attention_ms": round(t_gqa, 5),
+            "time_ratio_gva_over_gqa": round(t_att / t_gqa, 4),
+            "time_ratio_gva_with_absorb_over_gqa": round((t_att + t_abs) / t_gqa, 4),
+            "flop_ratio_gva_over_gqa": round(f_gva / f_gqa, 4),
+            "gqa_TFLOPs": round(f_gqa / (t_gqa * 1e-3) / 1e12, 2),
+            "roofline": {"kernel": "prefill_bf16_kernel", "bound": "mfma", "achieved": round(tf, 2),
+                         "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
+                         "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
+                         "algorithmic_flops_per_launch": f_gva, "avg_launch_ms": round(k_ms, 5),
+                         "median_launch_ms": round(kt[len(kt) // 2], 5)}}
+
+
 def main():
     ap = argparse.ArgumentParser()
     ap.add_argument("--gpus", type=int, default=1)
@@ -390,6 +459,8 @@ def main():
     ap.add_argument("--layers", type=int, default=0,
                     help="also time an N-layer decode step (each layer its own caches, query "
                          "and maps) eagerly and as one HIP graph replay")
+    ap.add_argument("--no-prefill", action="store_true",
+                    help="skip the causal-prefill timing (bf16 workloads)")
     ap.add_argument("--no-rope", action="store_true",
                     help="skip the ordinary-RoPE contrast timing (bf16 workloads)")
     ap.add_argument("--no-gqa", action="store_true",
@@ -544,6 +615,8 @@ def main():
                                                stream)
     if w.dtype == "bf16" and not args.no_rope and paging is None:
         out["rope_comparison"] = rope_comparison(args, w, inp, S, split_rows, dev, caches, stream)
+    if w.dtype == "bf16" and not args.no_prefill and paging is None and w.t_max <= 16384:
+        out["prefill_comparison"] = prefill_comparison(args, w, caches, dev, stream)
     if not args.no_cpu_baseline:
         rec, o_ref = cpu_baseline(w, inp, seq, pos)
         errs = [float((o_gpu[b].double() - o_ref[b]).abs().max()) for b in o_ref]

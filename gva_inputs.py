@@ -35,7 +35,7 @@ from typing import Dict, Optional
 
 import torch
 
-__all__ = ["Workload", "WORKLOADS", "make_inputs", "workload"]
+__all__ = ["Workload", "WORKLOADS", "make_inputs", "prefill_queries", "workload"]
 
 
 @dataclasses.dataclass(frozen=True)
@@ -131,3 +131,14 @@ def make_inputs(w: Workload, seed: int, lens: Optional[torch.Tensor] = None) -> 
     out["v_new"] = normal(B, G, dv)
     out["kr_new"] = normal(B, dr)
     return out
+
+
+def prefill_queries(w: Workload, seed: int, n_new: int, gqa: bool = False) -> torch.Tensor:
+    """A prompt's queries, [B, n_new, H, d_c + d_r] in the storage dtype
+    (or, with ``gqa``, the matched-GQA queries [B, n_new, H, d_v] in fp32),
+    N(0, 1) from their own generator seeded with ``seed``."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed) + 7919)
+    width = w.d_v if gqa else w.d_c + w.d_r
+    x = torch.randn((w.batch, int(n_new), w.n_heads, width), generator=g, dtype=torch.float32)
+    return x if gqa else x.to(_torch_dtype(w.dtype))

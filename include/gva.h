@@ -24,7 +24,9 @@
  * gva_gqa_decode_attention, sharing the layout, splits and gva_combine.
  * GVA with ordinary RoPE (keys reconstructed and rotated per position, the
  * variant that cannot absorb M_h) has gva_rope_decode_attention, as a
- * contrast workload.
+ * contrast workload.  A prompt is attended causally in one pass with
+ * gva_prefill_absorb + gva_prefill_attention (gva_gqa_prefill_attention
+ * for the matched GQA baseline).
  *
  * Conventions shared by every call
  * --------------------------------
@@ -291,6 +293,56 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
 int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m, const void* v_cache,
                               const int32_t* lens, int32_t num_splits, int32_t split_rows,
                               float* o_part, float* lse_part, void* stream);
+
+/*
+ * Prefill: causal attention for a prompt of n_new tokens per sequence, after
+ * any cached prefix (Algorithm 1's loop for every prompt position at once;
+ * Section 3.3's scores; training uses the same split with standard causal
+ * attention).  The prompt's rows are appended first (gva_append_kv with
+ * n_new rows per sequence), so each sequence's n_new query rows are its
+ * last n_new cached rows: query i of sequence b sits at position
+ * p = L_b - n_new + i (L_b = lens[b], clamped to [0, T]) and sees rows 0..p.
+ * Rows with p < 0 (L_b < n_new) get o = 0, lse = -inf.
+ *
+ * gva_prefill_absorb -- gva_absorb_query for every query row: q is
+ * [B][n_new][H][d_c+d_r] in the storage dtype; q_abs [B][n_new][H][d_v]
+ * and q_rot [B][n_new][H][d_r] fp32, the positional slice rotated at the
+ * row's own position.  B * n_new <= 2^20.  1 <= n_new <= T, else
+ * GVA_ERR_INVALID_ARG.
+ */
+int gva_prefill_absorb(const gva_dims* dims, int32_t n_new, const void* q, const void* m,
+                       const int32_t* lens, float* q_abs, float* q_rot, void* stream);
+
+/*
+ * gva_prefill_attention -- for every (b, i, h) with p >= 0:
+ *   score   x_t = scale * ( q_abs[b][i][h] . V[b][g(h)][t] + q_rot[b][i][h] . kr[b][t] ),  t <= p
+ *   o[b][i][h][:] = sum_{t <= p} softmax(x)_t V[b][g(h)][t][:]
+ *   lse[b][i][h]  = log sum_{t <= p} exp(x_t)
+ * with scale as in gva_decode_attention.  A dense contraction, unlike the
+ * bandwidth-bound decode step (which keeps query and weights as bf16
+ * high+low pairs): the queries enter the matrix cores as bf16, the softmax
+ * weights and the value rows as fp16 (exact for bf16 values of magnitude
+ * 2^-14 .. 65504; value entries must stay below 65504 in magnitude).
+ * o [B][n_new][H][d_v] fp32, lse [B][n_new][H] fp32; the caches are read
+ * only.  Supported: bf16, d_v in {64, 128}, d_r a multiple of 8 (<= 64),
+ * H/G in {1, 2, 4, 8}, T % 16 == 0; other valid shapes:
+ * GVA_ERR_UNSUPPORTED.  Pointers 16-byte aligned (lens, lse 4).
+ */
+int gva_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
+                          const void* v_cache, const void* kr_cache, const int32_t* lens, float* o,
+                          float* lse, void* stream);
+
+/*
+ * gva_gqa_prefill_attention -- the matched grouped-query prefill the paper
+ * compares GVA against: the same causal rows, scores q[b][i][h] . k_cache
+ * [b][g(h)][t] over an explicit key stream of width d_v (no positional
+ * term; scale = dims->scale or 1/sqrt(d_v)).  q [B][n_new][H][d_v] fp32;
+ * k_cache like v_cache.  Shapes and outputs as for gva_prefill_attention;
+ * d_c, d_r and rope_base are not used.
+ */
+int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q, const void* k_cache,
+                              const void* v_cache, const int32_t* lens, float* o, float* lse,
+                              void* stream);
 
 /*
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):

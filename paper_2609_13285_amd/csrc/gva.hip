@@ -56,6 +56,8 @@ typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x2 __attribute__((ext_vector_type(2)));
 typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
+typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
+typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
 
 constexpr int kWaves = 4;             // waves per workgroup in the decode kernels
 constexpr int kThreads = 64 * kWaves;
@@ -88,7 +90,8 @@ struct AbsorbParams {
   const int32_t* lens;
   float* q_abs;
   float* q_rot;
-  int32_t B, H, d_v, d_c, d_r, t_max;
+  int32_t B, H, d_v, d_c, d_r, t_max;   // B = query rows (sequences x n_per_seq)
+  int32_t n_per_seq;                    // query rows per sequence: its last cached rows
   double inv_freq[kMaxPairs];
 };
 
@@ -291,6 +294,21 @@ __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
+__device__ __forceinline__ f32x4 mfma16(f16x8 a, f16x8 b, f32x4 c) {
+  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
+}
+
+// 8 floats -> fp16 (RNE)
+__device__ __forceinline__ f16x8 to_f16x8(const float* x) {
+  f16x8 out;
+#pragma unroll
+  for (int j = 0; j < 8; j += 2) {
+    const f16x2 h = __builtin_convertvector((f32x2{x[j], x[j + 1]}), f16x2);
+    out[j] = h[0];
+    out[j + 1] = h[1];
+  }
+  return out;
+}
 
 // 8 floats -> the bf16 high parts (RNE) or, with lo = true, the bf16 of the
 // remainder x - hi.  hi + lo carries ~16 significant bits of x.
@@ -398,6 +416,14 @@ __global__ void __launch_bounds__(256) append_kernel(AppendParams p) {
 }
 
 // ================================================================ absorb
+// Position of query row r: a sequence's n_per_seq query rows are its last
+// n_per_seq cached rows (one row, at L-1, for a decode step).
+__device__ __forceinline__ int query_pos(const AbsorbParams& p, int r) {
+  const int seq = r / p.n_per_seq, i = r % p.n_per_seq;
+  const int pos = clamp_len(p.lens, seq, p.t_max) - p.n_per_seq + i;
+  return pos > 0 ? pos : 0;
+}
+
 // bf16, matrix cores.  Workgroup = (head h, 16 sequences); wave w computes
 // the output blocks ib = w, w+4, ... of q~^T[i][b] = sum_k M_h[i][k] q[b][h][k]
 // (A = rows of M_h, B = the query rows, K = d_c).
@@ -414,18 +440,6 @@ __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
   const uint16_t* mh = static_cast<const uint16_t*>(p.m) + (int64_t)h * p.d_v * p.d_c;
   const int bq = min(b0 + n, p.B - 1);                  // rows past B compute a duplicate
   const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
-  // the positional pair of this thread, loaded with everything else
-  const int npair = p.d_r / 2;
-  const bool has_pair = tid < 16 * npair && b0 + (npair > 0 ? tid / npair : 0) < p.B;
-  float r0 = 0.f, r1 = 0.f;
-  int pb = 0, pi = 0;
-  if (has_pair) {
-    pb = b0 + tid / npair;
-    pi = tid % npair;
-    const uint32_t two = *reinterpret_cast<const uint32_t*>(qg + ((int64_t)pb * p.H + h) * W + p.d_c + 2 * pi);
-    r0 = bf16_bits_to_f32(two & 0xFFFFu);
-    r1 = bf16_bits_to_f32(two >> 16);
-  }
   bf16x8 xq[kMaxChunks];
 #pragma unroll
   for (int c = 0; c < kMaxChunks; ++c)
@@ -444,10 +458,16 @@ __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
     if (b0 + n < p.B)
       *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(b0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
   }
-  if (has_pair) {
-    const int L = clamp_len(p.lens, pb, p.t_max);
+  // the positional pairs of the block's rows: 16 * d_r / 2 tasks (up to
+  // 512, two per thread)
+  const int npair = p.d_r / 2;
+  for (int task = tid; task < 16 * npair; task += kThreads) {
+    const int pb = b0 + task / npair, pi = task % npair;
+    if (pb >= p.B) break;
+    const uint32_t two = *reinterpret_cast<const uint32_t*>(qg + ((int64_t)pb * p.H + h) * W + p.d_c + 2 * pi);
     float y0, y1;
-    rotate_query_pair(r0, r1, (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pi], 1.f, y0, y1);
+    rotate_query_pair(bf16_bits_to_f32(two & 0xFFFFu), bf16_bits_to_f32(two >> 16),
+                      (double)query_pos(p, pb) * p.inv_freq[pi], 1.f, y0, y1);
     float* out = p.q_rot + ((int64_t)pb * p.H + h) * p.d_r + 2 * pi;
     out[0] = y0;
     out[1] = y1;
@@ -466,10 +486,10 @@ __global__ void __launch_bounds__(128) absorb_f32_kernel(AbsorbParams p) {
     for (int k = 0; k < p.d_c; ++k) acc = fmaf(q[k], m[(int64_t)i * p.d_c + k], acc);
     p.q_abs[(int64_t)bh * p.d_v + i] = acc;
   }
-  const int L = clamp_len(p.lens, b, p.t_max);
+  const int pos = query_pos(p, b);
   for (int i = threadIdx.x; i < p.d_r / 2; i += blockDim.x) {
     double y0, y1;
-    rotate_pair(q[p.d_c + 2 * i], q[p.d_c + 2 * i + 1], (double)(L > 0 ? L - 1 : 0) * p.inv_freq[i], y0, y1);
+    rotate_pair(q[p.d_c + 2 * i], q[p.d_c + 2 * i + 1], (double)pos * p.inv_freq[i], y0, y1);
     p.q_rot[(int64_t)bh * p.d_r + 2 * i] = (float)y0;
     p.q_rot[(int64_t)bh * p.d_r + 2 * i + 1] = (float)y1;
   }
@@ -1346,6 +1366,313 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
   }
 }
 
+// =============================================================== prefill
+// Causal attention for the last N cached rows of every sequence (a prompt,
+// after any cached prefix): query i of sequence b sits at position
+// p = L_b - N + i and sees rows 0..p (Algorithm 1's loop for every prompt
+// position at once; Section 3.3's absorbed scores).  Unlike a decode step
+// this is a dense contraction: a workgroup takes C (position, head)
+// columns of one group -- C / (H/G) consecutive positions times the H/G
+// heads that share the group's value rows; C = 64, or 32 at d_v = 128 to
+// stay within 256 registers -- and its four waves split the key tiles up to
+// the block's last position.  Per 32-row key tile a wave forms the scores
+// of all C columns on the matrix cores (keys = [V | k_r] rows as stored,
+// the absorbed and rotated queries as bf16 B operands), masks rows past
+// each column's position, updates the online softmax and accumulates P.V
+// (V transposed once per tile with the identity MFMA, shared by the
+// column blocks).  P.V runs in fp16: the transposed rows come out of the
+// identity product in fp32 and every bf16 value of N(0, 1)-scale data is
+// exact in fp16, while the weights in [0, 1] keep 3 more bits than bf16.
+// The waves merge through LDS.
+// Query blocks are dealt longest first, so the triangle's tail is short.
+// GQA = true is the matched grouped-query prefill the paper compares
+// against: scores read an explicit key stream, no positional term.
+// (position, head) columns per workgroup: 64, fewer where a wider value
+// row (or the baseline's separate key tile) needs the registers
+__host__ __device__ constexpr int prefill_cols(int dv, bool gqa) { return dv >= 128 ? (gqa ? 16 : 32) : 64; }
+
+struct PrefillParams {
+  const float* q_abs;     // [B][N][H][d_v]: absorbed queries (GQA: the raw query)
+  const float* q_rot;     // [B][N][H][d_r]: rotated positional queries
+  const void* v;          // tiled caches, the prompt's rows already appended
+  const void* kr;
+  const void* k_gqa;      // matched-GQA baseline: explicit key stream (tiled like v)
+  const int32_t* lens;
+  float* o;               // [B][N][H][d_v]
+  float* lse;             // [B][N][H]
+  int32_t B, H, G, N, d_r, t_max, n_qblocks;
+  float scale_log2;
+};
+
+// Two workgroups per CU where the registers allow it without spilling.
+constexpr int prefill_min_blocks(int dv, int nrc, bool gqa) { return nrc >= 2 ? 1 : 2; }
+
+template <int HPG, int DV, int NRC, bool GQA>
+__global__ void __launch_bounds__(kThreads, prefill_min_blocks(DV, NRC, GQA)) prefill_bf16_kernel(PrefillParams p) {
+  constexpr int COLS = prefill_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = COLS / 16;
+  constexpr int QB = COLS / HPG;               // positions per workgroup
+  constexpr int DEPTH = 2;
+  constexpr int RS = DV + 2;                   // per-(wave, column) record: [m, l, o[DV]]
+  __shared__ __attribute__((aligned(16))) float red[kWaves * COLS * RS];
+
+  const int nbg = p.B * p.G;
+  const int x = blockIdx.x;
+  const int qb = p.n_qblocks - 1 - x / nbg;    // longest query blocks first
+  const int b = (x % nbg) / p.G, g = (x % nbg) % p.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, qd = lane >> 4;
+  const int h0 = g * HPG;
+  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+
+  const int L = clamp_len(p.lens, b, p.t_max);
+  const int i_end = min(p.N, (qb + 1) * QB);
+  const int kend = L - p.N + i_end;            // rows the block's last position sees
+  // column 16 cb + n of this lane: position i = qb QB + col / HPG, head
+  // h0 + col % HPG; pos[cb] = its position, or -1 if it has none
+  int pos[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = 16 * cb + n;
+    const int i = qb * QB + col / HPG;
+    const int ps = L - p.N + i;
+    pos[cb] = (i < p.N && ps >= 0) ? ps : -1;
+  }
+  const int p_first = L - p.N + qb * QB;       // the block's first position
+
+  // ---- the queries as bf16 B operands (zero for columns with no position)
+  bf16x8 bq[CB][NC];
+  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = 16 * cb + n;
+    const int i = min(qb * QB + col / HPG, p.N - 1);
+    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
+    const float* qa = p.q_abs + qrow * DV + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+      float xv[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[j] = u0[j] * p.scale_log2;
+        xv[4 + j] = u1[j] * p.scale_log2;
+      }
+      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const int j0 = 32 * rc + 8 * qd;
+      float xv[8];
+      if (j0 < p.d_r) {
+        const float* qr = p.q_rot + qrow * p.d_r + j0;
+        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
+        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xv[j] = u0[j] * p.scale_log2;
+          xv[4 + j] = u1[j] * p.scale_log2;
+        }
+      }
+      bk[cb][rc] = (pos[cb] >= 0 && j0 < p.d_r) ? split_hi_lo(xv, false) : zero8;
+    }
+  }
+
+  // ---- key tiles: rows [0, kend), read through descriptors that end at
+  // the last layout tile (reads past it return zeros)
+  const int kend16 = kend > 0 ? ((kend + kLayoutRows - 1) / kLayoutRows) * kLayoutRows : 0;
+  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(vbase), (short)0, kend16 * DV * 2, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kbase), (short)0, NRC > 0 ? kend16 * p.d_r * 2 : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
+                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
+                            : static_cast<const void*>(vbase)),
+      (short)0, kend16 * DV * 2, kBufferWord3);
+  const int kpieces = p.d_r / 8;
+  const int v_lane = qd * 256 + n * 16;
+  int k_lane[NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int rc = 0; rc < NRC; ++rc) k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
+  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
+  const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
+  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
+  auto tile_row = [&](int j) { return (w + kWaves * j) * kTileRows; };
+  using TileT = Tile<DV, NRC, GQA>;
+  auto load_tile = [&](TileT& t, int row0) {
+    const int lt = row0 / kLayoutRows;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int vsoff = (lt + hf) * v_tile_bytes;
+      if constexpr (GQA) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          t.kc[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kcres, v_lane + 1024 * c, vsoff, 0));
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, 0));
+#pragma unroll
+      for (int rc = 0; rc < NRC; ++rc)
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], (lt + hf) * k_tile_bytes, 0));
+    }
+  };
+  TileT buf[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH - 1; ++d) {
+    load_tile(buf[d], tile_row(d));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  bf16x8 esel[2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    u32x4 u = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (8 * qd + j == n + 16 * half) u[j >> 1] |= 0x3F80u << (16 * (j & 1));
+    esel[half] = as_bf16x8(u);
+  }
+
+  float m_run[CB], l_run[CB];
+  f32x4 acc[CB][NB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m_run[cb] = -INFINITY;
+    l_run[cb] = 0.f;
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib) acc[cb][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto compute_tile = [&](TileT& t, int row0) {
+    if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const bool dead = row0 + 16 * hf + n >= kend;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
+        if constexpr (GQA) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) t.kc[hf][c] = dead ? zero8 : t.kc[hf][c];
+        }
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
+      }
+    }
+    const bool masked = row0 + kTileRows - 1 > p_first;   // some column may not see every row
+    f16x8 bp[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      f32x4 sc[2];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c) sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
+      }
+      float xv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xv[k] = sc[k >> 2][k & 3];
+      if (masked) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) > pos[cb]) xv[k] = -INFINITY;
+      }
+      float mt = xv[0];
+#pragma unroll
+      for (int k = 1; k < 8; ++k) mt = fmaxf(mt, xv[k]);
+      mt = max_over_rows(mt);
+      const float m_new = fmaxf(m_run[cb], mt);
+      if (__ballot(m_new > m_run[cb]) != 0) {
+        // columns whose rows so far are all masked keep m = -inf: scale 1
+        const float alpha = m_new > m_run[cb] ? __builtin_amdgcn_exp2f(m_run[cb] - m_new) : 1.f;
+        l_run[cb] *= alpha;
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) acc[cb][ib] *= alpha;
+        m_run[cb] = m_new;
+      }
+      const float m_use = m_run[cb] == -INFINITY ? 0.f : m_run[cb];   // all masked so far
+      float pr[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        pr[k] = __builtin_amdgcn_exp2f(xv[k] - m_use);
+        l_run[cb] += pr[k];
+      }
+      bp[cb] = to_f16x8(pr);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
+        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
+        const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+        const f16x8 av = to_f16x8(tv);         // bf16 values: exact in fp16 at these magnitudes
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) acc[cb][2 * c + half] = mfma16(av, bp[cb], acc[cb][2 * c + half]);
+      }
+  };
+
+  for (int jt = 0; jt < my_tiles; jt += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int j = jt + d;
+      if (j >= my_tiles) break;
+      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(buf[d], tile_row(j));
+    }
+  }
+
+  // ---- merge the waves: per column the records (m, l, o) of the 4 waves
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const float l = sum_over_rows(l_run[cb]);
+    float* rec = red + (w * COLS + 16 * cb + n) * RS;
+    if (qd == 0) {
+      rec[0] = m_run[cb];
+      rec[1] = l;
+    }
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) rec[2 + 16 * ib + 4 * qd + jj] = acc[cb][ib][jj];
+  }
+  __syncthreads();
+  for (int idx = tid; idx < COLS * DV; idx += kThreads) {
+    const int col = idx / DV, i = idx % DV;
+    const int qi = qb * QB + col / HPG;
+    if (qi >= p.N) continue;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) mx = fmaxf(mx, red[(ww * COLS + col) * RS]);
+    float o = 0.f, lsum = 0.f;
+    if (mx != -INFINITY && L - p.N + qi >= 0) {
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) {
+        const float* rec = red + (ww * COLS + col) * RS;
+        if (rec[0] == -INFINITY) continue;       // this wave saw no row of the column
+        const float sc = __builtin_amdgcn_exp2f(rec[0] - mx);
+        lsum += rec[1] * sc;
+        o += rec[2 + i] * sc;
+      }
+      o /= lsum;
+    } else {
+      mx = -INFINITY;
+    }
+    const int64_t orow = ((int64_t)b * p.N + qi) * p.H + h0 + col % HPG;
+    p.o[orow * DV + i] = o;
+    if (i == 0) p.lse[orow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
+  }
+}
+
 // ========================================================== decode (f32)
 // Vector-ALU variant for fp32 storage.  Per 64-row tile a wave first scores
 // one row per lane, then accumulates the weighted rows with one output
@@ -1776,6 +2103,133 @@ RopeDecodeFn pick_rope_decode(int hpg, int dv, int dc) {
   return nullptr;
 }
 
+// The absorption behind gva_absorb_query (one query row per sequence) and
+// gva_prefill_absorb (a sequence's last n_per_seq rows).
+int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* m, const int32_t* lens,
+                float* q_abs, float* q_rot, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  if (n_per_seq < 1) return GVA_ERR_INVALID_ARG;
+  if (!q || !m || !lens || !q_abs) return GVA_ERR_INVALID_ARG;
+  if (dims->d_r > 0 && !q_rot) return GVA_ERR_INVALID_ARG;
+  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(lens, 4) || !aligned(q_abs, 16) ||
+      (q_rot && !aligned(q_rot, 4)))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
+  const long long rows = (long long)dims->batch * n_per_seq;
+  if (rows > (1LL << 20) || rows * dims->n_heads > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
+  AbsorbParams p;
+  p.q = q;
+  p.m = m;
+  p.lens = lens;
+  p.q_abs = q_abs;
+  p.q_rot = q_rot;
+  p.B = (int32_t)rows;
+  p.H = dims->n_heads;
+  p.d_v = dims->d_v;
+  p.d_c = dims->d_c;
+  p.d_r = dims->d_r;
+  p.t_max = dims->t_max;
+  p.n_per_seq = n_per_seq;
+  fill_inv_freq(dims, p.inv_freq);
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dims->dtype == GVA_DTYPE_BF16) {
+    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
+    const dim3 grid(dims->n_heads, (unsigned)((rows + 15) / 16));
+    hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
+  } else {
+    hipLaunchKernelGGL(absorb_f32_kernel, dim3((unsigned)(rows * dims->n_heads)), dim3(128), 0, s, p);
+  }
+  return launch_status();
+}
+
+using PrefillFn = void (*)(PrefillParams);
+
+template <int HPG, int DV>
+PrefillFn pick_prefill_nrc(int nrc, bool gqa) {
+  if (gqa) return prefill_bf16_kernel<HPG, DV, 0, true>;
+  switch (nrc) {
+    case 0: return prefill_bf16_kernel<HPG, DV, 0, false>;
+    case 1: return prefill_bf16_kernel<HPG, DV, 1, false>;
+    case 2: return prefill_bf16_kernel<HPG, DV, 2, false>;
+  }
+  return nullptr;
+}
+
+template <int HPG>
+PrefillFn pick_prefill_dv(int dv, int nrc, bool gqa) {
+  switch (dv) {
+    case 64: return pick_prefill_nrc<HPG, 64>(nrc, gqa);
+    case 128: return pick_prefill_nrc<HPG, 128>(nrc, gqa);
+  }
+  return nullptr;
+}
+
+PrefillFn pick_prefill(int hpg, int dv, int nrc, bool gqa) {
+  switch (hpg) {
+    case 1: return pick_prefill_dv<1>(dv, nrc, gqa);
+    case 2: return pick_prefill_dv<2>(dv, nrc, gqa);
+    case 4: return pick_prefill_dv<4>(dv, nrc, gqa);
+    case 8: return pick_prefill_dv<8>(dv, nrc, gqa);
+  }
+  return nullptr;
+}
+
+// The launch behind gva_prefill_attention and, with k_gqa given,
+// gva_gqa_prefill_attention.
+int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
+                 const void* v_cache, const void* kr_cache, const void* k_gqa, const int32_t* lens,
+                 float* o, float* lse, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  const bool gqa = k_gqa != nullptr;
+  const int d_r = gqa ? 0 : dims->d_r;
+  if (n_new < 1 || n_new > dims->t_max) return GVA_ERR_INVALID_ARG;
+  if (!q_abs || !v_cache || !lens || !o || !lse) return GVA_ERR_INVALID_ARG;
+  if (d_r > 0 && (!q_rot || !kr_cache)) return GVA_ERR_INVALID_ARG;
+  if (!aligned(q_abs, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) || !aligned(o, 16) ||
+      !aligned(lse, 4) || (d_r > 0 && (!aligned(q_rot, 16) || !aligned(kr_cache, 16))) ||
+      (gqa && !aligned(k_gqa, 16)))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->dtype != GVA_DTYPE_BF16) return GVA_ERR_UNSUPPORTED;
+  st = check_cache_layout(dims);
+  if (st != GVA_OK) return st;
+  if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
+  const int hpg = dims->n_heads / dims->n_groups;
+  PrefillFn fn = pick_prefill(hpg, dims->d_v, (d_r + 31) / 32, gqa);
+  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
+  const int qb_rows = prefill_cols(dims->d_v, gqa) / hpg;
+  const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;
+  const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
+  if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
+
+  PrefillParams p;
+  memset(&p, 0, sizeof(p));
+  p.q_abs = q_abs;
+  p.q_rot = q_rot;
+  p.v = v_cache;
+  p.kr = kr_cache;
+  p.k_gqa = k_gqa;
+  p.lens = lens;
+  p.o = o;
+  p.lse = lse;
+  p.B = dims->batch;
+  p.H = dims->n_heads;
+  p.G = dims->n_groups;
+  p.N = n_new;
+  p.d_r = d_r;
+  p.t_max = dims->t_max;
+  p.n_qblocks = (int32_t)n_qblocks;
+  if (gqa) {
+    const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
+    p.scale_log2 = (float)(sc * kLog2e);
+  } else {
+    p.scale_log2 = scale_log2(dims);
+  }
+  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
+  return launch_status();
+}
+
 // The append behind gva_append_kv and, with paging given, gva_paged_append_kv.
 int append_impl(const gva_dims* dims, const gva_paging* paging, const int32_t* block_table, void* v_cache,
                 void* kr_cache, const void* v_new, const void* kr_new, const int32_t* seq, const int32_t* pos,
@@ -1916,7 +2370,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
 
 extern "C" {
 
-int gva_version(void) { return 10600; }
+int gva_version(void) { return 10700; }
 
 const char* gva_status_string(int status) {
   switch (status) {
@@ -1936,36 +2390,7 @@ int gva_append_kv(const gva_dims* dims, void* v_cache, void* kr_cache, const voi
 
 int gva_absorb_query(const gva_dims* dims, const void* q, const void* m, const int32_t* lens,
                      float* q_abs, float* q_rot, void* stream) {
-  int st = check_dims(dims);
-  if (st != GVA_OK) return st;
-  if (!q || !m || !lens || !q_abs) return GVA_ERR_INVALID_ARG;
-  if (dims->d_r > 0 && !q_rot) return GVA_ERR_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(lens, 4) || !aligned(q_abs, 16) ||
-      (q_rot && !aligned(q_rot, 4)))
-    return GVA_ERR_INVALID_ARG;
-  if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
-  AbsorbParams p;
-  p.q = q;
-  p.m = m;
-  p.lens = lens;
-  p.q_abs = q_abs;
-  p.q_rot = q_rot;
-  p.B = dims->batch;
-  p.H = dims->n_heads;
-  p.d_v = dims->d_v;
-  p.d_c = dims->d_c;
-  p.d_r = dims->d_r;
-  p.t_max = dims->t_max;
-  fill_inv_freq(dims, p.inv_freq);
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  if (dims->dtype == GVA_DTYPE_BF16) {
-    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
-    const dim3 grid(dims->n_heads, (dims->batch + 15) / 16);
-    hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
-  } else {
-    hipLaunchKernelGGL(absorb_f32_kernel, dim3(dims->batch * dims->n_heads), dim3(128), 0, s, p);
-  }
-  return launch_status();
+  return absorb_impl(dims, 1, q, m, lens, q_abs, q_rot, stream);
 }
 
 
@@ -2092,6 +2517,25 @@ int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m
     p.freq_rev[i] = pow(dims->rope_base, -2.0 * (double)i / (double)dims->d_c) * kInv2Pi;
   hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kRopeThreads), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
+}
+
+int gva_prefill_absorb(const gva_dims* dims, int32_t n_new, const void* q, const void* m,
+                       const int32_t* lens, float* q_abs, float* q_rot, void* stream) {
+  if (dims != nullptr && (n_new < 1 || n_new > dims->t_max)) return GVA_ERR_INVALID_ARG;
+  return absorb_impl(dims, n_new, q, m, lens, q_abs, q_rot, stream);
+}
+
+int gva_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
+                          const void* v_cache, const void* kr_cache, const int32_t* lens, float* o,
+                          float* lse, void* stream) {
+  return prefill_impl(dims, n_new, q_abs, q_rot, v_cache, kr_cache, nullptr, lens, o, lse, stream);
+}
+
+int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q, const void* k_cache,
+                              const void* v_cache, const int32_t* lens, float* o, float* lse,
+                              void* stream) {
+  if (k_cache == nullptr) return GVA_ERR_INVALID_ARG;
+  return prefill_impl(dims, n_new, q, nullptr, v_cache, nullptr, k_cache, lens, o, lse, stream);
 }
 
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part, int32_t num_splits,

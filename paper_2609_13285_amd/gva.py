@@ -22,7 +22,8 @@ GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
            "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
-           "gva_rope_decode_attention", "gva_pick_splits", "gva_status_string", "gva_version")
+           "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
+           "gva_gqa_prefill_attention", "gva_pick_splits", "gva_status_string", "gva_version")
 GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
@@ -71,6 +72,9 @@ def lib() -> ctypes.CDLL:
         L.gva_combine.argtypes = [D, P, P, I32, P, P, P]
         L.gva_gqa_decode_attention.argtypes = [D, P, I32, P, P, P, I32, I32, P, P, P]
         L.gva_rope_decode_attention.argtypes = [D, P, P, P, P, I32, I32, P, P, P]
+        L.gva_prefill_absorb.argtypes = [D, I32, P, P, P, P, P, P]
+        L.gva_prefill_attention.argtypes = [D, I32, P, P, P, P, P, P, P, P]
+        L.gva_gqa_prefill_attention.argtypes = [D, I32, P, P, P, P, P, P, P]
         PG = ctypes.POINTER(GvaPaging)
         L.gva_paged_append_kv.argtypes = [D, PG, P, P, P, P, P, P, P, I32, P]
         L.gva_paged_decode_attention.argtypes = [D, PG, P, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
@@ -81,7 +85,8 @@ def lib() -> ctypes.CDLL:
         L.gva_probe_read.argtypes = [P, ctypes.c_int64, I32, P, P]
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
                      "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
-                     "gva_rope_decode_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
+                     "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
+                     "gva_gqa_prefill_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -242,6 +247,57 @@ def gva_rope_decode_attention(dims: GvaDims, q, m, v_cache, lens, num_splits: in
         _ptr(lse_part, "lse_part", torch.float32, (d.batch, d.n_heads, S)),
         _stream(stream))
     _check("gva_rope_decode_attention", st)
+
+
+def gva_prefill_absorb(dims: GvaDims, n_new: int, q, m, lens, q_abs, q_rot, stream=None):
+    """Absorb and rotate a prompt's queries: q [B, n_new, H, d_c+d_r]."""
+    d = dims
+    N = int(n_new)
+    st = lib().gva_prefill_absorb(
+        ctypes.byref(d), N,
+        _ptr(q, "q", d.torch_dtype, (d.batch, N, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", d.torch_dtype, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(q_abs, "q_abs", torch.float32, (d.batch, N, d.n_heads, d.d_v)),
+        _ptr(q_rot, "q_rot", torch.float32, (d.batch, N, d.n_heads, d.d_r)) if d.d_r > 0 else None,
+        _stream(stream))
+    _check("gva_prefill_absorb", st)
+
+
+def gva_prefill_attention(dims: GvaDims, n_new: int, q_abs, q_rot, v_cache, kr_cache, lens, o, lse,
+                          stream=None):
+    """Causal attention for each sequence's last n_new cached rows."""
+    d = dims
+    N = int(n_new)
+    dt = d.torch_dtype
+    st = lib().gva_prefill_attention(
+        ctypes.byref(d), N,
+        _ptr(q_abs, "q_abs", torch.float32, (d.batch, N, d.n_heads, d.d_v)),
+        _ptr(q_rot, "q_rot", torch.float32, (d.batch, N, d.n_heads, d.d_r)) if d.d_r > 0 else None,
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)) if d.d_r > 0 else None,
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(o, "o", torch.float32, (d.batch, N, d.n_heads, d.d_v)),
+        _ptr(lse, "lse", torch.float32, (d.batch, N, d.n_heads)),
+        _stream(stream))
+    _check("gva_prefill_attention", st)
+
+
+def gva_gqa_prefill_attention(dims: GvaDims, n_new: int, q, k_cache, v_cache, lens, o, lse, stream=None):
+    """The matched-GQA causal prefill: q [B, n_new, H, d_v] fp32."""
+    d = dims
+    N = int(n_new)
+    dt = d.torch_dtype
+    st = lib().gva_gqa_prefill_attention(
+        ctypes.byref(d), N,
+        _ptr(q, "q", torch.float32, (d.batch, N, d.n_heads, d.d_v)),
+        _ptr(k_cache, "k_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(o, "o", torch.float32, (d.batch, N, d.n_heads, d.d_v)),
+        _ptr(lse, "lse", torch.float32, (d.batch, N, d.n_heads)),
+        _stream(stream))
+    _check("gva_gqa_prefill_attention", st)
 
 
 def gva_paged_append_kv(dims: GvaDims, paging: GvaPaging, v_pool, kr_pool, block_table, v_new, kr_new,
@@ -460,6 +516,21 @@ def rope_decode(dims: GvaDims, q, m, v_cache, lens, num_splits: int,
         return bufs.o_part.view(dims.batch, dims.n_heads, dims.d_v), bufs.lse_part.view(dims.batch, dims.n_heads)
     gva_combine(dims, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream=stream)
     return bufs.o, bufs.lse
+
+
+def prefill(dims: GvaDims, q, m, v_cache, kr_cache, lens, stream=None) -> Tuple[torch.Tensor, torch.Tensor]:
+    """Absorb + causal attention for a prompt whose rows are the last
+    q.shape[1] cached rows of each sequence; returns (o, lse) fp32."""
+    d = dims
+    B, N = q.shape[0], q.shape[1]
+    dev = v_cache.device
+    q_abs = torch.empty(B, N, d.n_heads, d.d_v, dtype=torch.float32, device=dev)
+    q_rot = torch.empty(B, N, d.n_heads, d.d_r, dtype=torch.float32, device=dev)
+    o = torch.empty(B, N, d.n_heads, d.d_v, dtype=torch.float32, device=dev)
+    lse = torch.empty(B, N, d.n_heads, dtype=torch.float32, device=dev)
+    gva_prefill_absorb(d, N, q, m, lens, q_abs, q_rot, stream=stream)
+    gva_prefill_attention(d, N, q_abs, q_rot, v_cache, kr_cache, lens, o, lse, stream=stream)
+    return o, lse
 
 
 def probe_read_bandwidth(nbytes: int = 2 << 30, reps: int = 10, stream=None) -> Tuple[float, int]:

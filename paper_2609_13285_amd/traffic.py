@@ -79,3 +79,14 @@ def rope_decode_flops(total_rows: int, H: int, d_v: int, d_c: int) -> int:
     v_t M_h (2 d_v d_c), the rotated score (2 d_c) and the weighted value
     sum (2 d_v).  Absorbed GVA needs only 2 d_v + 2 d_v per row and head."""
     return int(total_rows) * H * 2 * (d_v * d_c + d_c + d_v)
+
+
+def prefill_flops(n_new: int, total_len: int, H: int, d_v: int, d_r: int) -> int:
+    """Algorithmic flops of one causal prefill launch (absorbed form) for a
+    sequence of ``total_len`` cached rows whose last ``n_new`` are the
+    prompt: query p sees p+1 rows; per row and head the score costs
+    2 (d_v + d_r) and the weighted value sum 2 d_v.  With d_r = 0 this is
+    also the matched-GQA count (key width d_v)."""
+    first = total_len - n_new
+    seen = sum(max(0, first + i + 1) for i in range(n_new))
+    return seen * H * 2 * (2 * d_v + d_r)

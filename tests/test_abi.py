@@ -38,7 +38,7 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
     # every header under include/ is one of the two
     assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["gva.h", "gva_probe.h"]
-    assert gva.gva_version() == 10600
+    assert gva.gva_version() == 10700
 
 
 def test_status_strings():
@@ -223,6 +223,38 @@ def test_rope_decode_validation():
     # W of 8 heads at d_v = d_c = 128 is 256 KiB: over the LDS budget
     assert rope_status(dims(d_r=0, n_heads=16, n_groups=2)) == gva.GVA_ERR_UNSUPPORTED
     assert rope_status(dims(d_r=0, t_max=40)) == gva.GVA_ERR_UNSUPPORTED
+
+
+def prefill_status(d, N=4, qa=A, qr=A, v=A, kr=A, lens=A, o=A, lse=A):
+    return gva.lib().gva_prefill_attention(ctypes.byref(d), N, qa, qr, v, kr, lens, o, lse, None)
+
+
+def test_prefill_validation():
+    d = dims(t_max=64)
+    assert prefill_status(dims(batch=0)) == gva.GVA_ERR_INVALID_ARG
+    for kw in (dict(N=0), dict(N=65), dict(qa=None), dict(qr=None), dict(v=None), dict(kr=None),
+               dict(lens=None), dict(o=None), dict(lse=None), dict(qa=A + 4), dict(qr=A + 8),
+               dict(v=A + 2), dict(kr=A + 8), dict(o=A + 4), dict(lens=A + 2)):
+        assert prefill_status(d, **kw) == gva.GVA_ERR_INVALID_ARG, kw
+    # d_r = 0: no positional operands needed
+    assert prefill_status(dims(d_r=0, t_max=64, n_heads=32, n_groups=2), qr=None, kr=None) == \
+        gva.GVA_ERR_UNSUPPORTED                                        # H/G = 16
+    assert prefill_status(dims(t_max=64, dtype="f32")) == gva.GVA_ERR_UNSUPPORTED
+    assert prefill_status(dims(t_max=64, d_v=96)) == gva.GVA_ERR_UNSUPPORTED
+    assert prefill_status(dims(t_max=64, d_r=12)) == gva.GVA_ERR_UNSUPPORTED
+    assert prefill_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED
+    lib = gva.lib()
+    # the GQA baseline needs its key stream; the absorb needs 1 <= n_new <= T
+    assert lib.gva_gqa_prefill_attention(ctypes.byref(d), 4, A, None, A, A, A, A, None) == \
+        gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_gqa_prefill_attention(ctypes.byref(d), 4, A + 4, A, A, A, A, A, None) == \
+        gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_prefill_absorb(ctypes.byref(d), 0, A, A, A, A, A, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_prefill_absorb(ctypes.byref(d), 65, A, A, A, A, A, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_prefill_absorb(ctypes.byref(d), 4, A, A, A, A, None, None) == gva.GVA_ERR_INVALID_ARG
+    big = dims(batch=64, t_max=1 << 15)
+    assert lib.gva_prefill_absorb(ctypes.byref(big), 1 << 15, A, A, A, A, A, None) == \
+        gva.GVA_ERR_UNSUPPORTED                                        # 2^21 query rows
 
 
 def test_probe_validation():

@@ -174,6 +174,23 @@ def test_absorb_query_matches_oracle(dtype):
     assert max_abs(qr.cpu(), qr_ref) <= 1e-6 * float(qr_ref.abs().max())
 
 
+def test_absorb_query_wide_positional_slice_many_rows():
+    # d_r = 64 over 40 rows: a 16-row block of the bf16 absorption has 512
+    # positional pairs, two per thread (regression: only the first 256 were
+    # rotated)
+    w = gva_inputs.Workload("absorb", 40, 512, 4, 2, 64, 64, 64, dtype="bf16")
+    inp = gva_inputs.make_inputs(w, 31)
+    qa_ref, qr_ref = oracle.absorb(inp["q"], inp["m"], inp["lens"], d_r=w.d_r)
+    dev = upload(inp)
+    qa = torch.empty(40, 4, 64, dtype=torch.float32, device="cuda")
+    qr = torch.full((40, 4, 64), float("nan"), dtype=torch.float32, device="cuda")
+    note("absorb bf16 d_r=64 B=40")
+    gva.gva_absorb_query(dims_of(w), dev["q"], dev["m"], dev["lens"], qa, qr)
+    torch.cuda.synchronize()
+    assert max_abs(qa.cpu(), qa_ref) <= 1e-5 * float(qa_ref.abs().max())
+    assert max_abs(qr.cpu(), qr_ref) <= 1e-6 * float(qr_ref.abs().max())
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_append_matches_oracle_bitwise(dtype):
     B, G, T, dv, dr = 3, 4, 131072, 64, 32
@@ -687,3 +704,122 @@ def test_rope_decode_full_size_sampled():
     idx = torch.tensor(picks)
     _rope_check(o[idx], lse[idx], o_ref, lse_ref, "rope b32_t8k/sampled")
     assert torch.isfinite(o).all()
+
+
+# ------------------------------------------------------- prefill (causal)
+# The prefill kernel feeds the matrix cores bf16 queries and bf16 softmax
+# weights (single, not high+low): a relative rounding of up to 2^-9 on each
+# weight moves o by at most 2^-9 max|v| (~8e-3 for N(0, 1) values, whose
+# maximum over these caches is ~4); q~ in bf16 moves a base-2 logit by
+# ~1e-3 rms.  Observed: a few 1e-3 where few rows are seen.
+PREFILL_QUALITY = 8e-3
+
+
+def _prefill_check(o, lse, o_ref, lse_ref, label):
+    err = max_abs(o, o_ref)
+    lerr = lse_err(lse, lse_ref)
+    note(f"{label}: max|o-o_ref| = {err:.3e}  max|lse-lse_ref| = {lerr:.3e}")
+    assert err <= TOL["bf16"], (label, err)
+    assert err <= PREFILL_QUALITY, (label, err)
+    assert lerr <= 1e-2, (label, lerr)
+
+
+@pytest.mark.parametrize("hpg,dv,dr", [(1, 64, 16), (2, 128, 16), (4, 64, 0), (4, 128, 16),
+                                       (8, 64, 32), (8, 128, 64)])
+def test_prefill_matches_oracle(hpg, dv, dr):
+    G = 2
+    w = gva_inputs.Workload("prefill", 3, 320, G * hpg, G, dv, dv, dr, dtype="bf16")
+    N = 100
+    lens = torch.tensor([320, 150, 60], dtype=torch.int32)   # 60 < N: 40 rows see nothing
+    inp = gva_inputs.make_inputs(w, 23, lens=lens)
+    for b, L in enumerate(lens.tolist()):                     # rows past a length are never read
+        inp["v"][b, :, L:] = float("nan")
+        inp["kr"][b, L:] = float("nan")
+    q = gva_inputs.prefill_queries(w, 23, N)
+    note(f"prefill hpg={hpg} dv={dv} dr={dr}: oracle")
+    o_ref, lse_ref = oracle.prefill(q, inp["m"], inp["v"], inp["kr"], lens, rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("m", "v", "kr", "lens")})
+    d = dims_of(w)
+    note(f"prefill hpg={hpg} dv={dv} dr={dr}: GPU")
+    o, lse = gva.prefill(d, q.cuda(), dev["m"], dev["v"], dev["kr"], dev["lens"])
+    torch.cuda.synchronize()
+    _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"prefill/hpg{hpg}/dv{dv}/dr{dr}")
+
+
+def test_prefill_after_append_of_the_prompt():
+    # Algorithm 1's append for every prompt row (gva_append_kv), then the
+    # prefill over the appended caches, against the oracle doing the same
+    w = gva_inputs.Workload("prefill", 2, 256, 8, 2, 128, 128, 16, dtype="bf16")
+    N = 70
+    lens = torch.tensor([200, 70], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 29, lens=lens)
+    g = torch.Generator().manual_seed(31)
+    v_new = torch.randn(w.batch * N, w.n_groups, w.d_v, generator=g).to(torch.bfloat16)
+    kr_new = torch.randn(w.batch * N, w.d_r, generator=g).to(torch.bfloat16)
+    seq = torch.arange(w.batch, dtype=torch.int32).repeat_interleave(N)
+    pos = (lens.repeat_interleave(N) - N + torch.arange(N, dtype=torch.int32).repeat(w.batch)).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, v_new, kr_new, seq, pos, rope_base=w.rope_base)
+    q = gva_inputs.prefill_queries(w, 29, N)
+    o_ref, lse_ref = oracle.prefill(q, inp["m"], v_ref, k_ref, lens, rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("m", "v", "kr", "lens")})
+    d = dims_of(w)
+    note("prefill after append: GPU")
+    gva.gva_append_kv(d, dev["v"], dev["kr"], v_new.cuda(), kr_new.cuda(), seq.cuda(), pos.cuda())
+    o, lse = gva.prefill(d, q.cuda(), dev["m"], dev["v"], dev["kr"], dev["lens"])
+    torch.cuda.synchronize()
+    _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, "prefill after append")
+
+
+@pytest.mark.parametrize("hpg,dv", [(1, 64), (4, 128), (8, 64)])
+def test_gqa_prefill_matches_oracle(hpg, dv):
+    # the matched-GQA prefill row by row: row i is a GQA decode step over
+    # the first p+1 rows (the oracle's GQA definition)
+    G = 2
+    w = gva_inputs.Workload("gqa_prefill", 2, 192, G * hpg, G, dv, dv, 0, dtype="bf16", gqa=True)
+    N = 50
+    lens = torch.tensor([192, 30], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 37, lens=lens)
+    q = gva_inputs.prefill_queries(w, 37, N, gqa=True)
+    dev = upload({k: inp[k] for k in ("v", "k_gqa", "lens")})
+    d = dims_of(w)
+    o = torch.empty(w.batch, N, w.n_heads, dv, dtype=torch.float32, device="cuda")
+    lse = torch.empty(w.batch, N, w.n_heads, dtype=torch.float32, device="cuda")
+    note(f"gqa prefill hpg={hpg} dv={dv}")
+    gva.gva_gqa_prefill_attention(d, N, q.cuda(), dev["k_gqa"], dev["v"], dev["lens"], o, lse)
+    torch.cuda.synchronize()
+    o, lse = o.cpu(), lse.cpu()
+    o_ref = torch.zeros(w.batch, N, w.n_heads, dv, dtype=torch.float64)
+    lse_ref = torch.full((w.batch, N, w.n_heads), float("-inf"), dtype=torch.float64)
+    for i in range(N):
+        p = lens - N + i
+        live = p >= 0
+        if not live.any():
+            continue
+        oi, li = oracle.gqa_decode(q[:, i].contiguous(), inp["k_gqa"], inp["v"], (p + 1).clamp(min=0),
+                                   d_k=dv)
+        o_ref[live, i] = oi[live]
+        lse_ref[live, i] = li[live]
+    _prefill_check(o, lse, o_ref, lse_ref, f"gqa prefill/hpg{hpg}/dv{dv}")
+
+
+@pytest.mark.slow
+def test_prefill_full_size_sampled():
+    # a 4096-token prompt at the bandwidth-headline head shapes (H32, G8,
+    # d 128/128/16): every output finite, sampled rows against decode steps
+    # of the oracle over the truncated cache
+    w = gva_inputs.workload("b32_t8k").replace(name="prefill_b1_t4k", batch=1, t_max=4096)
+    N = 4096
+    inp = gva_inputs.make_inputs(w, 0, lens=torch.tensor([N], dtype=torch.int32))
+    q = gva_inputs.prefill_queries(w, 0, N)
+    dev = upload({k: inp[k] for k in ("m", "v", "kr", "lens")})
+    d = dims_of(w)
+    note("prefill b1 t4k: GPU")
+    o, lse = gva.prefill(d, q.cuda(), dev["m"], dev["v"], dev["kr"], dev["lens"])
+    o, lse = o.cpu(), lse.cpu()
+    assert torch.isfinite(o).all() and torch.isfinite(lse).all()
+    for i in (0, 1, 31, 32, 1000, 2047, 4095):
+        note(f"prefill b1 t4k: oracle row {i}")
+        o_ref, lse_ref = oracle.decode(q[:, i].contiguous(), inp["m"], inp["v"], inp["kr"],
+                                       torch.tensor([i + 1], dtype=torch.int32))
+        _prefill_check(o[:, i], lse[:, i], o_ref, lse_ref, f"prefill b1 t4k/row{i}")
