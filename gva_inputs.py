@@ -69,6 +69,9 @@ WORKLOADS: Dict[str, Workload] = {
     "gva350m_b8_t2k": Workload("gva350m_b8_t2k", 8, 2048, 16, 4, 64, 64, 16),
     # Bandwidth headline: B32, T8192, H32, G8, d 128/128/16, bf16.
     "b32_t8k": Workload("b32_t8k", 32, 8192, 32, 8, 128, 128, 16),
+    # The paper's wider positional slice (d_r = 24) at the bandwidth-headline
+    # shape: B32, T8192, H32, G8, d 128/128/24, bf16.
+    "b32_t8k_dr24": Workload("b32_t8k_dr24", 32, 8192, 32, 8, 128, 128, 24),
     # Long context: B4, T<=131072 (lengths U[T/2, T]), H32, G8, d 128/128/32.
     "long_b4_t128k": Workload("long_b4_t128k", 4, 131072, 32, 8, 128, 128, 32,
                               lengths="uniform_half"),

@@ -92,6 +92,7 @@ struct AbsorbParams {
   float* q_rot;
   int32_t B, H, d_v, d_c, d_r, t_max;   // B = query rows (sequences x n_per_seq)
   int32_t n_per_seq;                    // query rows per sequence: its last cached rows
+  int32_t row_blocks;                   // bf16 kernel: 16-row blocks per workgroup (1..4)
   double inv_freq[kMaxPairs];
 };
 
@@ -430,7 +431,8 @@ __device__ __forceinline__ int query_pos(const AbsorbParams& p, int r) {
 __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
   constexpr int kMaxChunks = 16;                          // d_c <= 512
   const int h = blockIdx.x;
-  const int b0 = blockIdx.y * 16;
+  const int RB = p.row_blocks;                            // M_h rows reused for RB row blocks
+  const int b0 = blockIdx.y * 16 * RB;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, qd = lane >> 4;
@@ -438,30 +440,33 @@ __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
   const int nck = p.d_c / 32;
   const uint16_t* qg = static_cast<const uint16_t*>(p.q);
   const uint16_t* mh = static_cast<const uint16_t*>(p.m) + (int64_t)h * p.d_v * p.d_c;
-  const int bq = min(b0 + n, p.B - 1);                  // rows past B compute a duplicate
-  const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
-  bf16x8 xq[kMaxChunks];
-#pragma unroll
-  for (int c = 0; c < kMaxChunks; ++c)
-    if (c < nck) xq[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
   const int nb = p.d_v / 16;
   for (int ib = w; ib < nb; ib += kWaves) {
     bf16x8 a[kMaxChunks];
 #pragma unroll
     for (int c = 0; c < kMaxChunks; ++c)
       if (c < nck) a[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
-    f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+    for (int rb = 0; rb < RB; ++rb) {
+      const int r0 = b0 + 16 * rb;
+      if (r0 >= p.B) break;
+      const int bq = min(r0 + n, p.B - 1);                // rows past B compute a duplicate
+      const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
+      bf16x8 xq[kMaxChunks];
 #pragma unroll
-    for (int c = 0; c < kMaxChunks; ++c)
-      if (c < nck) acc = mfma16(a[c], xq[c], acc);
-    // lane (n, qd) holds q~[b0 + n][16 ib + 4 qd + jj]
-    if (b0 + n < p.B)
-      *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(b0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
+      for (int c = 0; c < kMaxChunks; ++c)
+        if (c < nck) xq[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
+      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < kMaxChunks; ++c)
+        if (c < nck) acc = mfma16(a[c], xq[c], acc);
+      // lane (n, qd) holds q~[r0 + n][16 ib + 4 qd + jj]
+      if (r0 + n < p.B)
+        *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(r0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
+    }
   }
-  // the positional pairs of the block's rows: 16 * d_r / 2 tasks (up to
-  // 512, two per thread)
+  // the positional pairs of the workgroup's rows: 16 RB d_r / 2 tasks
   const int npair = p.d_r / 2;
-  for (int task = tid; task < 16 * npair; task += kThreads) {
+  for (int task = tid; task < 16 * RB * npair; task += kThreads) {
     const int pb = b0 + task / npair, pi = task % npair;
     if (pb >= p.B) break;
     const uint32_t two = *reinterpret_cast<const uint32_t*>(qg + ((int64_t)pb * p.H + h) * W + p.d_c + 2 * pi);
@@ -2131,11 +2136,15 @@ int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* 
   p.d_r = dims->d_r;
   p.t_max = dims->t_max;
   p.n_per_seq = n_per_seq;
+  // many rows (a prompt): each workgroup reuses M_h over 64 rows, which cuts
+  // the re-reads of M_h fourfold; a decode batch keeps 16 rows per workgroup
+  p.row_blocks = rows >= 4096 ? 4 : 1;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
   if (dims->dtype == GVA_DTYPE_BF16) {
     if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
-    const dim3 grid(dims->n_heads, (unsigned)((rows + 15) / 16));
+    const long long rows_per_wg = 16LL * p.row_blocks;
+    const dim3 grid(dims->n_heads, (unsigned)((rows + rows_per_wg - 1) / rows_per_wg));
     hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
   } else {
     hipLaunchKernelGGL(absorb_f32_kernel, dim3((unsigned)(rows * dims->n_heads)), dim3(128), 0, s, p);

@@ -267,7 +267,7 @@ def test_full_step_append_then_decode():
 
 # ----------------------------------------------- full-size workloads, sampled
 @pytest.mark.slow
-@pytest.mark.parametrize("name", ["b32_t8k", "long_b4_t128k", "ragged_b64"])
+@pytest.mark.parametrize("name", ["b32_t8k", "b32_t8k_dr24", "long_b4_t128k", "ragged_b64"])
 def test_full_size_sampled(name):
     w = gva_inputs.workload(name)
     note(f"{name}: drawing inputs")
@@ -722,6 +722,27 @@ def _prefill_check(o, lse, o_ref, lse_ref, label):
     assert err <= TOL["bf16"], (label, err)
     assert err <= PREFILL_QUALITY, (label, err)
     assert lerr <= 1e-2, (label, lerr)
+
+
+@pytest.mark.parametrize("B,N,dr", [(3, 90, 16), (3, 1500, 64)])
+def test_prefill_absorb_matches_oracle(B, N, dr):
+    # every prompt row absorbed and rotated at its own position L-N+i
+    # (4500 rows: the 64-rows-per-workgroup form with a ragged last block)
+    w = gva_inputs.Workload("prefill", B, 2048, 8, 2, 128, 96, dr, dtype="bf16")
+    lens = torch.tensor([2048, 1600, N], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 41, lens=lens)
+    q = gva_inputs.prefill_queries(w, 41, N)
+    pos1 = (lens.view(B, 1) - N + torch.arange(N, dtype=torch.int32).view(1, N) + 1).reshape(-1)
+    qa_ref, qr_ref = oracle.absorb(q.reshape(B * N, w.n_heads, -1), inp["m"], pos1.to(torch.int32), d_r=dr)
+    d = dims_of(w)
+    qa = torch.empty(B, N, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+    qr = torch.full((B, N, w.n_heads, dr), float("nan"), dtype=torch.float32, device="cuda")
+    note(f"prefill absorb B={B} N={N} dr={dr}")
+    gva.gva_prefill_absorb(d, N, q.cuda(), inp["m"].cuda(), lens.cuda(), qa, qr)
+    torch.cuda.synchronize()
+    qa, qr = qa.cpu().reshape(B * N, w.n_heads, -1), qr.cpu().reshape(B * N, w.n_heads, -1)
+    assert max_abs(qa, qa_ref) <= 1e-5 * float(qa_ref.abs().max())
+    assert max_abs(qr, qr_ref) <= 1e-6 * float(qr_ref.abs().max())
 
 
 @pytest.mark.parametrize("hpg,dv,dr", [(1, 64, 16), (2, 128, 16), (4, 64, 0), (4, 128, 16),
