@@ -292,6 +292,34 @@ __device__ __forceinline__ float mirror(float x) {
 
 __device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
 
+// dot product of eight bf16 pairs (two 16-byte pieces), fp32 accumulation.
+// The pairs are taken with shufflevector: a bit_cast of one 32-bit element
+// of the u32x4 compiled to four uses of element 0.
+__device__ __forceinline__ float dot8_bf16(u32x4 x, u32x4 y) {
+  const bf16x8 xv = as_bf16x8(x), yv = as_bf16x8(y);
+  float acc = 0.f;
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 0, 1), __builtin_shufflevector(yv, yv, 0, 1),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 2, 3), __builtin_shufflevector(yv, yv, 2, 3),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 4, 5), __builtin_shufflevector(yv, yv, 4, 5),
+                                        acc, false);
+  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 6, 7), __builtin_shufflevector(yv, yv, 6, 7),
+                                        acc, false);
+  return acc;
+}
+
+template <int CTRL>
+__device__ __forceinline__ float dpp_add(float x) {
+  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
+}
+
+// sum over each aligned group of 16 lanes, every lane of the group receiving
+// it: quad_perm [1,0,3,2], quad_perm [3,2,1,0], row_half_mirror, row_mirror
+__device__ __forceinline__ float sum16(float x) {
+  return dpp_add<0x140>(dpp_add<0x141>(dpp_add<0x1B>(dpp_add<0xB1>(x))));
+}
+
 __device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
   return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
 }
@@ -508,9 +536,9 @@ struct DecodeCfg {
   static constexpr int NC = DV / 32;                         // K-chunks per V row
   static constexpr int NB = DV / 16;                         // 16-wide i-blocks of the output
   static constexpr int DEPTH = DV >= 128 ? 2 : 3;
-  // d_c chunks per absorption round: one round of 32 loads where the
-  // registers allow it (no spills), else rounds of 16
-  static constexpr int CR = ((DV >= 128 && NRC < 2 && HPG <= 4) ? 32 : 16) / NB;
+  // fused absorption: 16-byte pieces of M_h per lane and load round, one
+  // round of 32 where the registers allow it (no spills), else rounds of 16
+  static constexpr int AR = (DV >= 128 && NRC < 2 && HPG <= 4) ? 32 : 16;
   static constexpr int QS_STRIDE = DV + 4;                   // padded LDS rows (floats)
   static constexpr int QR_STRIDE = 32 * NRC + 4;
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
@@ -540,7 +568,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   request_args<FUSED || GQA>(a);
   using Cfg = DecodeCfg<HPG, DV, NRC>;
   using TileT = Tile<DV, NRC, GQA>;
-  constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, CR = Cfg::CR;
+  constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, AR = Cfg::AR;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
   int b, s, g;
@@ -590,11 +618,14 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   // (kept as loaded bits: converting them here would wait for them here)
   u32x4 pend_piece = {0u, 0u, 0u, 0u};
   uint32_t pend_kbits = 0u;
+  double kfreq = 0.0;                          // the pair's RoPE frequency (kernel arguments)
   if (!GQA && a.v_new != nullptr) {
     if (tid < DV / 8)
       pend_piece = *(reinterpret_cast<const u32x4*>(static_cast<const uint16_t*>(a.v_new) + ((int64_t)b * a.G + g) * DV) + tid);
-    if (tid < a.d_r / 2)
+    if (tid < a.d_r / 2) {
       pend_kbits = *reinterpret_cast<const uint32_t*>(static_cast<const uint16_t*>(a.kr_new) + (int64_t)b * a.d_r + 2 * tid);
+      kfreq = p.inv_freq[tid];
+    }
   }
   // The query: raw bf16 (GQA baseline); pre-absorbed fp32 (q_abs, q_rot);
   // or, fused, the raw positional pair and the first round of q / M_h
@@ -602,26 +633,36 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   u32x4 xqg[GQA ? NC : 1];
   f32x4 xa[GQA ? 1 : NC][2];
   f32x4 xr[NRC > 0 ? NRC : 1][2];
-  bf16x8 am[CR][NB];
-  bf16x8 xqf[CR];
   const int W = a.d_c + a.d_r;
-  const int nck = a.d_c / 32;
+  // Fused absorption, q~[i] = sum_k q[k] M_h[i][k]: M_h is read in whole
+  // rows, 16 lanes of 16 bytes per row and 4 rows per load, so each load
+  // covers whole cache lines (the MFMA operand order, 64 bytes of 16 rows
+  // per load, took four times as long to arrive).  Each lane forms an
+  // 8-term bf16 dot product with its piece of q, and a DPP sum over the
+  // row's 16 lanes finishes the row.  Columns come in segments of 128, rows
+  // in blocks of 4 AR: one load round per (segment, row block).  Loads are
+  // unconditional, from clamped addresses (selecting a loaded value would
+  // wait for it and for every load before it); pieces past d_c meet a
+  // zeroed query piece.
+  constexpr int ARB = DV / 4 / AR;             // row blocks per segment
+  u32x4 am[FUSED ? AR : 1];
+  u32x4 xqf = {0u, 0u, 0u, 0u};                // the query piece of the lane's columns
+  const int nrounds = ((a.d_c + 127) / 128) * ARB;
+  const int a_row = lane >> 4, a_col = 8 * (lane & 15);
   const int npair = a.d_r / 2;
-  const bool has_pair = FUSED && tid < HPG * npair;
-  const int pair_h = npair > 0 ? tid / npair : 0, pair_i = npair > 0 ? tid % npair : 0;
+  const int ptid = kThreads - 1 - tid;
+  const bool has_pair = FUSED && ptid < HPG * npair;
+  const int pair_h = npair > 0 ? ptid / npair : 0, pair_i = npair > 0 ? ptid % npair : 0;
   uint32_t rq_bits = 0u;                       // the raw positional pair (bf16 x 2)
-  auto load_round = [&](int hl, int c0) {      // q chunks and M_h rows of one absorption round
+  double qfreq = 0.0;
+  auto load_round = [&](int hl, int ro) {      // the query piece and M_h pieces of one round
     const int h = h0 + hl;
+    const int col = min((ro / ARB) * 128 + a_col, a.d_c - 8), rb = ro % ARB;
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + h) * W;
-    const uint16_t* mh = static_cast<const uint16_t*>(a.m) + (int64_t)h * DV * a.d_c;
+    const uint16_t* mh = static_cast<const uint16_t*>(a.m) + ((int64_t)h * DV + rb * AR * 4 + a_row) * a.d_c + col;
+    xqf = *reinterpret_cast<const u32x4*>(qrow + col);
 #pragma unroll
-    for (int cr = 0; cr < CR; ++cr) {
-      const int c = min(c0 + cr, nck - 1);
-      xqf[cr] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
-#pragma unroll
-      for (int ib = 0; ib < NB; ++ib)
-        am[cr][ib] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * a.d_c + 32 * c + 8 * qd));
-    }
+    for (int r = 0; r < AR; ++r) am[r] = *reinterpret_cast<const u32x4*>(mh + (int64_t)(4 * r) * a.d_c);
   };
   if constexpr (GQA) {
     const uint16_t* qrow = static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + hq) * a.q_stride + 8 * qd;
@@ -642,9 +683,11 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       xr[rc][1] = *reinterpret_cast<const f32x4*>(qr + 4);
     }
   } else {
-    if (has_pair)
+    if (has_pair) {
       rq_bits = *reinterpret_cast<const uint32_t*>(
           static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + h0 + pair_h) * W + a.d_c + 2 * pair_i);
+      qfreq = p.inv_freq[pair_i];
+    }
     if (w < HPG) load_round(w, 0);
   }
   __builtin_amdgcn_sched_barrier(0);
@@ -775,7 +818,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       if (tid < a.d_r / 2) {
         double y0, y1;
         rotate_pair(bf16_bits_to_f32(pend_kbits & 0xFFFFu), bf16_bits_to_f32(pend_kbits >> 16),
-                    (double)(L - 1) * p.inv_freq[tid], y0, y1);
+                    (double)(L - 1) * kfreq, y0, y1);
         y0b = f64_to_bf16_rne(y0);
         y1b = f64_to_bf16_rne(y1);
         if (g == 0) {
@@ -828,29 +871,38 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       bk[rc] = (active && in_range) ? split_hi_lo(x, is_lo) : zero8;
     }
   } else {
-    // Fused absorption: q~_h = q^nope_h M_h^T on the matrix cores, wave w
-    // taking heads w, w+4, ...; A = rows i of M_h (K = d_c), B = the query
-    // chunk broadcast to all 16 columns.  The first round was loaded above.
+    // Fused absorption, wave w taking heads w, w+4, ...: each round's rows
+    // are finished by a sum over their lanes and stored (first segment) or
+    // added (later segments) by the row's first lane, pre-scaled.  The first
+    // round was loaded above.
     float* qs = lds;                                  // [HPG][QS_STRIDE]
     float* qrs = lds + HPG * Cfg::QS_STRIDE;          // [HPG][QR_STRIDE]
-    for (int hl = w; hl < HPG; hl += kWaves) {
-      f32x4 acc[NB];
+    auto absorb_round = [&](int hl, int ro) {
+      const int rb = ro % ARB;
+      const u32x4 qv = (ro / ARB) * 128 + a_col < a.d_c ? xqf : u32x4{0u, 0u, 0u, 0u};
+      float v[AR];
 #pragma unroll
-      for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
-      for (int c0 = 0; c0 < nck; c0 += CR) {
-        if (hl != w || c0 != 0) load_round(hl, c0);
+      for (int r = 0; r < AR; ++r) v[r] = dot8_bf16(am[r], qv);
 #pragma unroll
-        for (int cr = 0; cr < CR; ++cr)
-          if (c0 + cr < nck)
+      for (int r = 0; r < AR; ++r) v[r] = sum16(v[r]) * a.scale_log2;
+      // every lane of a row's 16 writes the same value
+      float* dst = qs + hl * Cfg::QS_STRIDE + rb * AR * 4 + a_row;
+      if (ro < ARB) {
 #pragma unroll
-            for (int ib = 0; ib < NB; ++ib) acc[ib] = mfma16(am[cr][ib], xqf[cr], acc[ib]);
+        for (int r = 0; r < AR; ++r) dst[4 * r] = v[r];
+      } else {
+#pragma unroll
+        for (int r = 0; r < AR; ++r) dst[4 * r] += v[r];
       }
-      if (n == 0) {
-#pragma unroll
-        for (int ib = 0; ib < NB; ++ib)
-          *reinterpret_cast<f32x4*>(qs + hl * Cfg::QS_STRIDE + 16 * ib + 4 * qd) = acc[ib] * a.scale_log2;
+    };
+    // the first round (loaded before the tiles) in straight-line code, so
+    // its waits count only its own loads; then the rest
+    if (w < HPG) absorb_round(w, 0);
+    for (int hl = w; hl < HPG; hl += kWaves)
+      for (int ro = hl == w ? 1 : 0; ro < nrounds; ++ro) {
+        load_round(hl, ro);
+        absorb_round(hl, ro);
       }
-    }
     stage_current_row();
     // rotate the positional query at position L-1 (fp64 angle, reduced
     // exactly, fp32 rotation); the padding past d_r is written as zeros in
@@ -858,7 +910,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     if (has_pair) {
       float y0, y1;
       rotate_query_pair(bf16_bits_to_f32(rq_bits & 0xFFFFu), bf16_bits_to_f32(rq_bits >> 16),
-                        (double)(L > 0 ? L - 1 : 0) * p.inv_freq[pair_i], a.scale_log2, y0, y1);
+                        (double)(L > 0 ? L - 1 : 0) * qfreq, a.scale_log2, y0, y1);
       qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i] = y0;
       qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = y1;
     }
