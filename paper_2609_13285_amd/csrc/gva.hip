@@ -453,11 +453,20 @@ __device__ __forceinline__ int query_pos(const AbsorbParams& p, int r) {
   return pos > 0 ? pos : 0;
 }
 
-// bf16, matrix cores.  Workgroup = (head h, 16 sequences); wave w computes
-// the output blocks ib = w, w+4, ... of q~^T[i][b] = sum_k M_h[i][k] q[b][h][k]
-// (A = rows of M_h, B = the query rows, K = d_c).
+// bf16, matrix cores.  Workgroup = (head h, 16 RB query rows); wave w
+// computes the output blocks ib = w, w+4, ... of
+// q~^T[i][r] = sum_k M_h[i][k] q[r][h][k] (A = rows of M_h, B = the query
+// rows, K = d_c).  M_h is staged through LDS in passes of 128 rows x 128
+// columns: the workgroup reads each pass as whole rows (16 threads x 16 B
+// per row, so every load covers whole cache lines; the MFMA operand order,
+// 64 bytes of 16 rows per load, took four times as long to arrive), and the
+// waves take their A operands from LDS (rows padded by 16 bytes: the 16
+// rows of an operand fall in distinct banks).
+constexpr int kAbsorbRows = 128, kAbsorbCols = 128, kAbsorbStride = kAbsorbCols + 8;
+constexpr int kAbsorbMaxRB = 4;
+
 __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
-  constexpr int kMaxChunks = 16;                          // d_c <= 512
+  __shared__ __attribute__((aligned(16))) uint16_t ms[kAbsorbRows * kAbsorbStride];
   const int h = blockIdx.x;
   const int RB = p.row_blocks;                            // M_h rows reused for RB row blocks
   const int b0 = blockIdx.y * 16 * RB;
@@ -468,28 +477,71 @@ __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
   const int nck = p.d_c / 32;
   const uint16_t* qg = static_cast<const uint16_t*>(p.q);
   const uint16_t* mh = static_cast<const uint16_t*>(p.m) + (int64_t)h * p.d_v * p.d_c;
-  const int nb = p.d_v / 16;
-  for (int ib = w; ib < nb; ib += kWaves) {
-    bf16x8 a[kMaxChunks];
+  const int nseg = (p.d_c + kAbsorbCols - 1) / kAbsorbCols;
+  constexpr int kFill = kAbsorbRows * kAbsorbCols / 8 / kThreads;   // 16-byte pieces per thread and pass
+  for (int rbase = 0; rbase < p.d_v; rbase += kAbsorbRows) {
+    f32x4 acc[2][kAbsorbMaxRB];
 #pragma unroll
-    for (int c = 0; c < kMaxChunks; ++c)
-      if (c < nck) a[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(mh + (int64_t)(16 * ib + n) * p.d_c + 32 * c + 8 * qd));
-    for (int rb = 0; rb < RB; ++rb) {
-      const int r0 = b0 + 16 * rb;
-      if (r0 >= p.B) break;
-      const int bq = min(r0 + n, p.B - 1);                // rows past B compute a duplicate
-      const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W;
-      bf16x8 xq[kMaxChunks];
+    for (int k2 = 0; k2 < 2; ++k2)
 #pragma unroll
-      for (int c = 0; c < kMaxChunks; ++c)
-        if (c < nck) xq[c] = as_bf16x8(*reinterpret_cast<const u32x4*>(qrow + 32 * c + 8 * qd));
-      f32x4 acc = {0.f, 0.f, 0.f, 0.f};
+      for (int rb = 0; rb < kAbsorbMaxRB; ++rb) acc[k2][rb] = f32x4{0.f, 0.f, 0.f, 0.f};
+    for (int seg = 0; seg < nseg; ++seg) {
+      u32x4 piece[kFill];
 #pragma unroll
-      for (int c = 0; c < kMaxChunks; ++c)
-        if (c < nck) acc = mfma16(a[c], xq[c], acc);
-      // lane (n, qd) holds q~[r0 + n][16 ib + 4 qd + jj]
-      if (r0 + n < p.B)
-        *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(r0 + n) * p.H + h) * p.d_v + 16 * ib + 4 * qd) = acc;
+      for (int k = 0; k < kFill; ++k) {
+        const int pc = tid + kThreads * k, row = pc >> 4, col = seg * kAbsorbCols + 8 * (pc & 15);
+        piece[k] = (rbase + row < p.d_v && col < p.d_c)
+                       ? *reinterpret_cast<const u32x4*>(mh + (int64_t)(rbase + row) * p.d_c + col)
+                       : u32x4{0u, 0u, 0u, 0u};
+      }
+      // the query rows' chunks of this segment, requested with the pass (one
+      // memory round trip for both)
+      u32x4 xq[kAbsorbMaxRB][4];
+#pragma unroll
+      for (int rb = 0; rb < kAbsorbMaxRB; ++rb) {
+        const int bq = min(b0 + 16 * rb + n, p.B - 1);    // rows past B compute a duplicate
+        const uint16_t* qrow = qg + ((int64_t)bq * p.H + h) * W + seg * kAbsorbCols + 8 * qd;
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          xq[rb][c] = (rb < RB && seg * 4 + c < nck) ? *reinterpret_cast<const u32x4*>(qrow + 32 * c)
+                                                      : u32x4{0u, 0u, 0u, 0u};
+      }
+      if (rbase > 0 || seg > 0) __syncthreads();         // the previous pass has been read
+#pragma unroll
+      for (int k = 0; k < kFill; ++k) {
+        const int pc = tid + kThreads * k;
+        *reinterpret_cast<u32x4*>(ms + (pc >> 4) * kAbsorbStride + 8 * (pc & 15)) = piece[k];
+      }
+      __syncthreads();
+#pragma unroll
+      for (int k2 = 0; k2 < 2; ++k2) {
+        const int ibl = w + kWaves * k2;                  // 16-row block of the pass
+        if (rbase + 16 * ibl >= p.d_v) break;
+        bf16x8 a[4];
+#pragma unroll
+        for (int c = 0; c < 4; ++c)
+          a[c] = *reinterpret_cast<const bf16x8*>(ms + (16 * ibl + n) * kAbsorbStride + 32 * c + 8 * qd);
+#pragma unroll
+        for (int rb = 0; rb < kAbsorbMaxRB; ++rb) {
+          if (rb >= RB || b0 + 16 * rb >= p.B) break;
+#pragma unroll
+          for (int c = 0; c < 4; ++c)
+            if (seg * 4 + c < nck) acc[k2][rb] = mfma16(a[c], as_bf16x8(xq[rb][c]), acc[k2][rb]);
+        }
+      }
+    }
+    // lane (n, qd) holds q~[r0 + n][rbase + 16 ibl + 4 qd + jj]
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int i0 = rbase + 16 * (w + kWaves * k2);
+      if (i0 >= p.d_v) break;
+#pragma unroll
+      for (int rb = 0; rb < kAbsorbMaxRB; ++rb) {
+        const int r0 = b0 + 16 * rb;
+        if (rb >= RB || r0 >= p.B) break;
+        if (r0 + n < p.B)
+          *reinterpret_cast<f32x4*>(p.q_abs + ((int64_t)(r0 + n) * p.H + h) * p.d_v + i0 + 4 * qd) = acc[k2][rb];
+      }
     }
   }
   // the positional pairs of the workgroup's rows: 16 RB d_r / 2 tasks
@@ -1956,13 +2008,28 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   const float* op = p.o_part + (int64_t)row * p.S * p.d_v;
   // the row's split LSEs, up to 4 per lane (S <= 256), and their maximum
   float l[4];
-  float mx = -INFINITY;
 #pragma unroll
   for (int k = 0; k < 4; ++k) {
     const int s = lane + 64 * k;
     l[k] = s < p.S ? lp[s] : -INFINITY;
-    mx = fmaxf(mx, l[k]);
   }
+  // The first kSpec splits' partials are requested with the LSEs, before it
+  // is known which are empty (splits hold a sequence's rows from the front,
+  // so the first ones are the likely non-empty ones): one memory round trip
+  // less.  Empty splits' values are loaded but never used (selected away,
+  // so whatever they hold cannot reach the output).
+  constexpr int kSpec = 8;
+  float v0[kSpec][4];
+#pragma unroll
+  for (int j = 0; j < kSpec; ++j)
+#pragma unroll
+    for (int u = 0; u < 4; ++u) {
+      const int i = lane + 64 * u;
+      v0[j][u] = (j < p.S && i < p.d_v) ? op[(int64_t)j * p.d_v + i] : 0.f;
+    }
+  float mx = -INFINITY;
+#pragma unroll
+  for (int k = 0; k < 4; ++k) mx = fmaxf(mx, l[k]);
   mx = wave_max(mx);
   float acc[4] = {0.f, 0.f, 0.f, 0.f};
   float z = 0.f;
@@ -1974,11 +2041,20 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
       z += wk[k];
     }
     z = wave_sum(z);
-    // only the splits with rows are read, 8 at a time so their loads overlap
+#pragma unroll
+    for (int j = 0; j < kSpec; ++j) {
+      if (j >= p.S) break;
+      const float wj = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(wk[0]), j));
+      const bool live = __int_as_float(__builtin_amdgcn_readlane(__float_as_int(l[0]), j)) != -INFINITY;
+#pragma unroll
+      for (int u = 0; u < 4; ++u) acc[u] = live ? fmaf(wj, v0[j][u], acc[u]) : acc[u];
+    }
+    // the remaining splits with rows, 8 at a time so their loads overlap
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       if (64 * k >= p.S) break;
       unsigned long long mask = __ballot(l[k] != -INFINITY);
+      if (k == 0) mask &= ~((1ull << kSpec) - 1ull);
       while (mask != 0ull) {
         int sel[8];
         float wsel[8];

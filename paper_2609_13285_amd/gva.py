@@ -409,12 +409,13 @@ def device_cu_count(device=None) -> int:
 
 
 def prefer_fused(dims: GvaDims, num_splits: int, n_cu: int = 0) -> bool:
-    """Fuse the absorption into the attention kernel when the grid fits one
-    workgroup per CU (B * G * S workgroups) with at most two splits per
-    sequence: every fused workgroup absorbs its group's heads again, so
-    with more workgroups one gva_absorb_query launch is cheaper."""
+    """Fuse the absorption into the attention kernel when every workgroup of
+    the grid (B * G * S) is resident at once (two per CU): each fused
+    workgroup absorbs its group's heads again, which then costs one
+    absorption's time in all; with more workgroups the re-reads of M_h add
+    up and one gva_absorb_query launch is cheaper."""
     n_cu = int(n_cu) or device_cu_count()
-    return int(num_splits) <= 2 and dims.batch * dims.n_groups * int(num_splits) <= n_cu
+    return dims.batch * dims.n_groups * int(num_splits) <= 2 * n_cu
 
 
 def gva_version() -> int:

@@ -146,9 +146,9 @@ def test_pick_splits_is_host_only_and_bounded():
     assert spread == 2 * even                                   # widely spread lengths
     for S in (even, spread):
         assert 1 <= S <= gva.GVA_MAX_SPLITS
-    # fused only with at most two splits and B * G * S workgroups fitting one per CU
-    assert gva.prefer_fused(d, 1, n_cu=256) and not gva.prefer_fused(d, 2, n_cu=256)
-    assert gva.prefer_fused(d3, 2, n_cu=256) and not gva.prefer_fused(d3, 8, n_cu=256)
+    # fused only while the B * G * S workgroups are all resident (two per CU)
+    assert gva.prefer_fused(d, 2, n_cu=256) and not gva.prefer_fused(d, 3, n_cu=256)
+    assert gva.prefer_fused(d3, 16, n_cu=256) and not gva.prefer_fused(d3, 17, n_cu=256)
 
 
 def test_pick_splits_fixed_chunks_for_ragged_lengths():

@@ -191,6 +191,22 @@ def test_absorb_query_wide_positional_slice_many_rows():
     assert max_abs(qr.cpu(), qr_ref) <= 1e-6 * float(qr_ref.abs().max())
 
 
+def test_absorb_query_multi_pass_shapes():
+    # d_v = 256 and d_c = 320: M_h goes through LDS in two 128-row passes of
+    # three column segments (128, 128, 64), 33 rows in three row blocks
+    w = gva_inputs.Workload("absorb", 33, 512, 4, 2, 256, 320, 16, dtype="bf16")
+    inp = gva_inputs.make_inputs(w, 37)
+    qa_ref, qr_ref = oracle.absorb(inp["q"], inp["m"], inp["lens"], d_r=w.d_r)
+    dev = upload(inp)
+    qa = torch.full((33, 4, 256), float("nan"), dtype=torch.float32, device="cuda")
+    qr = torch.empty(33, 4, 16, dtype=torch.float32, device="cuda")
+    note("absorb bf16 d_v=256 d_c=320 B=33")
+    gva.gva_absorb_query(dims_of(w), dev["q"], dev["m"], dev["lens"], qa, qr)
+    torch.cuda.synchronize()
+    assert max_abs(qa.cpu(), qa_ref) <= 1e-5 * float(qa_ref.abs().max())
+    assert max_abs(qr.cpu(), qr_ref) <= 1e-6 * float(qr_ref.abs().max())
+
+
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 def test_append_matches_oracle_bitwise(dtype):
     B, G, T, dv, dr = 3, 4, 131072, 64, 32
