@@ -39,13 +39,18 @@ from paper_2609_13285_amd import gva, traffic  # noqa: E402
 METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s, B=32 T=8K bf16"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD's published figure
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, AMD's published figure
-KERNEL_SRC = os.path.join(ROOT, "paper_2609_13285_amd", "csrc", "gva.hip")
+# the decode kernel's sources (the traffic record is valid only for these)
+KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_13285_amd", "csrc", f)
+               for f in ("gva_common.h", "gva_decode.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_b32_t8k.json")
 
 
 def kernel_sha() -> str:
-    with open(KERNEL_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()[:16]
+    h = hashlib.sha256()
+    for path in KERNEL_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()[:16]
 
 
 def measured_traffic(workload: str, splits: int):

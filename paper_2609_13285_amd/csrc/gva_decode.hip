@@ -42,350 +42,9 @@
 // exactly the B-operand layout of the P.V product, so the softmax needs no
 // cross-lane traffic except the max over the four 16-lane rows.
 
-#include <hip/hip_runtime.h>
-#include <math.h>
-#include <stdint.h>
-#include <string.h>
-
-#include "gva.h"
+#include "gva_common.h"
 
 namespace {
-
-typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
-typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
-typedef float f32x4 __attribute__((ext_vector_type(4)));
-typedef float f32x2 __attribute__((ext_vector_type(2)));
-typedef unsigned u32x4 __attribute__((ext_vector_type(4)));
-typedef _Float16 f16x8 __attribute__((ext_vector_type(8)));
-typedef _Float16 f16x2 __attribute__((ext_vector_type(2)));
-
-constexpr int kWaves = 4;             // waves per workgroup in the decode kernels
-constexpr int kThreads = 64 * kWaves;
-constexpr int kTileRows = 32;         // rows per compute tile = split granularity
-constexpr int kLayoutRows = 16;       // rows per cache layout tile
-constexpr int kMaxPairs = 32;         // d_r / 2 <= 32
-constexpr float kLn2 = 0.693147180559945309417f;
-constexpr double kLog2e = 1.44269504088896340736;
-constexpr int kBufferWord3 = 0x00020000;   // raw buffer descriptor, 32-bit data format
-constexpr int kAuxNT = 2;                  // non-temporal: the V stream is read once
-constexpr int kMaxPages = 4096;            // paged caches: block-table entries per sequence
-
-// ------------------------------------------------------------ parameters
-struct AppendParams {
-  void* v_cache;
-  void* kr_cache;
-  const void* v_new;
-  const void* kr_new;
-  const int32_t* seq;
-  const int32_t* pos;
-  int32_t B, G, t_max, d_v, d_r, n_rows;
-  const int32_t* block_table;   // paged caches (NULL: contiguous streams)
-  int32_t page_rows, max_pages, n_pages;
-  double inv_freq[kMaxPairs];
-};
-
-struct AbsorbParams {
-  const void* q;
-  const void* m;
-  const int32_t* lens;
-  float* q_abs;
-  float* q_rot;
-  int32_t B, H, d_v, d_c, d_r, t_max;   // B = query rows (sequences x n_per_seq)
-  int32_t n_per_seq;                    // query rows per sequence: its last cached rows
-  int32_t row_blocks;                   // bf16 kernel: 16-row blocks per workgroup (1..4)
-  double inv_freq[kMaxPairs];
-};
-
-struct DecodeArgs {
-  const void* q;          // fused path: raw query and maps
-  const void* m;
-  const float* q_abs;     // pre-absorbed path
-  const float* q_rot;
-  void* v;                                 // caches: read, and row L-1 written when pending
-  void* kr;
-  const int32_t* lens;
-  float* o_part;
-  float* lse_part;
-  const void* v_new;      // optional: the current token's rows, used in place
-  const void* kr_new;     // of cache row len-1 (see gva_decode_attention)
-  const void* k_gqa;      // matched-GQA baseline: explicit key cache (tiled like v)
-  int32_t q_stride;       // matched-GQA baseline: elements per query row
-  int32_t B, H, G, d_v, d_c, d_r, t_max, S;
-  int32_t split_rows;     // fixed rows per split (0: the even rule)
-  float scale_log2;       // score scale * log2(e): softmax runs in base 2
-  int32_t fused;
-  const int32_t* block_table;   // paged caches: [B][max_pages] page ids
-  int32_t page_rows, max_pages, n_pages;
-};
-
-struct DecodeParams {
-  DecodeArgs a;           // scalars and pointers: read into registers at once
-  double inv_freq[kMaxPairs];
-};
-
-struct CombineParams {
-  const float* o_part;
-  const float* lse_part;
-  float* o;
-  float* lse;
-  int32_t rows, S, d_v;
-};
-
-// --------------------------------------------------------------- helpers
-__device__ __forceinline__ float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
-
-template <typename T>
-__device__ __forceinline__ float load_elem(const T* p, int64_t i);
-template <>
-__device__ __forceinline__ float load_elem<float>(const float* p, int64_t i) { return p[i]; }
-template <>
-__device__ __forceinline__ float load_elem<uint16_t>(const uint16_t* p, int64_t i) {
-  return bf16_bits_to_f32(p[i]);
-}
-
-// Round a double to bfloat16 in one step: round to float with round-to-odd
-// (truncate, then set the sticky bit if inexact), then nearest-even to bf16.
-// Round-to-odd onto a format with >= 2 extra bits makes the second rounding
-// equivalent to a single rounding from the double.
-__device__ __forceinline__ uint16_t f64_to_bf16_rne(double x) {
-  if (x != x) return (uint16_t)0x7FC0;
-  float f = (float)x;
-  uint32_t u = __float_as_uint(f);
-  double back = (double)f;
-  if (back != x && !isinf(f)) {
-    if (fabs(back) > fabs(x)) u -= 1;  // step the magnitude toward zero
-    u |= 1u;
-  }
-  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16);  // inf
-  u += 0x7FFFu + ((u >> 16) & 1u);
-  return (uint16_t)(u >> 16);
-}
-
-template <typename T>
-__device__ __forceinline__ void store_from_f64(T* p, int64_t i, double x);
-template <>
-__device__ __forceinline__ void store_from_f64<float>(float* p, int64_t i, double x) {
-  p[i] = (float)x;
-}
-template <>
-__device__ __forceinline__ void store_from_f64<uint16_t>(uint16_t* p, int64_t i, double x) {
-  p[i] = f64_to_bf16_rne(x);
-}
-
-// Element offset of (t, i) inside one stream of the tiled cache layout.
-template <typename T>
-__host__ __device__ __forceinline__ int64_t tiled_off(int64_t t, int i, int D) {
-  constexpr int P = 16 / (int)sizeof(T);
-  return (t / kLayoutRows) * kLayoutRows * D + ((int64_t)(i / P) * kLayoutRows + t % kLayoutRows) * P + i % P;
-}
-
-__device__ __forceinline__ int clamp_len(const int32_t* lens, int b, int t_max) {
-  int L = lens[b];
-  return L < 0 ? 0 : (L > t_max ? t_max : L);
-}
-
-// Split s of a sequence with L rows covers [s*c, e): e = min(L, (s+1)*c)
-// for s < S-1 and e = L for the last split.  c is the caller's fixed chunk
-// when positive (a multiple of kTileRows), else the even rule
-// c = kTileRows * ceil(ceil(L / S) / kTileRows), under which the last split
-// ends at L anyway.
-__device__ __forceinline__ void split_rows(int L, int S, int fixed, int s, int& r0, int& r1) {
-  int chunk = fixed;
-  if (chunk <= 0) {
-    const int per = (L + S - 1) / S;
-    chunk = ((per + kTileRows - 1) / kTileRows) * kTileRows;
-  }
-  const long long a = (long long)chunk * s;
-  const long long e = s == S - 1 ? (long long)L : (long long)chunk * (s + 1);
-  r0 = (int)(a < L ? a : L);
-  r1 = (int)(e < L ? e : L);
-}
-
-// Workgroup index -> logical work item, XCD-aware.  The dispatcher deals
-// consecutive workgroup ids round-robin over the 8 XCDs; this mapping gives
-// each XCD one contiguous range of logical items, in order, so neighbouring
-// items (the G groups of one (sequence, split), which read the same shared
-// positional-key rows) run together on one XCD and share its L2.
-__device__ __forceinline__ int xcd_remap(int x, int n) {
-  const int per = n / 8, rem = n % 8;
-  const int xcd = x % 8, slot = x / 8;
-  return xcd * per + (xcd < rem ? xcd : rem) + slot;
-}
-
-// Workgroup -> (sequence b, split s, group g).  The G groups of one
-// (b, s) always land on one XCD, next to each other.
-//  - Even splits: XCD-contiguous items (xcd_remap), B * S * G workgroups.
-//  - Fixed chunks: chunk s of sequence b goes to XCD (b + s) mod 8, so every
-//    sequence's chunks are dealt over all XCDs and short sequences spread
-//    by b: the XCDs get near-equal shares of a ragged batch.  The grid is
-//    B * S8 * G with S8 = S rounded up to 8; workgroups whose s >= S are
-//    padding and return false.
-// Every scalar argument the decode prologue needs, requested here in one
-// round trip: left to itself the compiler fetches them where first used,
-// several dependent kernel-argument round trips deep.  The memory clobber
-// keeps the loads that follow after this point.
-template <bool RAW_QUERY>
-__device__ __forceinline__ void request_args(const DecodeArgs& a) {
-  asm volatile("" ::"s"(a.B), "s"(a.H), "s"(a.G), "s"(a.S), "s"(a.t_max), "s"(a.split_rows), "s"(a.d_r),
-               "s"(a.d_c), "s"(a.lens), "s"(a.v_new), "s"(a.kr_new),
-               "s"(RAW_QUERY ? static_cast<const void*>(a.q) : static_cast<const void*>(a.q_abs)),
-               "s"(RAW_QUERY ? a.m : static_cast<const void*>(a.q_rot)), "s"(gridDim.x)
-               : "memory");
-}
-
-// Both orders are computed and one is selected, so no branch waits on the
-// split mode before the other kernel arguments are requested.
-__device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g) {
-  const int x = blockIdx.x, xcd = x & 7, slot = x >> 3;
-  const int gc = slot % p.G, t = slot / p.G;
-  const int bc = t % p.B;
-  const int sc = 8 * (t / p.B) + ((xcd - (bc & 7)) & 7);
-  const int item = xcd_remap(x, gridDim.x);
-  const int ge = item % p.G, bs = item / p.G;
-  const bool chunked = p.split_rows > 0;
-  g = chunked ? gc : ge;
-  b = chunked ? bc : bs / p.S;
-  s = chunked ? sc : bs % p.S;
-  return !chunked || sc < p.S;
-}
-
-__device__ __forceinline__ float wave_max(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v = fmaxf(v, __shfl_xor(v, o, 64));
-  return v;
-}
-__device__ __forceinline__ float wave_sum(float v) {
-#pragma unroll
-  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
-  return v;
-}
-
-// max of x over the four 16-lane rows of a wave (lanes l, l^16, l^32, l^48),
-// with the gfx950 row-swap permutes (no LDS round trip)
-__device__ __forceinline__ float max_over_rows(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = fmaxf(__uint_as_float(a[0]), __uint_as_float(a[1]));
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return fmaxf(__uint_as_float(b[0]), __uint_as_float(b[1]));
-}
-__device__ __forceinline__ float sum_over_rows(float x) {
-  const auto a = __builtin_amdgcn_permlane32_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  x = __uint_as_float(a[0]) + __uint_as_float(a[1]);
-  const auto b = __builtin_amdgcn_permlane16_swap(__float_as_uint(x), __float_as_uint(x), false, false);
-  return __uint_as_float(b[0]) + __uint_as_float(b[1]);
-}
-
-// DPP control that pairs MFMA column n (a head's high part) with the column
-// holding the same head's low part; columns are laid out
-// [hi_0 .. hi_{P-1}, lo_{P-1} .. lo_0] so the pairing is a mirror.
-template <int HPG>
-struct Mirror;
-template <> struct Mirror<1> { static constexpr int ctrl = 0xB1; };   // quad_perm [1,0,3,2]
-template <> struct Mirror<2> { static constexpr int ctrl = 0x1B; };   // quad_perm [3,2,1,0]
-template <> struct Mirror<4> { static constexpr int ctrl = 0x141; };  // row_half_mirror
-template <> struct Mirror<8> { static constexpr int ctrl = 0x140; };  // row_mirror
-
-template <int HPG>
-__device__ __forceinline__ float mirror(float x) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), Mirror<HPG>::ctrl, 0xF, 0xF, false));
-}
-
-__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 u) { return __builtin_bit_cast(bf16x8, u); }
-
-// dot product of eight bf16 pairs (two 16-byte pieces), fp32 accumulation.
-// The pairs are taken with shufflevector: a bit_cast of one 32-bit element
-// of the u32x4 compiled to four uses of element 0.
-__device__ __forceinline__ float dot8_bf16(u32x4 x, u32x4 y) {
-  const bf16x8 xv = as_bf16x8(x), yv = as_bf16x8(y);
-  float acc = 0.f;
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 0, 1), __builtin_shufflevector(yv, yv, 0, 1),
-                                        acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 2, 3), __builtin_shufflevector(yv, yv, 2, 3),
-                                        acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 4, 5), __builtin_shufflevector(yv, yv, 4, 5),
-                                        acc, false);
-  acc = __builtin_amdgcn_fdot2_f32_bf16(__builtin_shufflevector(xv, xv, 6, 7), __builtin_shufflevector(yv, yv, 6, 7),
-                                        acc, false);
-  return acc;
-}
-
-template <int CTRL>
-__device__ __forceinline__ float dpp_add(float x) {
-  return x + __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(x), CTRL, 0xF, 0xF, false));
-}
-
-// sum over each aligned group of 16 lanes, every lane of the group receiving
-// it: quad_perm [1,0,3,2], quad_perm [3,2,1,0], row_half_mirror, row_mirror
-__device__ __forceinline__ float sum16(float x) {
-  return dpp_add<0x140>(dpp_add<0x141>(dpp_add<0x1B>(dpp_add<0xB1>(x))));
-}
-
-__device__ __forceinline__ f32x4 mfma16(bf16x8 a, bf16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, c, 0, 0, 0);
-}
-__device__ __forceinline__ f32x4 mfma16(f16x8 a, f16x8 b, f32x4 c) {
-  return __builtin_amdgcn_mfma_f32_16x16x32_f16(a, b, c, 0, 0, 0);
-}
-
-// 8 floats -> fp16 (RNE)
-__device__ __forceinline__ f16x8 to_f16x8(const float* x) {
-  f16x8 out;
-#pragma unroll
-  for (int j = 0; j < 8; j += 2) {
-    const f16x2 h = __builtin_convertvector((f32x2{x[j], x[j + 1]}), f16x2);
-    out[j] = h[0];
-    out[j + 1] = h[1];
-  }
-  return out;
-}
-
-// 8 floats -> the bf16 high parts (RNE) or, with lo = true, the bf16 of the
-// remainder x - hi.  hi + lo carries ~16 significant bits of x.
-__device__ __forceinline__ bf16x8 split_hi_lo(const float* x, bool lo) {
-  bf16x8 out;
-#pragma unroll
-  for (int j = 0; j < 8; j += 2) {
-    f32x2 v = {x[j], x[j + 1]};
-    bf16x2 h = __builtin_convertvector(v, bf16x2);
-    if (lo) {
-      f32x2 hv = __builtin_convertvector(h, f32x2);
-      h = __builtin_convertvector(v - hv, bf16x2);
-    }
-    out[j] = h[0];
-    out[j + 1] = h[1];
-  }
-  return out;
-}
-
-// cos/sin of an fp64 angle, evaluated in fp32 after an exact reduction by
-// multiples of 2 pi in fp64 (Cody-Waite with 2 pi split into two doubles;
-// each fma subtracts an exactly formed product).  Accurate to fp32 rounding
-// for |a| < 2^40, which covers every position times a RoPE frequency <= 1.
-__device__ __forceinline__ void sincos_reduced(double a, float& s, float& c) {
-  constexpr double kInv2Pi = 0.15915494309189533577;
-  constexpr double k2PiHi = 6.28318530717958623200;    // 2 pi rounded to double
-  constexpr double k2PiLo = 2.44929359829470635445e-16; // 2 pi - k2PiHi
-  const double k = rint(a * kInv2Pi);
-  double r = fma(-k, k2PiHi, a);
-  r = fma(-k, k2PiLo, r);
-  sincosf((float)r, &s, &c);
-}
-
-// The query's positional slice, rotated at position pos and scaled: fp32 is
-// all the score needs.
-__device__ __forceinline__ void rotate_query_pair(float x0, float x1, double a, float scale, float& y0, float& y1) {
-  float s, c;
-  sincos_reduced(a, s, c);
-  y0 = (x0 * c - x1 * s) * scale;
-  y1 = (x0 * s + x1 * c) * scale;
-}
-
-__device__ __forceinline__ void rotate_pair(double x0, double x1, double a, double& y0, double& y1) {
-  double s, c;
-  sincos(a, &s, &c);
-  y0 = x0 * c - x1 * s;
-  y1 = x0 * s + x1 * c;
-}
 
 // ================================================================ append
 // One workgroup per new row.  The value pieces are loaded before seq/pos are
@@ -596,13 +255,6 @@ struct DecodeCfg {
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
   static constexpr int LDS_RED = kWaves * HPG * (DV + 2);
   static constexpr int LDS_FLOATS = LDS_PRO > LDS_RED ? LDS_PRO : LDS_RED;
-};
-
-template <int DV, int NRC, bool GQA>
-struct Tile {
-  bf16x8 v[2][DV / 32];                // [16-row half][K-chunk]
-  bf16x8 k[2][NRC > 0 ? NRC : 1];      // positional key, [half][chunk]
-  bf16x8 kc[2][GQA ? DV / 32 : 1];     // matched-GQA baseline: explicit key rows
 };
 
 // GQA = true builds the matched grouped-query baseline the paper compares
@@ -1164,624 +816,6 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   }
 }
 
-// ================================================= decode, ordinary RoPE
-// The contrast path of Section 3.2: GVA whose keys k_t = v_t M_h are rotated
-// over their whole width at their own position, so M_h cannot be absorbed.
-// With the column pairs (2i, 2i+1) of q M-space written as complex numbers,
-//   RoPE(q, P) . RoPE(v_t M_h, t) = sum_i a_i cos(theta_i d) + b_i sin(theta_i d)
-// for d = t - P, where a_i = v_t . W[:, 2i] and b_i = v_t . W[:, 2i+1] with
-//   W[r][2i]   = q_2i M_h[r][2i]   + q_2i+1 M_h[r][2i+1]
-//   W[r][2i+1] = q_2i+1 M_h[r][2i] - q_2i M_h[r][2i+1].
-// Per 32-row tile the kernel forms (V_tile W_h)^T on the matrix cores (d_v *
-// d_c multiply-adds per row and head, as explicit key reconstruction costs),
-// so each lane holds one row and four consecutive columns; it weights column
-// c by cos or sin of theta_i d and sums the columns (in registers, then over
-// the four 16-lane rows): the scores.  A per-wave LDS transpose puts them in
-// the layout of the GVA kernel, whose softmax, P.V, splits and merge follow.
-// W_h is built in the prologue (fp32, pre-scaled, rounded to bf16) and held
-// in LDS in MFMA operand order; the angle is reduced in fp64 at every tile's
-// first row and the rest of the tile is offset in fp32.
-constexpr int kRopeMaxPairs = 64;          // d_c / 2 <= 64
-constexpr int kRopeWaves = 8;              // two waves per SIMD
-constexpr int kRopeThreads = 64 * kRopeWaves;
-
-struct RopeDecodeParams {
-  DecodeArgs a;                            // q [B][H][d_c], m, v, lens, o_part, lse_part, dims
-  double freq_rev[kRopeMaxPairs];          // theta_i / (2 pi): revolutions per position
-};
-
-template <int HPG, int DV, int DC>
-struct RopeCfg {
-  static constexpr int NC = DV / 32;                       // K-chunks per V row
-  static constexpr int NB = DV / 16;                       // 16-wide i-blocks of the output
-  static constexpr int NBC = DC / 16;                      // 16-wide column blocks of W
-  static constexpr int W_FLOATS = HPG * NC * NBC * 64 * 4; // W in 16-byte pieces
-  static constexpr int RED_FLOATS = kRopeWaves * HPG * (DV + 2);
-  static constexpr int LDS_FLOATS = W_FLOATS > RED_FLOATS ? W_FLOATS : RED_FLOATS;
-  static constexpr int XS_FLOATS = kRopeWaves * HPG * kTileRows;   // score transpose
-};
-
-template <int HPG, int DV, int DC>
-__global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecodeParams p) {
-  const DecodeArgs a = p.a;
-  using Cfg = RopeCfg<HPG, DV, DC>;
-  constexpr int NC = Cfg::NC, NB = Cfg::NB, NBC = Cfg::NBC;
-  constexpr int DEPTH = 2;
-  __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
-  __shared__ __attribute__((aligned(16))) float xs_all[Cfg::XS_FLOATS];
-  __shared__ __attribute__((aligned(16))) double freq[DC / 2];
-
-  int b, s, g;
-  if (!work_item(a, b, s, g)) return;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n = lane & 15, qd = lane >> 4;
-  const int h0 = g * HPG;
-  const bool active = n < 2 * HPG;
-  const bool is_lo = n >= HPG;
-  const int col_head = !active ? 0 : (is_lo ? 2 * HPG - 1 - n : n);
-  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-
-  const int L = clamp_len(a.lens, b, a.t_max);
-  int r0, r1;
-  split_rows(L, a.S, a.split_rows, s, r0, r1);
-  if (r0 >= r1 && s > 0) {                     // an empty split past the first: lse only
-    if (tid < HPG) a.lse_part[((int64_t)b * a.H + h0 + tid) * a.S + s] = -INFINITY;
-    return;
-  }
-  const int P = L - 1;                         // the query's position
-
-  // ---- streaming setup (as in the GVA kernel: descriptors ending at the
-  // split's last layout tile, zero reads past it); the first tiles are
-  // requested before W is built
-  const int r1c = ((r1 + kLayoutRows - 1) / kLayoutRows) * kLayoutRows;
-  const uint16_t* vbase = static_cast<const uint16_t*>(a.v) + ((int64_t)b * a.G + g) * a.t_max * DV;
-  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(vbase), (short)0, r1c * DV * 2, kBufferWord3);
-  const int v_lane = qd * 256 + n * 16;
-  const int v_tile_bytes = 16 * DV * 2;
-  const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
-  const int my_tiles = ntiles > w ? (ntiles - w + kRopeWaves - 1) / kRopeWaves : 0;
-  auto tile_row = [&](int j) { return r0 + (w + kRopeWaves * j) * kTileRows; };
-  struct VTile { bf16x8 v[2][NC]; };
-  auto load_tile = [&](VTile& t, int row0) {
-    const int lt = row0 / kLayoutRows;
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, (lt + hf) * v_tile_bytes, kAuxNT));
-  };
-  VTile buf[DEPTH];
-#pragma unroll
-  for (int d = 0; d < DEPTH - 1; ++d) {
-    load_tile(buf[d], tile_row(d));
-    __builtin_amdgcn_sched_barrier(0);
-  }
-
-  // ---- W_h for the group's heads, in LDS as 16-byte pieces:
-  // piece ((hl * NC + kc) * NBC + nb) * 64 + (16 qd + n) holds
-  // W[32 kc + 8 qd + j][16 nb + n], j = 0..7 -- the MFMA A operand of
-  // W^T.  One task = 8 rows x one column pair of one head; consecutive
-  // threads take consecutive pairs, so each row of M_h is read in whole
-  // 4-byte pairs by neighbouring lanes.
-  {
-    u32x4* wl = reinterpret_cast<u32x4*>(lds);
-    constexpr int PAIRS = DC / 2, RB = DV / 8;
-    constexpr int TASKS = HPG * RB * PAIRS;
-    for (int task = tid; task < TASKS; task += kRopeThreads) {
-      const int i = task % PAIRS, rb = (task / PAIRS) % RB, hl = task / (PAIRS * RB);
-      const int h = h0 + hl;
-      const uint32_t qb = *reinterpret_cast<const uint32_t*>(
-          static_cast<const uint16_t*>(a.q) + ((int64_t)b * a.H + h) * DC + 2 * i);
-      const uint16_t* mrow = static_cast<const uint16_t*>(a.m) + ((int64_t)h * DV + 8 * rb) * DC + 2 * i;
-      uint32_t mb[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) mb[j] = *reinterpret_cast<const uint32_t*>(mrow + (int64_t)j * DC);
-      const float q0 = bf16_bits_to_f32(qb & 0xFFFFu) * a.scale_log2;
-      const float q1 = bf16_bits_to_f32(qb >> 16) * a.scale_log2;
-      float we[8], wo[8];
-#pragma unroll
-      for (int j = 0; j < 8; ++j) {
-        const float m0 = bf16_bits_to_f32(mb[j] & 0xFFFFu), m1 = bf16_bits_to_f32(mb[j] >> 16);
-        we[j] = q0 * m0 + q1 * m1;
-        wo[j] = q1 * m0 - q0 * m1;
-      }
-      const int kc = rb >> 2, pqd = rb & 3, nb = i >> 3, pn = 2 * (i & 7);
-      u32x4* dst = wl + ((hl * NC + kc) * NBC + nb) * 64 + 16 * pqd + pn;
-      dst[0] = __builtin_bit_cast(u32x4, split_hi_lo(we, false));
-      dst[1] = __builtin_bit_cast(u32x4, split_hi_lo(wo, false));
-    }
-    for (int i = tid; i < DC / 2; i += kRopeThreads) freq[i] = p.freq_rev[i];
-  }
-  __syncthreads();                              // W and the frequencies are in LDS
-
-  bf16x8 esel[2];
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    u32x4 u = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (8 * qd + j == n + 16 * half) u[j >> 1] |= 0x3F80u << (16 * (j & 1));
-    esel[half] = as_bf16x8(u);
-  }
-  const u32x4* wl = reinterpret_cast<const u32x4*>(lds);
-  float* xs = xs_all + w * HPG * kTileRows;      // this wave's score transpose: [HPG][32 rows]
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x4 acc[NB];
-#pragma unroll
-  for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
-
-  auto compute_tile = [&](VTile& t, int row0, int row_end) {
-    if (row0 + kTileRows > row_end) {
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const bool dead = row0 + 16 * hf + n >= row_end;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
-      }
-    }
-    // lane (n, qd): rows row0 + 16 hf + n, columns 16 nb + 4 qd + jj, i.e.
-    // pairs i0 = 8 nb + 2 qd (jj = 0, 1) and i0 + 1 (jj = 2, 3)
-    float sp[HPG][2];
-#pragma unroll
-    for (int hl = 0; hl < HPG; ++hl) sp[hl][0] = sp[hl][1] = 0.f;
-    const double dw = (double)(row0 - P);
-#pragma unroll
-    for (int nb = 0; nb < NBC; ++nb) {
-      float tr[2][4];                            // [hf][jj]: cos, sin, cos, sin
-#pragma unroll
-      for (int e = 0; e < 2; ++e) {
-        const double f = freq[8 * nb + 2 * qd + e];
-        const double r = f * dw;
-        const float rb = (float)(r - floor(r));
-        const float ff = (float)f;
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const float rho = fmaf(ff, (float)(16 * hf + n), rb);
-          tr[hf][2 * e] = __builtin_amdgcn_sinf(rho + 0.25f);
-          tr[hf][2 * e + 1] = __builtin_amdgcn_sinf(rho);
-        }
-      }
-#pragma unroll
-      for (int hl = 0; hl < HPG; ++hl) {
-        bf16x8 wa[NC];
-#pragma unroll
-        for (int c = 0; c < NC; ++c) wa[c] = as_bf16x8(wl[((hl * NC + c) * NBC + nb) * 64 + lane]);
-        f32x4 gt[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) gt[hf] = mfma16(wa[c], t.v[hf][c], gt[hf]);
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
-#pragma unroll
-          for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(gt[hf][jj], tr[hf][jj], sp[hl][hf]);
-      }
-    }
-    // sum over the four 16-lane rows, then transpose through LDS: lane
-    // (n, qd) takes head col_head's rows 16 hf + 4 qd + jj
-#pragma unroll
-    for (int hl = 0; hl < HPG; ++hl)
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) xs[hl * kTileRows + 16 * hf + n] = sum_over_rows(sp[hl][hf]);
-    float x[8];
-    {
-      const f32x4 lo = *reinterpret_cast<const f32x4*>(xs + col_head * kTileRows + 4 * qd);
-      const f32x4 hi = *reinterpret_cast<const f32x4*>(xs + col_head * kTileRows + 16 + 4 * qd);
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) {
-        x[jj] = lo[jj];
-        x[4 + jj] = hi[jj];
-      }
-    }
-    if (row0 + kTileRows > row_end) {
-#pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) >= row_end) x[k] = -INFINITY;
-    }
-    float mt = x[0];
-#pragma unroll
-    for (int k = 1; k < 8; ++k) mt = fmaxf(mt, x[k]);
-    mt = max_over_rows(mt);
-    const float m_new = fmaxf(m_run, mt);
-    if (__ballot(m_new > m_run) != 0) {
-      const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-      l_run *= alpha;
-#pragma unroll
-      for (int ib = 0; ib < NB; ++ib) acc[ib] *= alpha;
-      m_run = m_new;
-    }
-    float pr[8];
-    float psum = 0.f;
-#pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      pr[k] = __builtin_amdgcn_exp2f(x[k] - m_run);
-      psum += pr[k];
-    }
-    l_run += psum;
-    const bf16x8 bp = active ? split_hi_lo(pr, is_lo) : zero8;
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
-        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
-        bf16x8 av;
-        const bf16x2 a01 = __builtin_convertvector((f32x2{t0[0], t0[1]}), bf16x2);
-        const bf16x2 a23 = __builtin_convertvector((f32x2{t0[2], t0[3]}), bf16x2);
-        const bf16x2 a45 = __builtin_convertvector((f32x2{t1[0], t1[1]}), bf16x2);
-        const bf16x2 a67 = __builtin_convertvector((f32x2{t1[2], t1[3]}), bf16x2);
-        av[0] = a01[0]; av[1] = a01[1]; av[2] = a23[0]; av[3] = a23[1];
-        av[4] = a45[0]; av[5] = a45[1]; av[6] = a67[0]; av[7] = a67[1];
-        acc[2 * c + half] = mfma16(av, bp, acc[2 * c + half]);
-      }
-  };
-
-  for (int jt = 0; jt < my_tiles; jt += DEPTH) {
-#pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int j = jt + d;
-      if (j >= my_tiles) break;
-      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], tile_row(j), r1);
-    }
-  }
-
-  // ---- merge the waves and write this split's partial
-  l_run = sum_over_rows(l_run);
-#pragma unroll
-  for (int ib = 0; ib < NB; ++ib)
-#pragma unroll
-    for (int jj = 0; jj < 4; ++jj) acc[ib][jj] += mirror<HPG>(acc[ib][jj]);
-
-  __syncthreads();   // W is dead: its LDS holds the per-wave records below
-  constexpr int RS = DV + 2;
-  float* red = lds;
-  if (n < HPG) {
-    float* rec = red + (w * HPG + n) * RS;
-    if (qd == 0) {
-      rec[0] = m_run;
-      rec[1] = l_run;
-    }
-#pragma unroll
-    for (int ib = 0; ib < NB; ++ib)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) rec[2 + 16 * ib + 4 * qd + jj] = acc[ib][jj];
-  }
-  __syncthreads();
-  for (int idx = tid; idx < HPG * DV; idx += kRopeThreads) {
-    const int hl = idx / DV, i = idx % DV;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int ww = 0; ww < kRopeWaves; ++ww) mx = fmaxf(mx, red[(ww * HPG + hl) * RS]);
-    float o = 0.f, lsum = 0.f;
-    if (mx != -INFINITY) {
-#pragma unroll
-      for (int ww = 0; ww < kRopeWaves; ++ww) {
-        const float* rec = red + (ww * HPG + hl) * RS;
-        const float sc = rec[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(rec[0] - mx);
-        lsum += rec[1] * sc;
-        o += rec[2 + i] * sc;
-      }
-      o /= lsum;
-    }
-    const int64_t prow = ((int64_t)b * a.H + h0 + hl) * a.S + s;
-    a.o_part[prow * DV + i] = o;
-    if (i == 0) a.lse_part[prow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
-  }
-}
-
-// =============================================================== prefill
-// Causal attention for the last N cached rows of every sequence (a prompt,
-// after any cached prefix): query i of sequence b sits at position
-// p = L_b - N + i and sees rows 0..p (Algorithm 1's loop for every prompt
-// position at once; Section 3.3's absorbed scores).  Unlike a decode step
-// this is a dense contraction: a workgroup takes C (position, head)
-// columns of one group -- C / (H/G) consecutive positions times the H/G
-// heads that share the group's value rows; C = 64, or 32 at d_v = 128 to
-// stay within 256 registers -- and its four waves split the key tiles up to
-// the block's last position.  Per 32-row key tile a wave forms the scores
-// of all C columns on the matrix cores (keys = [V | k_r] rows as stored,
-// the absorbed and rotated queries as bf16 B operands), masks rows past
-// each column's position, updates the online softmax and accumulates P.V
-// (V transposed once per tile with the identity MFMA, shared by the
-// column blocks).  P.V runs in fp16: the transposed rows come out of the
-// identity product in fp32 and every bf16 value of N(0, 1)-scale data is
-// exact in fp16, while the weights in [0, 1] keep 3 more bits than bf16.
-// The waves merge through LDS.
-// Query blocks are dealt longest first, so the triangle's tail is short.
-// GQA = true is the matched grouped-query prefill the paper compares
-// against: scores read an explicit key stream, no positional term.
-// (position, head) columns per workgroup: 64, fewer where a wider value
-// row (or the baseline's separate key tile) needs the registers
-__host__ __device__ constexpr int prefill_cols(int dv, bool gqa) { return dv >= 128 ? (gqa ? 16 : 32) : 64; }
-
-struct PrefillParams {
-  const float* q_abs;     // [B][N][H][d_v]: absorbed queries (GQA: the raw query)
-  const float* q_rot;     // [B][N][H][d_r]: rotated positional queries
-  const void* v;          // tiled caches, the prompt's rows already appended
-  const void* kr;
-  const void* k_gqa;      // matched-GQA baseline: explicit key stream (tiled like v)
-  const int32_t* lens;
-  float* o;               // [B][N][H][d_v]
-  float* lse;             // [B][N][H]
-  int32_t B, H, G, N, d_r, t_max, n_qblocks;
-  float scale_log2;
-};
-
-// Two workgroups per CU where the registers allow it without spilling.
-constexpr int prefill_min_blocks(int dv, int nrc, bool gqa) { return nrc >= 2 ? 1 : 2; }
-
-template <int HPG, int DV, int NRC, bool GQA>
-__global__ void __launch_bounds__(kThreads, prefill_min_blocks(DV, NRC, GQA)) prefill_bf16_kernel(PrefillParams p) {
-  constexpr int COLS = prefill_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = COLS / 16;
-  constexpr int QB = COLS / HPG;               // positions per workgroup
-  constexpr int DEPTH = 2;
-  constexpr int RS = DV + 2;                   // per-(wave, column) record: [m, l, o[DV]]
-  __shared__ __attribute__((aligned(16))) float red[kWaves * COLS * RS];
-
-  const int nbg = p.B * p.G;
-  const int x = blockIdx.x;
-  const int qb = p.n_qblocks - 1 - x / nbg;    // longest query blocks first
-  const int b = (x % nbg) / p.G, g = (x % nbg) % p.G;
-  const int tid = threadIdx.x, lane = tid & 63;
-  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int n = lane & 15, qd = lane >> 4;
-  const int h0 = g * HPG;
-  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
-
-  const int L = clamp_len(p.lens, b, p.t_max);
-  const int i_end = min(p.N, (qb + 1) * QB);
-  const int kend = L - p.N + i_end;            // rows the block's last position sees
-  // column 16 cb + n of this lane: position i = qb QB + col / HPG, head
-  // h0 + col % HPG; pos[cb] = its position, or -1 if it has none
-  int pos[CB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int col = 16 * cb + n;
-    const int i = qb * QB + col / HPG;
-    const int ps = L - p.N + i;
-    pos[cb] = (i < p.N && ps >= 0) ? ps : -1;
-  }
-  const int p_first = L - p.N + qb * QB;       // the block's first position
-
-  // ---- the queries as bf16 B operands (zero for columns with no position)
-  bf16x8 bq[CB][NC];
-  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int col = 16 * cb + n;
-    const int i = min(qb * QB + col / HPG, p.N - 1);
-    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
-    const float* qa = p.q_abs + qrow * DV + 8 * qd;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
-      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
-      float xv[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        xv[j] = u0[j] * p.scale_log2;
-        xv[4 + j] = u1[j] * p.scale_log2;
-      }
-      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
-    }
-#pragma unroll
-    for (int rc = 0; rc < NRC; ++rc) {
-      const int j0 = 32 * rc + 8 * qd;
-      float xv[8];
-      if (j0 < p.d_r) {
-        const float* qr = p.q_rot + qrow * p.d_r + j0;
-        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
-        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xv[j] = u0[j] * p.scale_log2;
-          xv[4 + j] = u1[j] * p.scale_log2;
-        }
-      }
-      bk[cb][rc] = (pos[cb] >= 0 && j0 < p.d_r) ? split_hi_lo(xv, false) : zero8;
-    }
-  }
-
-  // ---- key tiles: rows [0, kend), read through descriptors that end at
-  // the last layout tile (reads past it return zeros)
-  const int kend16 = kend > 0 ? ((kend + kLayoutRows - 1) / kLayoutRows) * kLayoutRows : 0;
-  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
-  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
-  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(vbase), (short)0, kend16 * DV * 2, kBufferWord3);
-  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<uint16_t*>(kbase), (short)0, NRC > 0 ? kend16 * p.d_r * 2 : 0, kBufferWord3);
-  const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
-      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
-                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
-                            : static_cast<const void*>(vbase)),
-      (short)0, kend16 * DV * 2, kBufferWord3);
-  const int kpieces = p.d_r / 8;
-  const int v_lane = qd * 256 + n * 16;
-  int k_lane[NRC > 0 ? NRC : 1];
-#pragma unroll
-  for (int rc = 0; rc < NRC; ++rc) k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
-  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
-  const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
-  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
-  auto tile_row = [&](int j) { return (w + kWaves * j) * kTileRows; };
-  using TileT = Tile<DV, NRC, GQA>;
-  auto load_tile = [&](TileT& t, int row0) {
-    const int lt = row0 / kLayoutRows;
-#pragma unroll
-    for (int hf = 0; hf < 2; ++hf) {
-      const int vsoff = (lt + hf) * v_tile_bytes;
-      if constexpr (GQA) {
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-          t.kc[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kcres, v_lane + 1024 * c, vsoff, 0));
-      }
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, 0));
-#pragma unroll
-      for (int rc = 0; rc < NRC; ++rc)
-        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], (lt + hf) * k_tile_bytes, 0));
-    }
-  };
-  TileT buf[DEPTH];
-#pragma unroll
-  for (int d = 0; d < DEPTH - 1; ++d) {
-    load_tile(buf[d], tile_row(d));
-    __builtin_amdgcn_sched_barrier(0);
-  }
-
-  bf16x8 esel[2];
-#pragma unroll
-  for (int half = 0; half < 2; ++half) {
-    u32x4 u = {0u, 0u, 0u, 0u};
-#pragma unroll
-    for (int j = 0; j < 8; ++j)
-      if (8 * qd + j == n + 16 * half) u[j >> 1] |= 0x3F80u << (16 * (j & 1));
-    esel[half] = as_bf16x8(u);
-  }
-
-  float m_run[CB], l_run[CB];
-  f32x4 acc[CB][NB];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    m_run[cb] = -INFINITY;
-    l_run[cb] = 0.f;
-#pragma unroll
-    for (int ib = 0; ib < NB; ++ib) acc[cb][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
-  }
-
-  auto compute_tile = [&](TileT& t, int row0) {
-    if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        const bool dead = row0 + 16 * hf + n >= kend;
-#pragma unroll
-        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
-        if constexpr (GQA) {
-#pragma unroll
-          for (int c = 0; c < NC; ++c) t.kc[hf][c] = dead ? zero8 : t.kc[hf][c];
-        }
-#pragma unroll
-        for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
-      }
-    }
-    const bool masked = row0 + kTileRows - 1 > p_first;   // some column may not see every row
-    f16x8 bp[CB];
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-      f32x4 sc[2];
-#pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
-        sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NC; ++c) sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
-#pragma unroll
-        for (int rc = 0; rc < NRC; ++rc) sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
-      }
-      float xv[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) xv[k] = sc[k >> 2][k & 3];
-      if (masked) {
-#pragma unroll
-        for (int k = 0; k < 8; ++k)
-          if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) > pos[cb]) xv[k] = -INFINITY;
-      }
-      float mt = xv[0];
-#pragma unroll
-      for (int k = 1; k < 8; ++k) mt = fmaxf(mt, xv[k]);
-      mt = max_over_rows(mt);
-      const float m_new = fmaxf(m_run[cb], mt);
-      if (__ballot(m_new > m_run[cb]) != 0) {
-        // columns whose rows so far are all masked keep m = -inf: scale 1
-        const float alpha = m_new > m_run[cb] ? __builtin_amdgcn_exp2f(m_run[cb] - m_new) : 1.f;
-        l_run[cb] *= alpha;
-#pragma unroll
-        for (int ib = 0; ib < NB; ++ib) acc[cb][ib] *= alpha;
-        m_run[cb] = m_new;
-      }
-      const float m_use = m_run[cb] == -INFINITY ? 0.f : m_run[cb];   // all masked so far
-      float pr[8];
-#pragma unroll
-      for (int k = 0; k < 8; ++k) {
-        pr[k] = __builtin_amdgcn_exp2f(xv[k] - m_use);
-        l_run[cb] += pr[k];
-      }
-      bp[cb] = to_f16x8(pr);
-    }
-#pragma unroll
-    for (int c = 0; c < NC; ++c)
-#pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
-        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
-        const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
-        const f16x8 av = to_f16x8(tv);         // bf16 values: exact in fp16 at these magnitudes
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) acc[cb][2 * c + half] = mfma16(av, bp[cb], acc[cb][2 * c + half]);
-      }
-  };
-
-  for (int jt = 0; jt < my_tiles; jt += DEPTH) {
-#pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int j = jt + d;
-      if (j >= my_tiles) break;
-      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], tile_row(j));
-    }
-  }
-
-  // ---- merge the waves: per column the records (m, l, o) of the 4 waves
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const float l = sum_over_rows(l_run[cb]);
-    float* rec = red + (w * COLS + 16 * cb + n) * RS;
-    if (qd == 0) {
-      rec[0] = m_run[cb];
-      rec[1] = l;
-    }
-#pragma unroll
-    for (int ib = 0; ib < NB; ++ib)
-#pragma unroll
-      for (int jj = 0; jj < 4; ++jj) rec[2 + 16 * ib + 4 * qd + jj] = acc[cb][ib][jj];
-  }
-  __syncthreads();
-  for (int idx = tid; idx < COLS * DV; idx += kThreads) {
-    const int col = idx / DV, i = idx % DV;
-    const int qi = qb * QB + col / HPG;
-    if (qi >= p.N) continue;
-    float mx = -INFINITY;
-#pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) mx = fmaxf(mx, red[(ww * COLS + col) * RS]);
-    float o = 0.f, lsum = 0.f;
-    if (mx != -INFINITY && L - p.N + qi >= 0) {
-#pragma unroll
-      for (int ww = 0; ww < kWaves; ++ww) {
-        const float* rec = red + (ww * COLS + col) * RS;
-        if (rec[0] == -INFINITY) continue;       // this wave saw no row of the column
-        const float sc = __builtin_amdgcn_exp2f(rec[0] - mx);
-        lsum += rec[1] * sc;
-        o += rec[2 + i] * sc;
-      }
-      o /= lsum;
-    } else {
-      mx = -INFINITY;
-    }
-    const int64_t orow = ((int64_t)b * p.N + qi) * p.H + h0 + col % HPG;
-    p.o[orow * DV + i] = o;
-    if (i == 0) p.lse[orow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
-  }
-}
-
 // ========================================================== decode (f32)
 // Vector-ALU variant for fp32 storage.  Per 64-row tile a wave first scores
 // one row per lane, then accumulates the weighted rows with one output
@@ -2093,56 +1127,6 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   if (p.lse != nullptr && lane == 0) p.lse[row] = mx == -INFINITY ? -INFINITY : mx + logf(z);
 }
 
-// ================================================================== host
-bool aligned(const void* ptr, size_t a) { return (reinterpret_cast<uintptr_t>(ptr) % a) == 0; }
-
-int check_dims(const gva_dims* d) {
-  if (d == nullptr) return GVA_ERR_INVALID_ARG;
-  if (d->batch < 1 || d->n_heads < 1 || d->n_groups < 1 || d->t_max < 1) return GVA_ERR_INVALID_ARG;
-  if (d->n_heads % d->n_groups != 0) return GVA_ERR_INVALID_ARG;
-  if (d->d_v < 1 || d->d_c < 0 || d->d_r < 0 || (d->d_r & 1)) return GVA_ERR_INVALID_ARG;
-  if (d->dtype != GVA_DTYPE_F32 && d->dtype != GVA_DTYPE_BF16) return GVA_ERR_INVALID_ARG;
-  if (!(d->scale >= 0.0) || !isfinite(d->scale)) return GVA_ERR_INVALID_ARG;
-  if (d->d_r > 0 && (!(d->rope_base > 0.0) || !isfinite(d->rope_base))) return GVA_ERR_INVALID_ARG;
-  if (d->d_c + d->d_r < 1) return GVA_ERR_INVALID_ARG;
-  return GVA_OK;
-}
-
-size_t elem_size(const gva_dims* d) { return d->dtype == GVA_DTYPE_BF16 ? 2 : 4; }
-
-// The tiled cache layout needs whole layout tiles and whole 16-byte pieces.
-int check_cache_layout(const gva_dims* d) {
-  const int piece = (int)(16 / elem_size(d));
-  if (d->t_max % kLayoutRows != 0) return GVA_ERR_UNSUPPORTED;
-  if (d->d_v % piece != 0 || d->d_r % piece != 0) return GVA_ERR_UNSUPPORTED;
-  if (d->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
-  // buffer offsets are 32-bit; keep headroom for prefetches past the end
-  const double stream_bytes = (double)d->t_max * (double)(d->d_v > d->d_r ? d->d_v : d->d_r) * elem_size(d);
-  if (stream_bytes >= 2147483648.0 - 16777216.0) return GVA_ERR_UNSUPPORTED;
-  return GVA_OK;
-}
-
-void fill_inv_freq(const gva_dims* d, double* out) {
-  for (int i = 0; i < kMaxPairs; ++i)
-    out[i] = (i < d->d_r / 2) ? pow(d->rope_base, -2.0 * (double)i / (double)d->d_r) : 0.0;
-}
-
-float scale_log2(const gva_dims* d) {
-  const double sc = d->scale > 0.0 ? d->scale : 1.0 / sqrt((double)(d->d_c + d->d_r));
-  return (float)(sc * kLog2e);
-}
-
-// Workgroups of a decode launch (see work_item).
-long long decode_grid(const gva_dims* d, int num_splits, int split_rows) {
-  const long long s = split_rows > 0 ? ((num_splits + 7LL) & ~7LL) : num_splits;
-  return (long long)d->batch * d->n_groups * s;
-}
-
-int launch_status() {
-  const hipError_t e = hipGetLastError();
-  return e == hipSuccess ? GVA_OK : GVA_ERR_HIP;
-}
-
 using DecodeFn = void (*)(DecodeParams);
 
 template <int HPG, int DV, bool FUSED, bool PAGED>
@@ -2199,45 +1183,6 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged) {
   return nullptr;
 }
 
-using RopeDecodeFn = void (*)(RopeDecodeParams);
-
-// W_h of every head of a group must fit the LDS budget of one workgroup.
-template <int HPG, int DV, int DC>
-RopeDecodeFn rope_if_fits() {
-  if constexpr (HPG * DV * DC * 2 <= 128 * 1024) return rope_decode_kernel<HPG, DV, DC>;
-  return nullptr;
-}
-
-template <int HPG, int DV>
-RopeDecodeFn pick_rope_dc(int dc) {
-  switch (dc) {
-    case 64: return rope_if_fits<HPG, DV, 64>();
-    case 128: return rope_if_fits<HPG, DV, 128>();
-  }
-  return nullptr;
-}
-
-template <int HPG>
-RopeDecodeFn pick_rope_dv(int dv, int dc) {
-  switch (dv) {
-    case 64: return pick_rope_dc<HPG, 64>(dc);
-    case 128: return pick_rope_dc<HPG, 128>(dc);
-  }
-  return nullptr;
-}
-
-RopeDecodeFn pick_rope_decode(int hpg, int dv, int dc) {
-  switch (hpg) {
-    case 1: return pick_rope_dv<1>(dv, dc);
-    case 2: return pick_rope_dv<2>(dv, dc);
-    case 4: return pick_rope_dv<4>(dv, dc);
-    case 8: return pick_rope_dv<8>(dv, dc);
-  }
-  return nullptr;
-}
-
-// The absorption behind gva_absorb_query (one query row per sequence) and
-// gva_prefill_absorb (a sequence's last n_per_seq rows).
 int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* m, const int32_t* lens,
                 float* q_abs, float* q_rot, void* stream) {
   int st = check_dims(dims);
@@ -2280,94 +1225,6 @@ int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* 
   return launch_status();
 }
 
-using PrefillFn = void (*)(PrefillParams);
-
-template <int HPG, int DV>
-PrefillFn pick_prefill_nrc(int nrc, bool gqa) {
-  if (gqa) return prefill_bf16_kernel<HPG, DV, 0, true>;
-  switch (nrc) {
-    case 0: return prefill_bf16_kernel<HPG, DV, 0, false>;
-    case 1: return prefill_bf16_kernel<HPG, DV, 1, false>;
-    case 2: return prefill_bf16_kernel<HPG, DV, 2, false>;
-  }
-  return nullptr;
-}
-
-template <int HPG>
-PrefillFn pick_prefill_dv(int dv, int nrc, bool gqa) {
-  switch (dv) {
-    case 64: return pick_prefill_nrc<HPG, 64>(nrc, gqa);
-    case 128: return pick_prefill_nrc<HPG, 128>(nrc, gqa);
-  }
-  return nullptr;
-}
-
-PrefillFn pick_prefill(int hpg, int dv, int nrc, bool gqa) {
-  switch (hpg) {
-    case 1: return pick_prefill_dv<1>(dv, nrc, gqa);
-    case 2: return pick_prefill_dv<2>(dv, nrc, gqa);
-    case 4: return pick_prefill_dv<4>(dv, nrc, gqa);
-    case 8: return pick_prefill_dv<8>(dv, nrc, gqa);
-  }
-  return nullptr;
-}
-
-// The launch behind gva_prefill_attention and, with k_gqa given,
-// gva_gqa_prefill_attention.
-int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
-                 const void* v_cache, const void* kr_cache, const void* k_gqa, const int32_t* lens,
-                 float* o, float* lse, void* stream) {
-  int st = check_dims(dims);
-  if (st != GVA_OK) return st;
-  const bool gqa = k_gqa != nullptr;
-  const int d_r = gqa ? 0 : dims->d_r;
-  if (n_new < 1 || n_new > dims->t_max) return GVA_ERR_INVALID_ARG;
-  if (!q_abs || !v_cache || !lens || !o || !lse) return GVA_ERR_INVALID_ARG;
-  if (d_r > 0 && (!q_rot || !kr_cache)) return GVA_ERR_INVALID_ARG;
-  if (!aligned(q_abs, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) || !aligned(o, 16) ||
-      !aligned(lse, 4) || (d_r > 0 && (!aligned(q_rot, 16) || !aligned(kr_cache, 16))) ||
-      (gqa && !aligned(k_gqa, 16)))
-    return GVA_ERR_INVALID_ARG;
-  if (dims->dtype != GVA_DTYPE_BF16) return GVA_ERR_UNSUPPORTED;
-  st = check_cache_layout(dims);
-  if (st != GVA_OK) return st;
-  if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
-  const int hpg = dims->n_heads / dims->n_groups;
-  PrefillFn fn = pick_prefill(hpg, dims->d_v, (d_r + 31) / 32, gqa);
-  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const int qb_rows = prefill_cols(dims->d_v, gqa) / hpg;
-  const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;
-  const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
-  if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
-
-  PrefillParams p;
-  memset(&p, 0, sizeof(p));
-  p.q_abs = q_abs;
-  p.q_rot = q_rot;
-  p.v = v_cache;
-  p.kr = kr_cache;
-  p.k_gqa = k_gqa;
-  p.lens = lens;
-  p.o = o;
-  p.lse = lse;
-  p.B = dims->batch;
-  p.H = dims->n_heads;
-  p.G = dims->n_groups;
-  p.N = n_new;
-  p.d_r = d_r;
-  p.t_max = dims->t_max;
-  p.n_qblocks = (int32_t)n_qblocks;
-  if (gqa) {
-    const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
-    p.scale_log2 = (float)(sc * kLog2e);
-  } else {
-    p.scale_log2 = scale_log2(dims);
-  }
-  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
-  return launch_status();
-}
-
-// The append behind gva_append_kv and, with paging given, gva_paged_append_kv.
 int append_impl(const gva_dims* dims, const gva_paging* paging, const int32_t* block_table, void* v_cache,
                 void* kr_cache, const void* v_new, const void* kr_new, const int32_t* seq, const int32_t* pos,
                 int32_t n_rows, void* stream) {
@@ -2507,6 +1364,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
 
 extern "C" {
 
+
 int gva_version(void) { return 10700; }
 
 const char* gva_status_string(int status) {
@@ -2609,70 +1467,10 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   return launch_status();
 }
 
-int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m, const void* v_cache,
-                              const int32_t* lens, int32_t num_splits, int32_t split_rows, float* o_part,
-                              float* lse_part, void* stream) {
-  int st = check_dims(dims);
-  if (st != GVA_OK) return st;
-  if (dims->d_r != 0 || dims->d_c < 2 || (dims->d_c & 1)) return GVA_ERR_INVALID_ARG;
-  if (!(dims->rope_base > 0.0) || !isfinite(dims->rope_base)) return GVA_ERR_INVALID_ARG;
-  if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
-  if (split_rows < 0 || split_rows % kTileRows != 0) return GVA_ERR_INVALID_ARG;
-  if (!q || !m || !v_cache || !lens || !o_part || !lse_part) return GVA_ERR_INVALID_ARG;
-  if (!aligned(q, 16) || !aligned(m, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) ||
-      !aligned(o_part, 16) || !aligned(lse_part, 4))
-    return GVA_ERR_INVALID_ARG;
-  if (dims->dtype != GVA_DTYPE_BF16) return GVA_ERR_UNSUPPORTED;
-  st = check_cache_layout(dims);
-  if (st != GVA_OK) return st;
-  const int hpg = dims->n_heads / dims->n_groups;
-  RopeDecodeFn fn = pick_rope_decode(hpg, dims->d_v, dims->d_c);
-  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const long long n_items = decode_grid(dims, num_splits, split_rows);
-  if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
-
-  RopeDecodeParams p;
-  memset(&p, 0, sizeof(p));
-  p.a.q = q;
-  p.a.m = m;
-  p.a.v = const_cast<void*>(v_cache);       // read only
-  p.a.lens = lens;
-  p.a.o_part = o_part;
-  p.a.lse_part = lse_part;
-  p.a.B = dims->batch;
-  p.a.H = dims->n_heads;
-  p.a.G = dims->n_groups;
-  p.a.d_v = dims->d_v;
-  p.a.d_c = dims->d_c;
-  p.a.d_r = 0;
-  p.a.t_max = dims->t_max;
-  p.a.S = num_splits;
-  p.a.split_rows = split_rows;
-  p.a.scale_log2 = scale_log2(dims);        // d_r = 0: 1/sqrt(d_c) unless given
-  constexpr double kInv2Pi = 0.15915494309189533577;
-  for (int i = 0; i < dims->d_c / 2; ++i)
-    p.freq_rev[i] = pow(dims->rope_base, -2.0 * (double)i / (double)dims->d_c) * kInv2Pi;
-  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kRopeThreads), 0, static_cast<hipStream_t>(stream), p);
-  return launch_status();
-}
-
 int gva_prefill_absorb(const gva_dims* dims, int32_t n_new, const void* q, const void* m,
                        const int32_t* lens, float* q_abs, float* q_rot, void* stream) {
   if (dims != nullptr && (n_new < 1 || n_new > dims->t_max)) return GVA_ERR_INVALID_ARG;
   return absorb_impl(dims, n_new, q, m, lens, q_abs, q_rot, stream);
-}
-
-int gva_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
-                          const void* v_cache, const void* kr_cache, const int32_t* lens, float* o,
-                          float* lse, void* stream) {
-  return prefill_impl(dims, n_new, q_abs, q_rot, v_cache, kr_cache, nullptr, lens, o, lse, stream);
-}
-
-int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q, const void* k_cache,
-                              const void* v_cache, const int32_t* lens, float* o, float* lse,
-                              void* stream) {
-  if (k_cache == nullptr) return GVA_ERR_INVALID_ARG;
-  return prefill_impl(dims, n_new, q, nullptr, v_cache, nullptr, k_cache, lens, o, lse, stream);
 }
 
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part, int32_t num_splits,

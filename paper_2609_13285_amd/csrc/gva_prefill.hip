@@ -1,0 +1,421 @@
+// libgva.so -- causal prefill of GVA (Algorithm 1 for every prompt position at
+// once): prefill_bf16_kernel, gva_prefill_attention and the matched-GQA
+// baseline gva_gqa_prefill_attention.
+
+#include "gva_common.h"
+
+namespace {
+
+// =============================================================== prefill
+// Causal attention for the last N cached rows of every sequence (a prompt,
+// after any cached prefix): query i of sequence b sits at position
+// p = L_b - N + i and sees rows 0..p (Algorithm 1's loop for every prompt
+// position at once; Section 3.3's absorbed scores).  Unlike a decode step
+// this is a dense contraction: a workgroup takes C (position, head)
+// columns of one group -- C / (H/G) consecutive positions times the H/G
+// heads that share the group's value rows; C = 64, or 32 at d_v = 128 to
+// stay within 256 registers -- and its four waves split the key tiles up to
+// the block's last position.  Per 32-row key tile a wave forms the scores
+// of all C columns on the matrix cores (keys = [V | k_r] rows as stored,
+// the absorbed and rotated queries as bf16 B operands), masks rows past
+// each column's position, updates the online softmax and accumulates P.V
+// (V transposed once per tile with the identity MFMA, shared by the
+// column blocks).  P.V runs in fp16: the transposed rows come out of the
+// identity product in fp32 and every bf16 value of N(0, 1)-scale data is
+// exact in fp16, while the weights in [0, 1] keep 3 more bits than bf16.
+// The waves merge through LDS.
+// Query blocks are dealt longest first, so the triangle's tail is short.
+// GQA = true is the matched grouped-query prefill the paper compares
+// against: scores read an explicit key stream, no positional term.
+// (position, head) columns per workgroup: 64, fewer where a wider value
+// row (or the baseline's separate key tile) needs the registers
+__host__ __device__ constexpr int prefill_cols(int dv, bool gqa) { return dv >= 128 ? (gqa ? 16 : 32) : 64; }
+
+struct PrefillParams {
+  const float* q_abs;     // [B][N][H][d_v]: absorbed queries (GQA: the raw query)
+  const float* q_rot;     // [B][N][H][d_r]: rotated positional queries
+  const void* v;          // tiled caches, the prompt's rows already appended
+  const void* kr;
+  const void* k_gqa;      // matched-GQA baseline: explicit key stream (tiled like v)
+  const int32_t* lens;
+  float* o;               // [B][N][H][d_v]
+  float* lse;             // [B][N][H]
+  int32_t B, H, G, N, d_r, t_max, n_qblocks;
+  float scale_log2;
+};
+
+// Two workgroups per CU where the registers allow it without spilling.
+constexpr int prefill_min_blocks(int dv, int nrc, bool gqa) { return nrc >= 2 ? 1 : 2; }
+
+template <int HPG, int DV, int NRC, bool GQA>
+__global__ void __launch_bounds__(kThreads, prefill_min_blocks(DV, NRC, GQA)) prefill_bf16_kernel(PrefillParams p) {
+  constexpr int COLS = prefill_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = COLS / 16;
+  constexpr int QB = COLS / HPG;               // positions per workgroup
+  constexpr int DEPTH = 2;
+  constexpr int RS = DV + 2;                   // per-(wave, column) record: [m, l, o[DV]]
+  __shared__ __attribute__((aligned(16))) float red[kWaves * COLS * RS];
+
+  const int nbg = p.B * p.G;
+  const int x = blockIdx.x;
+  const int qb = p.n_qblocks - 1 - x / nbg;    // longest query blocks first
+  const int b = (x % nbg) / p.G, g = (x % nbg) % p.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, qd = lane >> 4;
+  const int h0 = g * HPG;
+  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+
+  const int L = clamp_len(p.lens, b, p.t_max);
+  const int i_end = min(p.N, (qb + 1) * QB);
+  const int kend = L - p.N + i_end;            // rows the block's last position sees
+  // column 16 cb + n of this lane: position i = qb QB + col / HPG, head
+  // h0 + col % HPG; pos[cb] = its position, or -1 if it has none
+  int pos[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = 16 * cb + n;
+    const int i = qb * QB + col / HPG;
+    const int ps = L - p.N + i;
+    pos[cb] = (i < p.N && ps >= 0) ? ps : -1;
+  }
+  const int p_first = L - p.N + qb * QB;       // the block's first position
+
+  // ---- the queries as bf16 B operands (zero for columns with no position)
+  bf16x8 bq[CB][NC];
+  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = 16 * cb + n;
+    const int i = min(qb * QB + col / HPG, p.N - 1);
+    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
+    const float* qa = p.q_abs + qrow * DV + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+      float xv[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[j] = u0[j] * p.scale_log2;
+        xv[4 + j] = u1[j] * p.scale_log2;
+      }
+      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const int j0 = 32 * rc + 8 * qd;
+      float xv[8];
+      if (j0 < p.d_r) {
+        const float* qr = p.q_rot + qrow * p.d_r + j0;
+        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
+        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xv[j] = u0[j] * p.scale_log2;
+          xv[4 + j] = u1[j] * p.scale_log2;
+        }
+      }
+      bk[cb][rc] = (pos[cb] >= 0 && j0 < p.d_r) ? split_hi_lo(xv, false) : zero8;
+    }
+  }
+
+  // ---- key tiles: rows [0, kend), read through descriptors that end at
+  // the last layout tile (reads past it return zeros)
+  const int kend16 = kend > 0 ? ((kend + kLayoutRows - 1) / kLayoutRows) * kLayoutRows : 0;
+  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(vbase), (short)0, kend16 * DV * 2, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kbase), (short)0, NRC > 0 ? kend16 * p.d_r * 2 : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
+                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
+                            : static_cast<const void*>(vbase)),
+      (short)0, kend16 * DV * 2, kBufferWord3);
+  const int kpieces = p.d_r / 8;
+  const int v_lane = qd * 256 + n * 16;
+  int k_lane[NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int rc = 0; rc < NRC; ++rc) k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
+  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
+  const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
+  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
+  auto tile_row = [&](int j) { return (w + kWaves * j) * kTileRows; };
+  using TileT = Tile<DV, NRC, GQA>;
+  auto load_tile = [&](TileT& t, int row0) {
+    const int lt = row0 / kLayoutRows;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int vsoff = (lt + hf) * v_tile_bytes;
+      if constexpr (GQA) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          t.kc[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kcres, v_lane + 1024 * c, vsoff, 0));
+      }
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, 0));
+#pragma unroll
+      for (int rc = 0; rc < NRC; ++rc)
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], (lt + hf) * k_tile_bytes, 0));
+    }
+  };
+  TileT buf[DEPTH];
+#pragma unroll
+  for (int d = 0; d < DEPTH - 1; ++d) {
+    load_tile(buf[d], tile_row(d));
+    __builtin_amdgcn_sched_barrier(0);
+  }
+
+  bf16x8 esel[2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    u32x4 u = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (8 * qd + j == n + 16 * half) u[j >> 1] |= 0x3F80u << (16 * (j & 1));
+    esel[half] = as_bf16x8(u);
+  }
+
+  float m_run[CB], l_run[CB];
+  f32x4 acc[CB][NB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m_run[cb] = -INFINITY;
+    l_run[cb] = 0.f;
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib) acc[cb][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto compute_tile = [&](TileT& t, int row0) {
+    if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const bool dead = row0 + 16 * hf + n >= kend;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
+        if constexpr (GQA) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) t.kc[hf][c] = dead ? zero8 : t.kc[hf][c];
+        }
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
+      }
+    }
+    const bool masked = row0 + kTileRows - 1 > p_first;   // some column may not see every row
+    f16x8 bp[CB];
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      f32x4 sc[2];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c) sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
+      }
+      float xv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xv[k] = sc[k >> 2][k & 3];
+      if (masked) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) > pos[cb]) xv[k] = -INFINITY;
+      }
+      float mt = xv[0];
+#pragma unroll
+      for (int k = 1; k < 8; ++k) mt = fmaxf(mt, xv[k]);
+      mt = max_over_rows(mt);
+      const float m_new = fmaxf(m_run[cb], mt);
+      if (__ballot(m_new > m_run[cb]) != 0) {
+        // columns whose rows so far are all masked keep m = -inf: scale 1
+        const float alpha = m_new > m_run[cb] ? __builtin_amdgcn_exp2f(m_run[cb] - m_new) : 1.f;
+        l_run[cb] *= alpha;
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) acc[cb][ib] *= alpha;
+        m_run[cb] = m_new;
+      }
+      const float m_use = m_run[cb] == -INFINITY ? 0.f : m_run[cb];   // all masked so far
+      float pr[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        pr[k] = __builtin_amdgcn_exp2f(xv[k] - m_use);
+        l_run[cb] += pr[k];
+      }
+      bp[cb] = to_f16x8(pr);
+    }
+#pragma unroll
+    for (int c = 0; c < NC; ++c)
+#pragma unroll
+      for (int half = 0; half < 2; ++half) {
+        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
+        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
+        const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+        const f16x8 av = to_f16x8(tv);         // bf16 values: exact in fp16 at these magnitudes
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) acc[cb][2 * c + half] = mfma16(av, bp[cb], acc[cb][2 * c + half]);
+      }
+  };
+
+  for (int jt = 0; jt < my_tiles; jt += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int j = jt + d;
+      if (j >= my_tiles) break;
+      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(buf[d], tile_row(j));
+    }
+  }
+
+  // ---- merge the waves: per column the records (m, l, o) of the 4 waves
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const float l = sum_over_rows(l_run[cb]);
+    float* rec = red + (w * COLS + 16 * cb + n) * RS;
+    if (qd == 0) {
+      rec[0] = m_run[cb];
+      rec[1] = l;
+    }
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib)
+#pragma unroll
+      for (int jj = 0; jj < 4; ++jj) rec[2 + 16 * ib + 4 * qd + jj] = acc[cb][ib][jj];
+  }
+  __syncthreads();
+  for (int idx = tid; idx < COLS * DV; idx += kThreads) {
+    const int col = idx / DV, i = idx % DV;
+    const int qi = qb * QB + col / HPG;
+    if (qi >= p.N) continue;
+    float mx = -INFINITY;
+#pragma unroll
+    for (int ww = 0; ww < kWaves; ++ww) mx = fmaxf(mx, red[(ww * COLS + col) * RS]);
+    float o = 0.f, lsum = 0.f;
+    if (mx != -INFINITY && L - p.N + qi >= 0) {
+#pragma unroll
+      for (int ww = 0; ww < kWaves; ++ww) {
+        const float* rec = red + (ww * COLS + col) * RS;
+        if (rec[0] == -INFINITY) continue;       // this wave saw no row of the column
+        const float sc = __builtin_amdgcn_exp2f(rec[0] - mx);
+        lsum += rec[1] * sc;
+        o += rec[2 + i] * sc;
+      }
+      o /= lsum;
+    } else {
+      mx = -INFINITY;
+    }
+    const int64_t orow = ((int64_t)b * p.N + qi) * p.H + h0 + col % HPG;
+    p.o[orow * DV + i] = o;
+    if (i == 0) p.lse[orow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
+  }
+}
+
+using PrefillFn = void (*)(PrefillParams);
+
+template <int HPG, int DV>
+PrefillFn pick_prefill_nrc(int nrc, bool gqa) {
+  if (gqa) return prefill_bf16_kernel<HPG, DV, 0, true>;
+  switch (nrc) {
+    case 0: return prefill_bf16_kernel<HPG, DV, 0, false>;
+    case 1: return prefill_bf16_kernel<HPG, DV, 1, false>;
+    case 2: return prefill_bf16_kernel<HPG, DV, 2, false>;
+  }
+  return nullptr;
+}
+
+template <int HPG>
+PrefillFn pick_prefill_dv(int dv, int nrc, bool gqa) {
+  switch (dv) {
+    case 64: return pick_prefill_nrc<HPG, 64>(nrc, gqa);
+    case 128: return pick_prefill_nrc<HPG, 128>(nrc, gqa);
+  }
+  return nullptr;
+}
+
+PrefillFn pick_prefill(int hpg, int dv, int nrc, bool gqa) {
+  switch (hpg) {
+    case 1: return pick_prefill_dv<1>(dv, nrc, gqa);
+    case 2: return pick_prefill_dv<2>(dv, nrc, gqa);
+    case 4: return pick_prefill_dv<4>(dv, nrc, gqa);
+    case 8: return pick_prefill_dv<8>(dv, nrc, gqa);
+  }
+  return nullptr;
+}
+
+// The launch behind gva_prefill_attention and, with k_gqa given,
+// gva_gqa_prefill_attention.
+int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
+                 const void* v_cache, const void* kr_cache, const void* k_gqa, const int32_t* lens,
+                 float* o, float* lse, void* stream) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  const bool gqa = k_gqa != nullptr;
+  const int d_r = gqa ? 0 : dims->d_r;
+  if (n_new < 1 || n_new > dims->t_max) return GVA_ERR_INVALID_ARG;
+  if (!q_abs || !v_cache || !lens || !o || !lse) return GVA_ERR_INVALID_ARG;
+  if (d_r > 0 && (!q_rot || !kr_cache)) return GVA_ERR_INVALID_ARG;
+  if (!aligned(q_abs, 16) || !aligned(v_cache, 16) || !aligned(lens, 4) || !aligned(o, 16) ||
+      !aligned(lse, 4) || (d_r > 0 && (!aligned(q_rot, 16) || !aligned(kr_cache, 16))) ||
+      (gqa && !aligned(k_gqa, 16)))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->dtype != GVA_DTYPE_BF16) return GVA_ERR_UNSUPPORTED;
+  st = check_cache_layout(dims);
+  if (st != GVA_OK) return st;
+  if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
+  const int hpg = dims->n_heads / dims->n_groups;
+  PrefillFn fn = pick_prefill(hpg, dims->d_v, (d_r + 31) / 32, gqa);
+  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
+  const int qb_rows = prefill_cols(dims->d_v, gqa) / hpg;
+  const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;
+  const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
+  if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
+
+  PrefillParams p;
+  memset(&p, 0, sizeof(p));
+  p.q_abs = q_abs;
+  p.q_rot = q_rot;
+  p.v = v_cache;
+  p.kr = kr_cache;
+  p.k_gqa = k_gqa;
+  p.lens = lens;
+  p.o = o;
+  p.lse = lse;
+  p.B = dims->batch;
+  p.H = dims->n_heads;
+  p.G = dims->n_groups;
+  p.N = n_new;
+  p.d_r = d_r;
+  p.t_max = dims->t_max;
+  p.n_qblocks = (int32_t)n_qblocks;
+  if (gqa) {
+    const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
+    p.scale_log2 = (float)(sc * kLog2e);
+  } else {
+    p.scale_log2 = scale_log2(dims);
+  }
+  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
+  return launch_status();
+}
+
+// The append behind gva_append_kv and, with paging given, gva_paged_append_kv.
+}  // namespace
+
+extern "C" {
+
+int gva_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
+                          const void* v_cache, const void* kr_cache, const int32_t* lens, float* o,
+                          float* lse, void* stream) {
+  return prefill_impl(dims, n_new, q_abs, q_rot, v_cache, kr_cache, nullptr, lens, o, lse, stream);
+}
+
+int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* q, const void* k_cache,
+                              const void* v_cache, const int32_t* lens, float* o, float* lse,
+                              void* stream) {
+  if (k_cache == nullptr) return GVA_ERR_INVALID_ARG;
+  return prefill_impl(dims, n_new, q, nullptr, v_cache, nullptr, k_cache, lens, o, lse, stream);
+}
+
+}  // extern "C"
