@@ -44,6 +44,8 @@ struct PrefillParams {
   float scale_log2;
 };
 
+constexpr float kLazyMax = 8.f;
+
 // Two workgroups per CU where the registers allow it without spilling.
 constexpr int prefill_min_blocks(int dv, int nrc, bool gqa) { return nrc >= 2 ? 1 : 2; }
 
@@ -229,7 +231,11 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(DV, NRC, GQA)) pr
       for (int k = 1; k < 8; ++k) mt = fmaxf(mt, xv[k]);
       mt = max_over_rows(mt);
       const float m_new = fmaxf(m_run[cb], mt);
-      if (__ballot(m_new > m_run[cb]) != 0) {
+      // The running maximum moves only once some column's tile maximum
+      // exceeds it by more than kLazyMax (log2 units): the weights then stay
+      // below 2^kLazyMax (fp16 holds them; the sums are fp32), and the
+      // accumulators are rescaled on few tiles.
+      if (__ballot(mt > m_run[cb] + kLazyMax) != 0) {
         // columns whose rows so far are all masked keep m = -inf: scale 1
         const float alpha = m_new > m_run[cb] ? __builtin_amdgcn_exp2f(m_run[cb] - m_new) : 1.f;
         l_run[cb] *= alpha;

@@ -783,6 +783,29 @@ def test_prefill_matches_oracle(hpg, dv, dr):
     _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"prefill/hpg{hpg}/dv{dv}/dr{dr}")
 
 
+def test_prefill_sharp_scores():
+    # queries scaled by 2.5: scores spread ~2.5x wider than the workloads'.
+    # The running maximum keeps growing by less than the lazy-rescale
+    # threshold, so weights run above 1 between rescales.  The error grows
+    # with the score magnitude (the absorbed query is rounded once to bf16,
+    # the weights to fp16), so the bound is the bf16 gate, and the LSE bound
+    # scales with the queries.
+    w = gva_inputs.Workload("prefill", 2, 640, 8, 2, 128, 128, 16, dtype="bf16")
+    N = 200
+    lens = torch.tensor([640, 333], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 43, lens=lens)
+    q = (gva_inputs.prefill_queries(w, 43, N).float() * 2.5).to(torch.bfloat16)
+    o_ref, lse_ref = oracle.prefill(q, inp["m"], inp["v"], inp["kr"], lens, rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("m", "v", "kr", "lens")})
+    note("prefill sharp scores: GPU")
+    o, lse = gva.prefill(dims_of(w), q.cuda(), dev["m"], dev["v"], dev["kr"], dev["lens"])
+    torch.cuda.synchronize()
+    err, lerr = max_abs(o.cpu(), o_ref), lse_err(lse.cpu(), lse_ref)
+    note(f"prefill sharp scores: max|o-o_ref| = {err:.3e}  max|lse-lse_ref| = {lerr:.3e}")
+    assert err <= TOL["bf16"], err
+    assert lerr <= 2.5e-2, lerr
+
+
 def test_prefill_after_append_of_the_prompt():
     # Algorithm 1's append for every prompt row (gva_append_kv), then the
     # prefill over the appended caches, against the oracle doing the same
