@@ -69,6 +69,35 @@ def test_split_partials_match_oracle(name):
             assert lse_err(lse_part[:, :, s], lse_ref) <= 1e-3
 
 
+def test_random_shapes_sweep():
+    # 40 seeded random cases over the supported shape space: H/G, G, d_v,
+    # d_c (incl. widths that are not powers of two), d_r (incl. 0), batch,
+    # capacity, lengths (0, 1, capacity and random), even and fixed-chunk
+    # splits, fused and separate absorption, bf16 and fp32 storage
+    rng = torch.Generator().manual_seed(2609)
+    pick = lambda xs: xs[int(torch.randint(len(xs), (1,), generator=rng))]
+    for case in range(40):
+        dtype = "f32" if case % 8 == 7 else "bf16"
+        hpg, G = pick([1, 2, 4, 8]), pick([1, 2, 3])
+        dv, dc = pick([64, 128]), pick([32, 64, 96, 128, 160, 224, 256])
+        dr = pick([0, 8, 16, 24, 32, 40, 48, 64])
+        B, T = pick([1, 2, 3, 5]), 16 * pick([2, 3, 7, 16, 25])
+        w = gva_inputs.Workload("sweep", B, T, hpg * G, G, dv, dc, dr, dtype=dtype)
+        lens = torch.randint(0, T + 1, (B,), generator=rng, dtype=torch.int32)
+        lens[0] = pick([0, 1, T, int(lens[0])])
+        S = pick([1, 2, 3, 5])
+        rows = pick([0, 0, 32, 64, 96])
+        fused = bool(pick([True, False]))
+        inp = gva_inputs.make_inputs(w, 100 + case, lens=lens)
+        o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
+                                       rope_base=w.rope_base)
+        label = (f"sweep {case}: {dtype} H{hpg * G} G{G} dv{dv} dc{dc} dr{dr} B{B} T{T} "
+                 f"lens={lens.tolist()} S{S} rows{rows} fused={fused}")
+        note(label)
+        o, lse, _, _ = run_decode(w, upload(inp), S, fused=fused, split_rows=rows)
+        _check(w, o, lse, o_ref, lse_ref, label)
+
+
 # ------------------------------------------------------------------ shapes
 SHAPES = [
     # (H, G, d_v, d_c, d_r)
