@@ -311,7 +311,7 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
     d0 = gva.make_dims(w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, 0, w.t_max, w.dtype, w.rope_base)
     q0 = dev["q"][..., :w.d_c].contiguous()
     bufs = gva.DecodeBuffers(d0, S)
-    fused0 = gva.prefer_fused(d0, S)
+    fused0 = gva.gva_prefer_fused(d0, S, split_rows)
     q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
 
     def combine():
@@ -520,7 +520,7 @@ def main():
     seq = torch.arange(w.batch, dtype=torch.int32)
     pos = (inp["lens"] - 1).clamp(min=0).to(torch.int32)
     bufs = gva.DecodeBuffers(d, S)
-    fused = gva.prefer_fused(d, S) if args.absorb == "auto" else args.absorb == "fused"
+    fused = gva.gva_prefer_fused(d, S, split_rows) if args.absorb == "auto" else args.absorb == "fused"
     q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
     q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
     stream = torch.cuda.current_stream()

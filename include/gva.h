@@ -348,8 +348,10 @@ int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* 
  * gva_combine -- log-sum-exp merge of split partials, for every (b, h):
  *   LSE = log sum_s exp(lse_part[b][h][s]);
  *   o[b][h][:] = sum_s exp(lse_part[b][h][s] - LSE) * o_part[b][h][s][:]
- * Partials with lse = -inf are skipped without reading their o_part; if
- * all are, o = 0 and LSE = -inf.
+ * Partials with lse = -inf do not contribute, whatever their o_part holds
+ * (the first eight of a row are requested together with the LSEs, before
+ * it is known which are empty; later ones only when non-empty); if all are
+ * empty, o = 0 and LSE = -inf.
  * lse may be NULL.  o [B][H][d_v] fp32, lse [B][H] fp32; d_v <= 256.
  */
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part,
@@ -367,6 +369,18 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
  */
 int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
                     int32_t* split_rows);
+
+/*
+ * gva_prefer_fused -- host heuristic: 1 if a gva_decode_attention launch of
+ * num_splits splits (split_rows as for that call) should take the raw query
+ * and absorb it in the attention kernel (the fused path), 0 if one
+ * gva_absorb_query call ahead of it costs less.  The fused path pays for an
+ * absorption in every workgroup; it wins while all B * G * splits
+ * workgroups (fixed chunks: splits rounded up to 8) are resident at once,
+ * two per CU on a device with n_cu compute units (0 = ask the current
+ * device).  Returns 0 for invalid dims.  Pure host code; enqueues nothing.
+ */
+int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu);
 
 /* Human-readable name of a gva_status value (static storage). */
 const char* gva_status_string(int status);

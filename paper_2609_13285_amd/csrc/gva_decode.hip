@@ -1127,6 +1127,15 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   if (p.lse != nullptr && lane == 0) p.lse[row] = mx == -INFINITY ? -INFINITY : mx + logf(z);
 }
 
+// Compute units of the current device (256 if the runtime cannot say).
+int device_cu_count() {
+  int dev = 0, cu = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cu > 0)
+    return cu;
+  return 256;
+}
+
 using DecodeFn = void (*)(DecodeParams);
 
 template <int HPG, int DV, bool FUSED, bool PAGED>
@@ -1495,18 +1504,17 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   return launch_status();
 }
 
+int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu) {
+  if (check_dims(dims) != GVA_OK || num_splits < 1 || split_rows < 0) return 0;
+  if (n_cu <= 0) n_cu = device_cu_count();
+  return decode_grid(dims, num_splits, split_rows) <= 2LL * n_cu ? 1 : 0;
+}
+
 int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
                     int32_t* split_rows) {
   if (split_rows != nullptr) *split_rows = 0;
   if (check_dims(dims) != GVA_OK) return 1;
-  if (n_cu <= 0) {
-    int dev = 0, cu = 0;
-    if (hipGetDevice(&dev) == hipSuccess &&
-        hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cu > 0)
-      n_cu = cu;
-    else
-      n_cu = 256;
-  }
+  if (n_cu <= 0) n_cu = device_cu_count();
   if (max_len <= 0 || max_len > dims->t_max) max_len = dims->t_max;
   const long long streams = (long long)dims->batch * dims->n_groups;
   if (total_len <= 0) total_len = (long long)dims->batch * max_len;

@@ -23,7 +23,8 @@ GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
            "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
            "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
-           "gva_gqa_prefill_attention", "gva_pick_splits", "gva_status_string", "gva_version")
+           "gva_gqa_prefill_attention", "gva_pick_splits", "gva_prefer_fused", "gva_status_string",
+           "gva_version")
 GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
@@ -79,6 +80,7 @@ def lib() -> ctypes.CDLL:
         L.gva_paged_append_kv.argtypes = [D, PG, P, P, P, P, P, P, P, I32, P]
         L.gva_paged_decode_attention.argtypes = [D, PG, P, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32, ctypes.POINTER(I32)]
+        L.gva_prefer_fused.argtypes = [D, I32, I32, I32]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
@@ -408,14 +410,15 @@ def device_cu_count(device=None) -> int:
                                                 torch.cuda.current_device()).multi_processor_count)
 
 
-def prefer_fused(dims: GvaDims, num_splits: int, n_cu: int = 0) -> bool:
-    """Fuse the absorption into the attention kernel when every workgroup of
-    the grid (B * G * S) is resident at once (two per CU): each fused
-    workgroup absorbs its group's heads again, which then costs one
-    absorption's time in all; with more workgroups the re-reads of M_h add
-    up and one gva_absorb_query launch is cheaper."""
-    n_cu = int(n_cu) or device_cu_count()
-    return dims.batch * dims.n_groups * int(num_splits) <= 2 * n_cu
+def gva_prefer_fused(dims: GvaDims, num_splits: int, split_rows: int = 0, n_cu: int = 0) -> bool:
+    """The library's choice between the fused absorption and one
+    gva_absorb_query launch for a decode launch of this plan."""
+    return bool(lib().gva_prefer_fused(ctypes.byref(dims), int(num_splits), int(split_rows), int(n_cu)))
+
+
+def prefer_fused(dims: GvaDims, num_splits: int, n_cu: int = 0, split_rows: int = 0) -> bool:
+    """gva_prefer_fused (kept under its former name for callers)."""
+    return gva_prefer_fused(dims, num_splits, split_rows, n_cu)
 
 
 def gva_version() -> int:
@@ -470,7 +473,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
     """
     S = int(num_splits)
     if fused is None:
-        fused = prefer_fused(dims, S)
+        fused = gva_prefer_fused(dims, S, split_rows)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
     pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)
@@ -567,7 +570,7 @@ def paged_decode(dims: GvaDims, paging: GvaPaging, q, m, v_pool, kr_pool, block_
     """decode() on paged caches."""
     S = int(num_splits)
     if fused is None:
-        fused = prefer_fused(dims, S)
+        fused = gva_prefer_fused(dims, S, split_rows)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_pool.device)
     pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)

@@ -147,8 +147,11 @@ def test_pick_splits_is_host_only_and_bounded():
     for S in (even, spread):
         assert 1 <= S <= gva.GVA_MAX_SPLITS
     # fused only while the B * G * S workgroups are all resident (two per CU)
-    assert gva.prefer_fused(d, 2, n_cu=256) and not gva.prefer_fused(d, 3, n_cu=256)
-    assert gva.prefer_fused(d3, 16, n_cu=256) and not gva.prefer_fused(d3, 17, n_cu=256)
+    assert gva.gva_prefer_fused(d, 2, 0, 256) and not gva.gva_prefer_fused(d, 3, 0, 256)
+    assert gva.gva_prefer_fused(d3, 16, 0, 256) and not gva.gva_prefer_fused(d3, 17, 0, 256)
+    # fixed chunks pad the splits to a multiple of 8
+    assert gva.gva_prefer_fused(d3, 16, 64, 256) and not gva.gva_prefer_fused(d3, 9, 64, 128)
+    assert not gva.gva_prefer_fused(d3, 0, 0, 256) and not gva.gva_prefer_fused(d3, 2, -32, 256)
 
 
 def test_pick_splits_fixed_chunks_for_ragged_lengths():
