@@ -1205,7 +1205,7 @@ int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* 
   if (dims->d_r / 2 > kMaxPairs) return GVA_ERR_UNSUPPORTED;
   const long long rows = (long long)dims->batch * n_per_seq;
   if (rows > (1LL << 20) || rows * dims->n_heads > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
-  AbsorbParams p;
+  AbsorbParams p{};
   p.q = q;
   p.m = m;
   p.lens = lens;
@@ -1248,7 +1248,7 @@ int append_impl(const gva_dims* dims, const gva_paging* paging, const int32_t* b
   if (dims->d_r > 0 && (!aligned(kr_cache, 16) || !aligned(kr_new, 4))) return GVA_ERR_INVALID_ARG;
   st = check_cache_layout(dims);
   if (st != GVA_OK) return st;
-  AppendParams p;
+  AppendParams p{};
   p.v_cache = v_cache;
   p.kr_cache = kr_cache;
   p.v_new = v_new;
@@ -1321,7 +1321,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
   const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
-  DecodeParams p;
+  DecodeParams p{};
   p.a.q = q;
   p.a.m = m;
   p.a.q_abs = q_abs;
@@ -1452,7 +1452,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
-  DecodeParams p;
+  DecodeParams p{};
   memset(&p, 0, sizeof(p));
   p.a.q = q;
   p.a.v = const_cast<void*>(v_cache);       // read only: the GQA kernel never appends
@@ -1491,7 +1491,7 @@ int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part
   if (!aligned(o_part, 4) || !aligned(lse_part, 4) || !aligned(o, 4) || (lse && !aligned(lse, 4)))
     return GVA_ERR_INVALID_ARG;
   if (dims->d_v > kCombineMaxDv) return GVA_ERR_UNSUPPORTED;
-  CombineParams p;
+  CombineParams p{};
   p.o_part = o_part;
   p.lse_part = lse_part;
   p.o = o;

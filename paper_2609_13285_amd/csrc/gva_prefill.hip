@@ -379,7 +379,7 @@ int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const 
   const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
-  PrefillParams p;
+  PrefillParams p{};
   memset(&p, 0, sizeof(p));
   p.q_abs = q_abs;
   p.q_rot = q_rot;

@@ -382,7 +382,7 @@ int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m
   const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
-  RopeDecodeParams p;
+  RopeDecodeParams p{};
   memset(&p, 0, sizeof(p));
   p.a.q = q;
   p.a.m = m;
