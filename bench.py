@@ -477,8 +477,9 @@ def main():
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(json.dumps({"error": "this build measures one GPU only; the decode path is "
-                          "single-GPU (see DESIGN.md for how it would shard)",
+        print(json.dumps({"error": "one GPU only: the decode path runs on a single GPU; sharding it "
+                          "(by sequence, by group with the positional keys replicated, or by "
+                          "context with gva_combine merging the shards) is not built",
                           "n_gpus": args.gpus}))
         sys.exit(2)
     if not torch.cuda.is_available():
