@@ -376,7 +376,7 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
  * and absorb it in the attention kernel (the fused path), 0 if one
  * gva_absorb_query call ahead of it costs less.  The fused path pays for an
  * absorption in every workgroup; it wins while all B * G * splits
- * workgroups (fixed chunks: splits rounded up to 8) are resident at once,
+ * workgroups (fixed chunks: B * splits rounded up to 8, times G) are resident at once,
  * two per CU on a device with n_cu compute units (0 = ask the current
  * device).  Returns 0 for invalid dims.  Pure host code; enqueues nothing.
  */

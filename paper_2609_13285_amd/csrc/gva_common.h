@@ -177,11 +177,10 @@ __device__ __forceinline__ int xcd_remap(int x, int n) {
 // Workgroup -> (sequence b, split s, group g).  The G groups of one
 // (b, s) always land on one XCD, next to each other.
 //  - Even splits: XCD-contiguous items (xcd_remap), B * S * G workgroups.
-//  - Fixed chunks: chunk s of sequence b goes to XCD (b + s) mod 8, so every
-//    sequence's chunks are dealt over all XCDs and short sequences spread
-//    by b: the XCDs get near-equal shares of a ragged batch.  The grid is
-//    B * S8 * G with S8 = S rounded up to 8; workgroups whose s >= S are
-//    padding and return false.
+//  - Fixed chunks (see chunk_item): the (b, s) slots in the order full
+//    chunks, then partial chunks, then empty slots, dealt round-robin over
+//    the XCDs; the grid is B * S rounded up to 8, times G, and workgroups
+//    past B * S are padding and return false.
 // Every scalar argument the decode prologue needs, requested here in one
 // round trip: left to itself the compiler fetches them where first used,
 // several dependent kernel-argument round trips deep.  The memory clobber
@@ -195,20 +194,92 @@ __device__ __forceinline__ void request_args(const DecodeArgs& a) {
                : "memory");
 }
 
-// Both orders are computed and one is selected, so no branch waits on the
-// split mode before the other kernel arguments are requested.
-__device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g) {
-  const int x = blockIdx.x, xcd = x & 7, slot = x >> 3;
-  const int gc = slot % p.G, t = slot / p.G;
-  const int bc = t % p.B;
-  const int sc = 8 * (t / p.B) + ((xcd - (bc & 7)) & 7);
+// Fixed-chunk split sizes of sequence bb (0 past the batch): nfull splits
+// of at least c rows, npart (0 or 1) shorter one after them; the other
+// S - nfull - npart splits are empty.
+__device__ __forceinline__ void chunk_counts(const DecodeArgs& p, int bb, int& nfull, int& npart) {
+  int L = bb < p.B ? p.lens[bb] : 0;
+  L = L < 0 ? 0 : (L > p.t_max ? p.t_max : L);
+  const int q = L / p.split_rows;
+  nfull = q < p.S ? q : p.S;
+  npart = (q < p.S && L > q * p.split_rows) ? 1 : 0;
+}
+
+__device__ __forceinline__ int wave_sum_int(int v) {
+#pragma unroll
+  for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, 64);
+  return v;
+}
+
+__device__ __forceinline__ int wave_incl_scan(int v) {
+  const int lane = threadIdx.x & 63;
+#pragma unroll
+  for (int o = 1; o < 64; o <<= 1) {
+    const int u = __shfl_up(v, o, 64);
+    if (lane >= o) v += u;
+  }
+  return v;
+}
+
+// Fixed chunks: slot i of the B * S (sequence, split) slots.  Slots are
+// numbered full chunks first (sequence-major), then the partial chunks,
+// then the empty splits, so the dispatcher hands out every chunk with rows
+// before any workgroup that only records an empty split, and the longer
+// chunks before the shorter ones.  Every wave of the workgroup reads the
+// lengths (64 at a time) and finds the same (b, s); the map is a
+// bijection of [0, B S) onto the slots.  empty: the slot has no rows.
+__device__ __forceinline__ void chunk_item(const DecodeArgs& p, int i, int& b, int& s, bool& empty) {
+  const int lane = threadIdx.x & 63;
+  const int nchunks = (p.B + 63) >> 6;
+  int nf0, np0;
+  chunk_counts(p, lane, nf0, np0);
+  int F = wave_sum_int(nf0), P = wave_sum_int(np0);
+  for (int c = 1; c < nchunks; ++c) {
+    int nf, np;
+    chunk_counts(p, 64 * c + lane, nf, np);
+    F += wave_sum_int(nf);
+    P += wave_sum_int(np);
+  }
+  const int cat = i < F ? 0 : (i < F + P ? 1 : 2);
+  const int k = cat == 0 ? i : (cat == 1 ? i - F : i - F - P);
+  int base = 0;
+  b = 0;
+  s = 0;
+  for (int c = 0; c < nchunks; ++c) {
+    int nf = nf0, np = np0;
+    if (c > 0) chunk_counts(p, 64 * c + lane, nf, np);
+    const int cnt = cat == 0 ? nf : (cat == 1 ? np : (64 * c + lane < p.B ? p.S - nf - np : 0));
+    const int incl = base + wave_incl_scan(cnt);
+    const int j = __popcll(__ballot(incl <= k));
+    if (j < 64) {
+      const int excl = __shfl(incl - cnt, j, 64);
+      const int nfj = __shfl(nf, j, 64), npj = __shfl(np, j, 64);
+      b = __builtin_amdgcn_readfirstlane(64 * c + j);
+      s = __builtin_amdgcn_readfirstlane(cat == 0 ? k - excl : (cat == 1 ? nfj : nfj + npj + k - excl));
+      break;
+    }
+    base = __shfl(incl, 63, 64);
+  }
+  empty = cat == 2;
+}
+
+__device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g, bool& empty) {
+  const int x = blockIdx.x;
+  empty = false;
+  if (p.split_rows > 0) {
+    const int slot = x >> 3;
+    g = slot % p.G;
+    const int i = 8 * (slot / p.G) + (x & 7);
+    if (i >= p.B * p.S) return false;
+    chunk_item(p, i, b, s, empty);
+    return true;
+  }
   const int item = xcd_remap(x, gridDim.x);
-  const int ge = item % p.G, bs = item / p.G;
-  const bool chunked = p.split_rows > 0;
-  g = chunked ? gc : ge;
-  b = chunked ? bc : bs / p.S;
-  s = chunked ? sc : bs % p.S;
-  return !chunked || sc < p.S;
+  g = item % p.G;
+  const int bs = item / p.G;
+  b = bs / p.S;
+  s = bs % p.S;
+  return true;
 }
 
 __device__ __forceinline__ float wave_max(float v) {
@@ -397,8 +468,8 @@ inline float scale_log2(const gva_dims* d) {
 
 // Workgroups of a decode launch (see work_item).
 inline long long decode_grid(const gva_dims* d, int num_splits, int split_rows) {
-  const long long s = split_rows > 0 ? ((num_splits + 7LL) & ~7LL) : num_splits;
-  return (long long)d->batch * d->n_groups * s;
+  const long long slots = (long long)d->batch * num_splits;
+  return d->n_groups * (split_rows > 0 ? (slots + 7LL) & ~7LL : slots);
 }
 
 inline int launch_status() {

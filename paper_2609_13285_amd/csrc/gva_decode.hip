@@ -276,7 +276,8 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
   int b, s, g;
-  if (!work_item(a, b, s, g)) return;          // grid padding (fixed chunks)
+  bool empty_slot;
+  if (!work_item(a, b, s, g, empty_slot)) return;   // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform (SGPR)
   const int n = lane & 15, qd = lane >> 4;     // MFMA column / row slot and 16-lane row
@@ -304,16 +305,9 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   auto write_empty = [&]() {                   // an empty split past the first: lse only
     if (tid < HPG) a.lse_part[((int64_t)b * a.H + h0 + tid) * a.S + s] = -INFINITY;
   };
-  if (a.split_rows > 0 && s > 0) {
-    // Fixed chunks of a ragged batch leave many splits empty: those return
-    // before any load.  (A volatile load of its own, so the compiler cannot
-    // merge it with the length used below and wait for that one up here.)
-    const int lc = __builtin_amdgcn_readfirstlane(*reinterpret_cast<const volatile int32_t*>(a.lens + b));
-    const int Lc = lc < 0 ? 0 : (lc > a.t_max ? a.t_max : lc);
-    if ((long long)a.split_rows * s >= Lc) {
-      write_empty();
-      return;
-    }
+  if (empty_slot && s > 0) {                   // fixed chunks: a split with no rows
+    write_empty();
+    return;
   }
 
   // ---- loads that do not depend on the length, oldest first: the current
@@ -832,7 +826,8 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
   __shared__ float red_o[kWaves][kF32MaxHpg][kF32MaxDv];
 
   int b, s, g;
-  if (!work_item(p.a, b, s, g)) return;          // grid padding (fixed chunks)
+  bool empty_slot;
+  if (!work_item(p.a, b, s, g, empty_slot)) return;   // grid padding (fixed chunks)
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int hpg = p.a.H / p.a.G, h0 = g * hpg;
   const int DV = p.a.d_v, DR = p.a.d_r;
@@ -1522,10 +1517,15 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
   const bool spread = 2 * total_len < (long long)dims->batch * max_len;
   if (spread && split_rows != nullptr) {
     // Ragged lengths: fixed chunks, so every workgroup streams about the
-    // same bytes whatever its sequence's length.  About kChunkItemsPerCu
-    // chunks per CU, none shorter than kMinChunkBytes of value rows.
+    // same bytes whatever its sequence's length.  Chunks with rows number
+    // at most stream_rows / c + streams (one partial chunk per stream);
+    // c is chosen so that they fit the kChunkItemsPerCu resident
+    // workgroups per CU, one dispatch round with no tail, when the streams
+    // leave room for that; none shorter than kMinChunkBytes of value rows.
     const long long stream_rows = total_len * dims->n_groups;
-    long long c = (stream_rows + kChunkItemsPerCu * n_cu - 1) / (kChunkItemsPerCu * n_cu);
+    const long long slots = kChunkItemsPerCu * n_cu;
+    const long long room = slots - streams > slots / 2 ? slots - streams : slots / 2;
+    long long c = (stream_rows + room - 1) / room;
     const long long min_rows = (kMinChunkBytes + row_bytes - 1) / row_bytes;
     if (c < min_rows) c = min_rows;
     c = (c + kTileRows - 1) / kTileRows * kTileRows;

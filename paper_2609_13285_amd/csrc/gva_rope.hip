@@ -54,7 +54,8 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
   __shared__ __attribute__((aligned(16))) double freq[DC / 2];
 
   int b, s, g;
-  if (!work_item(a, b, s, g)) return;
+  bool empty_slot;
+  if (!work_item(a, b, s, g, empty_slot)) return;
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int n = lane & 15, qd = lane >> 4;

@@ -159,9 +159,13 @@ def test_pick_splits_fixed_chunks_for_ragged_lengths():
     S, rows = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256)
     assert rows > 0 and rows % 32 == 0
     assert S == -(-32768 // rows) and S <= gva.GVA_MAX_SPLITS  # every row of the longest covered
-    # chunks of about two per CU, none under 128 KiB of value rows
+    # none under 128 KiB of value rows; the chunks with rows (at most one
+    # partial chunk per stream) fit two resident workgroups per CU, with
+    # the shortest chunk that does
     assert rows * 128 * 2 >= 128 << 10
-    assert rows <= 2 * (64 * 6000 * 2) // (2 * 256) + 32
+    stream_rows, streams = 64 * 6000 * 2, 64 * 2
+    assert -(-stream_rows // rows) + streams <= 2 * 256
+    assert rows - 32 < -(-stream_rows // (2 * 256 - streams))
     # uniform lengths keep even splits
     assert gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)[1] == 0
     # a very long, very ragged batch stays within GVA_MAX_SPLITS

@@ -509,6 +509,48 @@ def test_fixed_chunks_with_current_row():
         assert torch.equal(gva.untiled(dev["kr"].cpu()).view(torch.int16), k_ref.view(torch.int16))
 
 
+@pytest.mark.parametrize("fused", [True, False])
+def test_fixed_chunk_slots_large_batch(fused):
+    # fixed chunks over more than 64 sequences (the slot map reads the
+    # lengths 64 at a time) and B * S not a multiple of 8 (padding
+    # workgroups): every (b, h, s) partial is written exactly as the oracle's
+    # split says, the buffers having been filled with NaN first
+    w = gva_inputs.Workload("chunks_b150", 150, 512, 8, 2, 128, 64, 16)
+    g = torch.Generator().manual_seed(31)
+    lens = torch.randint(0, w.t_max + 1, (w.batch,), generator=g, dtype=torch.int32)
+    lens[::7] = 0
+    lens[1::11] = w.t_max
+    lens[2::13] = 1
+    lens[3::17] = 64
+    inp = gva_inputs.make_inputs(w, 33, lens=lens)
+    d = dims_of(w)
+    dev = upload(inp)
+    q_abs = q_rot = None
+    if not fused:
+        q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+        q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+        gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot)
+    for S, rows in ((9, 64), (3, 128), (5, 32)):
+        assert (w.batch * S) % 8 != 0
+        note(f"chunks B150 fused={fused} S={S} split_rows={rows}")
+        o_part = torch.full((w.batch, w.n_heads, S, w.d_v), math.nan, device="cuda")
+        lse_part = torch.full((w.batch, w.n_heads, S), math.nan, device="cuda")
+        gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, o_part, lse_part,
+                                 q=dev["q"] if fused else None, m=dev["m"] if fused else None,
+                                 q_abs=q_abs, q_rot=q_rot, split_rows=rows)
+        torch.cuda.synchronize()
+        o_part, lse_part = o_part.cpu(), lse_part.cpu()
+        begins, ends = oracle.split_bounds(inp["lens"], S, split_rows=rows)
+        for s in range(S):
+            o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
+                                           t_begin=begins[s], t_end=ends[s])
+            assert not torch.isnan(lse_part[:, :, s]).any(), (S, rows, s, "lse not written")
+            assert lse_err(lse_part[:, :, s], lse_ref) <= 1e-3, (S, rows, s)
+            live = (ends[s] > begins[s]) | (s == 0)
+            err = max_abs(o_part[live][:, :, s], o_ref[live])
+            assert err <= QUALITY["bf16"], (S, rows, s, err)
+
+
 def test_combine_never_reads_empty_partials():
     # partials of empty splits hold NaN: a combine that read them would
     # return NaN
