@@ -564,6 +564,9 @@ def main():
     kt = sorted(a.elapsed_time(b) for a, b in evs)
     decode_ms = sum(kt) / len(kt)
     achievable, probe_wg = gva.probe_read_bandwidth(stream=stream)
+    # a plain streaming read of the launch's algorithmic bytes, rotating over
+    # as many buffers as the caches: the same start-up and tail, no compute
+    same_ms, same_wg = gva.probe_read_time(dec_b, copies=n_copies, stream=stream)
 
     step_b = traffic.step_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
                                 appended_rows=w.batch)
@@ -607,6 +610,10 @@ def main():
             "achievable_read_GBps": round(achievable, 1),
             "frac_of_achievable": round(achieved / achievable, 4),
             "achievable_probe": f"gva_probe_read, 2 GiB, {probe_wg} workgroups",
+            "same_bytes_read_ms": round(same_ms, 5),
+            "frac_of_same_bytes_read": round(same_ms / decode_ms, 4),
+            "same_bytes_probe": f"gva_probe_read over the launch's algorithmic bytes, {n_copies} buffers "
+                                f"in rotation, {same_wg} workgroups, mean of 50 launches",
         },
         "cpu_baseline": None,
     }

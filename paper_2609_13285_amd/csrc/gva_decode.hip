@@ -219,6 +219,52 @@ __global__ void __launch_bounds__(kThreads) absorb_bf16_kernel(AbsorbParams p) {
 }
 
 // fp32 storage, vector ALUs: one workgroup per (b, h).
+// sum_k x[k] y[k] over fp32 rows of n.  Rows that are 16-byte aligned with
+// n a multiple of 4 are read as 16-byte pieces, eight of each row requested
+// per step (32 terms per memory round trip); any others element by element,
+// eight per step.
+__device__ __forceinline__ float dot_f32(const float* x, const float* y, int n) {
+  if ((((uintptr_t)x | (uintptr_t)y) & 15) == 0 && (n & 3) == 0) {
+    const f32x4* x4 = reinterpret_cast<const f32x4*>(x);
+    const f32x4* y4 = reinterpret_cast<const f32x4*>(y);
+    const int n4 = n >> 2;
+    f32x4 a4 = {0.f, 0.f, 0.f, 0.f};
+    int k = 0;
+    for (; k + 8 <= n4; k += 8) {
+      f32x4 xv[8], yv[8];
+#pragma unroll
+      for (int j = 0; j < 8; ++j) {
+        xv[j] = x4[k + j];
+        yv[j] = y4[k + j];
+      }
+#pragma unroll
+      for (int j = 0; j < 8; ++j)
+#pragma unroll
+        for (int e = 0; e < 4; ++e) a4[e] = fmaf(xv[j][e], yv[j][e], a4[e]);
+    }
+    for (; k < n4; ++k) {
+      const f32x4 xv = x4[k], yv = y4[k];
+#pragma unroll
+      for (int e = 0; e < 4; ++e) a4[e] = fmaf(xv[e], yv[e], a4[e]);
+    }
+    return (a4[0] + a4[1]) + (a4[2] + a4[3]);
+  }
+  float acc8[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+  int k = 0;
+  for (; k + 8 <= n; k += 8) {
+    float xv[8], yv[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+      xv[j] = x[k + j];
+      yv[j] = y[k + j];
+    }
+#pragma unroll
+    for (int j = 0; j < 8; ++j) acc8[j] = fmaf(xv[j], yv[j], acc8[j]);
+  }
+  for (; k < n; ++k) acc8[0] = fmaf(x[k], y[k], acc8[0]);
+  return ((acc8[0] + acc8[1]) + (acc8[2] + acc8[3])) + ((acc8[4] + acc8[5]) + (acc8[6] + acc8[7]));
+}
+
 __global__ void __launch_bounds__(128) absorb_f32_kernel(AbsorbParams p) {
   const int bh = blockIdx.x;
   const int b = bh / p.H, h = bh % p.H;
@@ -226,9 +272,7 @@ __global__ void __launch_bounds__(128) absorb_f32_kernel(AbsorbParams p) {
   const float* q = static_cast<const float*>(p.q) + (int64_t)bh * W;
   const float* m = static_cast<const float*>(p.m) + (int64_t)h * p.d_v * p.d_c;
   for (int i = threadIdx.x; i < p.d_v; i += blockDim.x) {
-    float acc = 0.f;
-    for (int k = 0; k < p.d_c; ++k) acc = fmaf(q[k], m[(int64_t)i * p.d_c + k], acc);
-    p.q_abs[(int64_t)bh * p.d_v + i] = acc;
+    p.q_abs[(int64_t)bh * p.d_v + i] = dot_f32(q, m + (int64_t)i * p.d_c, p.d_c);
   }
   const int pos = query_pos(p, b);
   for (int i = threadIdx.x; i < p.d_r / 2; i += blockDim.x) {
@@ -849,8 +893,7 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
       const int hl = idx / DV, i = idx % DV;
       const float* qrow = qg + ((int64_t)b * p.a.H + h0 + hl) * W;
       const float* mrow = mg + ((int64_t)(h0 + hl) * DV + i) * p.a.d_c;
-      float a = 0.f;
-      for (int k = 0; k < p.a.d_c; ++k) a = fmaf(qrow[k], mrow[k], a);
+      const float a = dot_f32(qrow, mrow, p.a.d_c);
       qs[hl][i] = a * p.a.scale_log2;
     }
     const int L1 = L > 0 ? L - 1 : 0;
@@ -897,17 +940,44 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 #pragma unroll
       for (int h = 0; h < kF32MaxHpg; ++h) sc[h] = 0.f;
       if (valid) {
-        for (int i = 0; i < DV; ++i) {
-          const float v = vb[tiled_off<float>(t, i, DV)];
+        // the row's 16-byte pieces (4 floats each, contiguous in the tiled
+        // layout), eight requested per step
+        const float* vrow = vb + tiled_off<float>(t, 0, DV);
+        const int npc = DV / 4;
+        for (int pc0 = 0; pc0 < npc; pc0 += 8) {
+          f32x4 vv[8];
 #pragma unroll
-          for (int h = 0; h < kF32MaxHpg; ++h)
-            if (h < hpg) sc[h] = fmaf(qs[h][i], v, sc[h]);
+          for (int u = 0; u < 8; ++u)
+            vv[u] = pc0 + u < npc ? *reinterpret_cast<const f32x4*>(vrow + (int64_t)(pc0 + u) * 4 * kLayoutRows)
+                                  : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (pc0 + u >= npc) break;
+#pragma unroll
+            for (int e = 0; e < 4; ++e) {
+              const int i = 4 * (pc0 + u) + e;
+#pragma unroll
+              for (int h = 0; h < kF32MaxHpg; ++h)
+                if (h < hpg) sc[h] = fmaf(qs[h][i], vv[u][e], sc[h]);
+            }
+          }
         }
-        for (int j = 0; j < DR; ++j) {
-          const float k = kb[tiled_off<float>(t, j, DR)];
+        const float* krow = kb + tiled_off<float>(t, 0, DR);
+        for (int pc0 = 0; pc0 < DR / 4; pc0 += 8) {
+          f32x4 kv[8];
 #pragma unroll
-          for (int h = 0; h < kF32MaxHpg; ++h)
-            if (h < hpg) sc[h] = fmaf(qr[h][j], k, sc[h]);
+          for (int u = 0; u < 8; ++u)
+            kv[u] = pc0 + u < DR / 4 ? *reinterpret_cast<const f32x4*>(krow + (int64_t)(pc0 + u) * 4 * kLayoutRows)
+                                     : f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            if (pc0 + u >= DR / 4) break;
+#pragma unroll
+            for (int e = 0; e < 4; ++e)
+#pragma unroll
+              for (int h = 0; h < kF32MaxHpg; ++h)
+                if (h < hpg) sc[h] = fmaf(qr[h][4 * (pc0 + u) + e], kv[u][e], sc[h]);
+          }
         }
       }
 #pragma unroll
@@ -929,6 +999,7 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
     __syncthreads();
     if (has) {
       const int nrow = r1 - row0 < 64 ? r1 - row0 : 64;
+#pragma unroll 16
       for (int t = 0; t < nrow; ++t) {
 #pragma unroll
         for (int u = 0; u < 4; ++u) {

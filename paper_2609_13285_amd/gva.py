@@ -10,6 +10,7 @@ missing, the first call raises.
 from __future__ import annotations
 
 import ctypes
+import math
 import os
 from typing import Optional, Tuple
 
@@ -561,6 +562,37 @@ def probe_read_bandwidth(nbytes: int = 2 << 30, reps: int = 10, stream=None) -> 
         if gbs > best[0]:
             best = (gbs, wg)
     del buf
+    return best
+
+
+def probe_read_time(nbytes: int, copies: int = 2, reps: int = 50, stream=None) -> Tuple[float, int]:
+    """Mean duration (ms) of one gva_probe_read launch over ``nbytes``, each
+    launch reading the next of ``copies`` buffers (whose total can then
+    exceed the 256 MB last-level cache), timed with events around every
+    launch; the best of a few workgroup counts.  Returns (ms, workgroups)."""
+    nbytes = (int(nbytes) + 15) // 16 * 16
+    bufs = [torch.ones(nbytes // 4, dtype=torch.int32, device="cuda") for _ in range(max(1, int(copies)))]
+    sink = torch.zeros(1, dtype=torch.int32, device="cuda")
+    st = _stream(stream)
+    ev_stream = stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.current_stream()
+    n_cu = torch.cuda.get_device_properties(bufs[0].device).multi_processor_count
+    best = (math.inf, 0)
+    for per_cu in (1, 2, 4):
+        wg = per_cu * n_cu
+        launch = lambda i: _check("gva_probe_read", lib().gva_probe_read(
+            ctypes.c_void_p(bufs[i % len(bufs)].data_ptr()), nbytes, wg, ctypes.c_void_p(sink.data_ptr()), st))
+        for i in range(5):
+            launch(i)
+        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
+        for i, (a, b) in enumerate(evs):
+            a.record(ev_stream)
+            launch(i)
+            b.record(ev_stream)
+        torch.cuda.synchronize()
+        ms = sum(a.elapsed_time(b) for a, b in evs) / reps
+        if ms < best[0]:
+            best = (ms, wg)
+    del bufs
     return best
 
 

@@ -98,6 +98,23 @@ def test_random_shapes_sweep():
         _check(w, o, lse, o_ref, lse_ref, label)
 
 
+@pytest.mark.parametrize("fused", [True, False])
+def test_f32_query_rows_not_16_byte_aligned(fused):
+    # fp32 storage takes any d_c: with d_c + d_r odd the query rows are not
+    # 16-byte aligned and the absorption reads them element by element
+    for dc, dr in ((37, 8), (64, 4), (5, 0)):
+        w = gva_inputs.Workload("f32_odd", 3, 96, 8, 2, 64, dc, dr, dtype="f32")
+        lens = torch.tensor([96, 41, 1], dtype=torch.int32)
+        inp = gva_inputs.make_inputs(w, 61, lens=lens)
+        o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
+                                       rope_base=w.rope_base)
+        for S in (1, 2):
+            label = f"f32 dc{dc} dr{dr} fused={fused} S{S}"
+            note(label)
+            o, lse, _, _ = run_decode(w, upload(inp), S, fused=fused)
+            _check(w, o, lse, o_ref, lse_ref, label)
+
+
 # ------------------------------------------------------------------ shapes
 SHAPES = [
     # (H, G, d_v, d_c, d_r)
