@@ -293,7 +293,7 @@ struct DecodeCfg {
   static constexpr int DEPTH = DV >= 128 ? 2 : 3;
   // fused absorption: 16-byte pieces of M_h per lane and load round, one
   // round of 32 where the registers allow it (no spills), else rounds of 16
-  static constexpr int AR = (DV >= 128 && NRC < 2 && HPG <= 4) ? 32 : 16;
+  static constexpr int AR = (DV >= 128 && NRC < 2) ? 32 : 16;
   static constexpr int QS_STRIDE = DV + 4;                   // padded LDS rows (floats)
   static constexpr int QR_STRIDE = 32 * NRC + 4;
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
