@@ -95,8 +95,8 @@ def write_traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, workload
     by what the same counter reads for a plain device copy of known size."""
     def pick(means, key):
         hits = [v for k, v in means.items() if key in k]
-        if not hits:
-            raise SystemExit(f"no {key} dispatch in the counter file")
+        if len(hits) != 1:
+            raise SystemExit(f"{len(hits)} kernels named like {key} in the counter file (need one)")
         return hits[0]
     copy_bytes = copy_mb * (1 << 20)
     f_copy = pick(_pmc_means(copy_fetch_csv, "FETCH_SIZE"), "copyBuffer")
