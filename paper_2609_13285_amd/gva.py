@@ -568,8 +568,9 @@ def probe_read_bandwidth(nbytes: int = 2 << 30, reps: int = 10, stream=None) -> 
 def probe_read_time(nbytes: int, copies: int = 2, reps: int = 50, stream=None) -> Tuple[float, int]:
     """Mean duration (ms) of one gva_probe_read launch over ``nbytes``, each
     launch reading the next of ``copies`` buffers (whose total can then
-    exceed the 256 MB last-level cache), timed with events around every
-    launch; the best of a few workgroup counts.  Returns (ms, workgroups)."""
+    exceed the 256 MB last-level cache), ``reps`` launches back to back
+    between two events; the best of a few workgroup counts.  Returns
+    (ms, workgroups)."""
     nbytes = (int(nbytes) + 15) // 16 * 16
     bufs = [torch.ones(nbytes // 4, dtype=torch.int32, device="cuda") for _ in range(max(1, int(copies)))]
     sink = torch.zeros(1, dtype=torch.int32, device="cuda")
@@ -583,13 +584,14 @@ def probe_read_time(nbytes: int, copies: int = 2, reps: int = 50, stream=None) -
             ctypes.c_void_p(bufs[i % len(bufs)].data_ptr()), nbytes, wg, ctypes.c_void_p(sink.data_ptr()), st))
         for i in range(5):
             launch(i)
-        evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(reps)]
-        for i, (a, b) in enumerate(evs):
-            a.record(ev_stream)
-            launch(i)
-            b.record(ev_stream)
+        a, b = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
         torch.cuda.synchronize()
-        ms = sum(a.elapsed_time(b) for a, b in evs) / reps
+        a.record(ev_stream)
+        for i in range(reps):
+            launch(i)
+        b.record(ev_stream)
+        torch.cuda.synchronize()
+        ms = a.elapsed_time(b) / reps
         if ms < best[0]:
             best = (ms, wg)
     del bufs
