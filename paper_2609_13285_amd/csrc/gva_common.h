@@ -225,40 +225,58 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
 // numbered full chunks first (sequence-major), then the partial chunks,
 // then the empty splits, so the dispatcher hands out every chunk with rows
 // before any workgroup that only records an empty split, and the longer
-// chunks before the shorter ones.  Every wave of the workgroup reads the
-// lengths (64 at a time) and finds the same (b, s); the map is a
-// bijection of [0, B S) onto the slots.  empty: the slot has no rows.
+// chunks before the shorter ones.  The map is a bijection of [0, B S) onto
+// the slots, found by every wave of the workgroup from the lengths in two
+// levels: lane l first sums the counts of the k = ceil(B / 64) sequences
+// [l k, l k + k) (independent loads), a scan over the lanes finds the block
+// holding slot i, and for k > 1 a second scan over that block's sequences
+// (64 at a time) finds the sequence.  empty: the slot has no rows.
 __device__ __forceinline__ void chunk_item(const DecodeArgs& p, int i, int& b, int& s, bool& empty) {
   const int lane = threadIdx.x & 63;
-  const int nchunks = (p.B + 63) >> 6;
-  int nf0, np0;
-  chunk_counts(p, lane, nf0, np0);
-  int F = wave_sum_int(nf0), P = wave_sum_int(np0);
-  for (int c = 1; c < nchunks; ++c) {
+  const int k = (p.B + 63) >> 6;
+  int nf_sum = 0, np_sum = 0, nb = 0;
+#pragma unroll 4
+  for (int j = 0; j < k; ++j) {
     int nf, np;
-    chunk_counts(p, 64 * c + lane, nf, np);
-    F += wave_sum_int(nf);
-    P += wave_sum_int(np);
+    chunk_counts(p, lane * k + j, nf, np);
+    nf_sum += nf;
+    np_sum += np;
+    nb += lane * k + j < p.B ? 1 : 0;
   }
+  const int F = wave_sum_int(nf_sum), P = wave_sum_int(np_sum);
   const int cat = i < F ? 0 : (i < F + P ? 1 : 2);
-  const int k = cat == 0 ? i : (cat == 1 ? i - F : i - F - P);
-  int base = 0;
+  const int kk = cat == 0 ? i : (cat == 1 ? i - F : i - F - P);
+  auto pick = [&](int nf, int np, int valid) { return cat == 0 ? nf : (cat == 1 ? np : valid * p.S - nf - np); };
+  const int cnt1 = pick(nf_sum, np_sum, nb);
+  const int incl1 = wave_incl_scan(cnt1);
+  const int j1 = min(__popcll(__ballot(incl1 <= kk)), 63);   // < 64 whenever i < B S
+  int base = __shfl(incl1 - cnt1, j1, 64);
+  // the slot's position within its sequence: full chunk (k - excl), the
+  // partial chunk (after the nf full ones), or an empty split after both
+  auto split_of = [&](int nf, int np, int local) { return cat == 0 ? local : (cat == 1 ? nf : nf + np + local); };
   b = 0;
   s = 0;
-  for (int c = 0; c < nchunks; ++c) {
-    int nf = nf0, np = np0;
-    if (c > 0) chunk_counts(p, 64 * c + lane, nf, np);
-    const int cnt = cat == 0 ? nf : (cat == 1 ? np : (64 * c + lane < p.B ? p.S - nf - np : 0));
-    const int incl = base + wave_incl_scan(cnt);
-    const int j = __popcll(__ballot(incl <= k));
-    if (j < 64) {
-      const int excl = __shfl(incl - cnt, j, 64);
-      const int nfj = __shfl(nf, j, 64), npj = __shfl(np, j, 64);
-      b = __builtin_amdgcn_readfirstlane(64 * c + j);
-      s = __builtin_amdgcn_readfirstlane(cat == 0 ? k - excl : (cat == 1 ? nfj : nfj + npj + k - excl));
-      break;
+  if (k == 1) {                                // one sequence per lane: found
+    b = __builtin_amdgcn_readfirstlane(j1);
+    s = __builtin_amdgcn_readfirstlane(split_of(__shfl(nf_sum, j1, 64), __shfl(np_sum, j1, 64), kk - base));
+  } else {
+    const int first = j1 * k;
+    for (int c = 0; c < k; c += 64) {
+      const int bb = first + c + lane;
+      const bool in_blk = c + lane < k && bb < p.B;
+      int nf, np;
+      chunk_counts(p, in_blk ? bb : p.B, nf, np);
+      const int cnt = in_blk ? pick(nf, np, 1) : 0;
+      const int incl = base + wave_incl_scan(cnt);
+      const int j = __popcll(__ballot(incl <= kk));
+      if (j < 64) {
+        const int excl = __shfl(incl - cnt, j, 64);
+        b = __builtin_amdgcn_readfirstlane(first + c + j);
+        s = __builtin_amdgcn_readfirstlane(split_of(__shfl(nf, j, 64), __shfl(np, j, 64), kk - excl));
+        break;
+      }
+      base = __shfl(incl, 63, 64);
     }
-    base = __shfl(incl, 63, 64);
   }
   empty = cat == 2;
 }

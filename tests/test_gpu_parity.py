@@ -526,13 +526,24 @@ def test_fixed_chunks_with_current_row():
         assert torch.equal(gva.untiled(dev["kr"].cpu()).view(torch.int16), k_ref.view(torch.int16))
 
 
+# (batch, capacity, heads, groups, d_v, d_c, d_r, [(splits, split_rows)]): the
+# slot map reads the lengths in blocks of ceil(B / 64) per lane, then (B > 64)
+# scans the block holding the slot 64 sequences at a time; B = 4100 needs two
+# such passes
+LARGE_BATCH_CHUNKS = [
+    (150, 512, 8, 2, 128, 64, 16, [(9, 64), (3, 128), (5, 32)]),
+    (4100, 64, 2, 1, 64, 32, 8, [(3, 32), (1, 32)]),
+]
+
+
 @pytest.mark.parametrize("fused", [True, False])
-def test_fixed_chunk_slots_large_batch(fused):
-    # fixed chunks over more than 64 sequences (the slot map reads the
-    # lengths 64 at a time) and B * S not a multiple of 8 (padding
-    # workgroups): every (b, h, s) partial is written exactly as the oracle's
-    # split says, the buffers having been filled with NaN first
-    w = gva_inputs.Workload("chunks_b150", 150, 512, 8, 2, 128, 64, 16)
+@pytest.mark.parametrize("cfg", LARGE_BATCH_CHUNKS, ids=lambda c: f"B{c[0]}")
+def test_fixed_chunk_slots_large_batch(cfg, fused):
+    # fixed chunks over more than 64 sequences and B * S not a multiple of 8
+    # (padding workgroups): every (b, h, s) partial is written exactly as the
+    # oracle's split says, the buffers having been filled with NaN first
+    B, T, H, G, dv, dc, dr, plans = cfg
+    w = gva_inputs.Workload(f"chunks_b{B}", B, T, H, G, dv, dc, dr)
     g = torch.Generator().manual_seed(31)
     lens = torch.randint(0, w.t_max + 1, (w.batch,), generator=g, dtype=torch.int32)
     lens[::7] = 0
@@ -547,9 +558,9 @@ def test_fixed_chunk_slots_large_batch(fused):
         q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
         q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
         gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot)
-    for S, rows in ((9, 64), (3, 128), (5, 32)):
+    for S, rows in plans:
         assert (w.batch * S) % 8 != 0
-        note(f"chunks B150 fused={fused} S={S} split_rows={rows}")
+        note(f"chunks B{B} fused={fused} S={S} split_rows={rows}")
         o_part = torch.full((w.batch, w.n_heads, S, w.d_v), math.nan, device="cuda")
         lse_part = torch.full((w.batch, w.n_heads, S), math.nan, device="cuda")
         gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, o_part, lse_part,
