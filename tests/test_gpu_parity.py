@@ -822,11 +822,12 @@ def test_rope_decode_full_size_sampled():
 
 
 # ------------------------------------------------------- prefill (causal)
-# The prefill kernel feeds the matrix cores bf16 queries and bf16 softmax
-# weights (single, not high+low): a relative rounding of up to 2^-9 on each
-# weight moves o by at most 2^-9 max|v| (~8e-3 for N(0, 1) values, whose
-# maximum over these caches is ~4); q~ in bf16 moves a base-2 logit by
-# ~1e-3 rms.  Observed: a few 1e-3 where few rows are seen.
+# The prefill kernel feeds the matrix cores bf16 queries (single, not
+# high+low) and fp16 softmax weights: q~ in bf16 moves a base-2 logit by up
+# to 2^-9 of its size (~1e-3 rms here), which moves o by about that much
+# times the spread of the values (N(0, 1), maximum ~4 over these caches);
+# the weights' relative rounding of 2^-11 adds ~2e-3 at most.  Observed: a
+# few 1e-3 where few rows are seen.
 PREFILL_QUALITY = 8e-3
 
 
