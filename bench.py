@@ -255,7 +255,9 @@ def gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches, stream):
     slice, each rotating through its own cache copies; both merge their
     splits with gva_combine."""
     n = len(caches)
-    k_tiled = gva.tiled(inp["k_gqa"])
+    k_gqa = inp["k_gqa"] if "k_gqa" in inp else gva_inputs.gqa_keys(w, args.seed)
+    k_tiled = gva.tiled(k_gqa)
+    del k_gqa
     kcaches = [k_tiled.cuda() for _ in range(n)]
     del k_tiled
     bufs = gva.DecodeBuffers(d, S)
@@ -471,7 +473,7 @@ def main():
     ap.add_argument("--no-rope", action="store_true",
                     help="skip the ordinary-RoPE contrast timing (bf16 workloads)")
     ap.add_argument("--no-gqa", action="store_true",
-                    help="skip the matched-GQA comparison on workloads that carry a GQA key cache")
+                    help="skip the matched-GQA comparison (bf16 workloads; a key cache is drawn for workloads whose inputs carry none)")
     args = ap.parse_args()
     if args.write_traffic:
         write_traffic(*args.write_traffic, args.workload, args.splits or 1, args.copy_mb)
@@ -631,11 +633,11 @@ def main():
     }
 
     o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
-    if paging is not None and (args.layers > 0 or (w.gqa and not args.no_gqa)):
+    if paging is not None and args.layers > 0:
         raise SystemExit("--paged times the decode step only")
     if args.layers > 0:
         out["layer_stack"] = layer_stack(args, w, inp, d, S, split_rows, fused, dec_b)
-    if w.gqa and not args.no_gqa:
+    if w.dtype == "bf16" and not args.no_gqa and paging is None:
         out["gqa_comparison"] = gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches,
                                                stream)
     if w.dtype == "bf16" and not args.no_rope and paging is None:

@@ -136,6 +136,16 @@ def make_inputs(w: Workload, seed: int, lens: Optional[torch.Tensor] = None) -> 
     return out
 
 
+def gqa_keys(w: Workload, seed: int) -> torch.Tensor:
+    """The matched-GQA baseline's explicit key cache, [B, G, T, d_v] in the
+    storage dtype, N(0, 1) like the value cache, from its own generator
+    seeded with ``seed``: for workloads whose draw (make_inputs) has none."""
+    g = torch.Generator(device="cpu")
+    g.manual_seed(int(seed) + 104729)
+    x = torch.randn((w.batch, w.n_groups, w.t_max, w.d_v), generator=g, dtype=torch.float32)
+    return x.to(_torch_dtype(w.dtype))
+
+
 def prefill_queries(w: Workload, seed: int, n_new: int, gqa: bool = False) -> torch.Tensor:
     """A prompt's queries, [B, n_new, H, d_c + d_r] in the storage dtype
     (or, with ``gqa``, the matched-GQA queries [B, n_new, H, d_v] in fp32),

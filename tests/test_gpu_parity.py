@@ -413,7 +413,7 @@ def test_append_and_attend_in_one_launch_full_step():
 
 
 # ------------------------------------------------ matched-GQA baseline kernel
-@pytest.mark.parametrize("hpg,dv", [(1, 64), (2, 128), (4, 64), (8, 128)])
+@pytest.mark.parametrize("hpg,dv", [(1, 64), (2, 128), (4, 64), (4, 128), (8, 128)])
 def test_gqa_baseline_matches_oracle(hpg, dv):
     G = 2
     w = gva_inputs.Workload("gqa", 5, 304, G * hpg, G, dv, dv, 16, dtype="bf16", gqa=True)
