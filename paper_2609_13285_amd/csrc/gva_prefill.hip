@@ -47,10 +47,10 @@ struct PrefillParams {
 constexpr float kLazyMax = 8.f;
 
 // Two workgroups per CU where the registers allow it without spilling.
-constexpr int prefill_min_blocks(int dv, int nrc, bool gqa) { return nrc >= 2 ? 1 : 2; }
+constexpr int prefill_min_blocks(int nrc) { return nrc >= 2 ? 1 : 2; }
 
 template <int HPG, int DV, int NRC, bool GQA>
-__global__ void __launch_bounds__(kThreads, prefill_min_blocks(DV, NRC, GQA)) prefill_bf16_kernel(PrefillParams p) {
+__global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf16_kernel(PrefillParams p) {
   constexpr int COLS = prefill_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = COLS / 16;
   constexpr int QB = COLS / HPG;               // positions per workgroup
   constexpr int DEPTH = 2;
