@@ -168,6 +168,12 @@ def test_pick_splits_fixed_chunks_for_ragged_lengths():
     assert rows - 32 < -(-stream_rows // (2 * 256 - streams))
     # uniform lengths keep even splits
     assert gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)[1] == 0
+    # more streams than half the resident workgroups: chunks sized for about
+    # two per CU over the whole batch (the partial chunks can no longer all fit)
+    d6 = dims(batch=256, n_heads=16, n_groups=2, t_max=32768)
+    S6, rows6 = gva.gva_pick_splits(d6, 32768, 256 * 4000, 256)
+    assert rows6 > 0 and S6 == -(-32768 // rows6)
+    assert rows6 - 32 < -(-(256 * 4000 * 2) // 256) <= rows6
     # a very long, very ragged batch stays within GVA_MAX_SPLITS
     d5 = dims(batch=256, n_heads=8, n_groups=8, t_max=1 << 20, d_v=64)
     S5, rows5 = gva.gva_pick_splits(d5, 1 << 20, 256 * 1000, 256)
