@@ -583,6 +583,85 @@ def test_fixed_chunk_slots_large_batch(cfg, fused):
             assert err <= QUALITY["bf16"], (S, rows, s, err)
 
 
+# ------------------------------------------------- writes stay in bounds
+_GUARD = 4096          # sentinel elements on each side of an output (16 KB of fp32)
+_SENTINEL = 0x7FC0DEAD  # a NaN bit pattern no kernel writes
+
+
+def _guarded(shape):
+    """A contiguous fp32 output with sentinel words before and after it."""
+    n = math.prod(shape)
+    big = torch.empty(n + 2 * _GUARD, dtype=torch.int32, device="cuda").fill_(_SENTINEL)
+    return big, big[_GUARD:_GUARD + n].view(torch.float32).view(shape)
+
+
+def _guards_intact(big):
+    head, tail = big[:_GUARD], big[-_GUARD:]
+    return bool((head == _SENTINEL).all()) and bool((tail == _SENTINEL).all())
+
+
+def test_outputs_written_only_in_bounds():
+    # every output buffer sits between two 16 KB runs of a sentinel; after
+    # absorption, attention (fused and separate, even and fixed-chunk
+    # splits, bf16 and fp32), combine, the GQA baseline, the ordinary-RoPE
+    # contrast and the prefill, the sentinels must be untouched
+    for dtype in ("bf16", "f32"):
+        w = gva_inputs.Workload("guards", 3, 304, 8, 2, 128 if dtype == "bf16" else 64, 64, 16,
+                                dtype=dtype)
+        lens = torch.tensor([300, 1, 97], dtype=torch.int32)
+        inp = gva_inputs.make_inputs(w, 71, lens=lens)
+        d = dims_of(w)
+        dev = upload(inp)
+        B, H, dv, dr = w.batch, w.n_heads, w.d_v, w.d_r
+        bigs = []
+        qa_big, q_abs = _guarded((B, H, dv))
+        qr_big, q_rot = _guarded((B, H, dr))
+        bigs += [qa_big, qr_big]
+        note(f"guards {dtype}: absorb")
+        gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot)
+        for S, rows, fused in ((1, 0, True), (3, 0, False), (10, 32, True), (10, 32, False)):
+            note(f"guards {dtype}: attention S={S} rows={rows} fused={fused}")
+            op_big, o_part = _guarded((B, H, S, dv))
+            lp_big, lse_part = _guarded((B, H, S))
+            kw = dict(q=dev["q"], m=dev["m"]) if fused else dict(q_abs=q_abs, q_rot=q_rot)
+            gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, o_part, lse_part,
+                                     split_rows=rows, **kw)
+            o_big, o = _guarded((B, H, dv))
+            l_big, lse = _guarded((B, H))
+            gva.gva_combine(d, o_part, lse_part, S, o, lse)
+            bigs += [op_big, lp_big, o_big, l_big]
+        torch.cuda.synchronize()
+        if dtype == "bf16":
+            note("guards: GQA baseline and ordinary-RoPE contrast")
+            k_gqa = gva.tiled(gva_inputs.gqa_keys(w, 71)).cuda()
+            q_gqa = torch.randn(B, H, dv, generator=torch.Generator().manual_seed(72)).to(torch.bfloat16).cuda()
+            for S, rows in ((2, 0), (10, 32)):
+                op_big, o_part = _guarded((B, H, S, dv))
+                lp_big, lse_part = _guarded((B, H, S))
+                gva.gva_gqa_decode_attention(d, q_gqa, k_gqa, dev["v"], dev["lens"], S, o_part,
+                                             lse_part, split_rows=rows)
+                bigs += [op_big, lp_big]
+            d0 = gva.make_dims(B, H, w.n_groups, dv, w.d_c, 0, w.t_max, w.dtype, w.rope_base)
+            q0 = dev["q"][..., : w.d_c].contiguous()
+            op_big, o_part = _guarded((B, H, 2, dv))
+            lp_big, lse_part = _guarded((B, H, 2))
+            gva.gva_rope_decode_attention(d0, q0, dev["m"], dev["v"], dev["lens"], 2, o_part, lse_part)
+            bigs += [op_big, lp_big]
+            note("guards: prefill")
+            N = 90
+            qp = gva_inputs.prefill_queries(w, 71, N).cuda()
+            pa_big, pq_abs = _guarded((B, N, H, dv))
+            pr_big, pq_rot = _guarded((B, N, H, dr))
+            gva.gva_prefill_absorb(d, N, qp, dev["m"], dev["lens"], pq_abs, pq_rot)
+            po_big, po = _guarded((B, N, H, dv))
+            pl_big, plse = _guarded((B, N, H))
+            gva.gva_prefill_attention(d, N, pq_abs, pq_rot, dev["v"], dev["kr"], dev["lens"], po, plse)
+            bigs += [pa_big, pr_big, po_big, pl_big]
+        torch.cuda.synchronize()
+        bad = [i for i, big in enumerate(bigs) if not _guards_intact(big)]
+        assert not bad, (dtype, bad)
+
+
 def test_combine_never_reads_empty_partials():
     # partials of empty splits hold NaN: a combine that read them would
     # return NaN
