@@ -195,11 +195,16 @@ def test_split_count_invariance_and_determinism():
     inp = gva_inputs.make_inputs(w, 23)
     dev = upload(inp)
     note("split invariance")
-    outs = {S: run_decode(w, dev, S)[0] for S in (1, 2, 7, 64)}
+    # up to GVA_MAX_SPLITS: 256 even splits of 2048 rows are 64 of 32 rows
+    # and 192 empty ones
+    outs = {S: run_decode(w, dev, S)[0] for S in (1, 2, 7, 64, gva.GVA_MAX_SPLITS)}
+    outs["chunks"] = run_decode(w, dev, 64, split_rows=32)[0]     # 64 fixed chunks of 32 rows
     for S, o in outs.items():
         assert max_abs(o, outs[1]) <= 2 * QUALITY["bf16"], S
     again = run_decode(w, dev, 7)[0]
     assert torch.equal(again, outs[7])          # bitwise deterministic
+    again = run_decode(w, dev, 64, split_rows=32)[0]
+    assert torch.equal(again, outs["chunks"])
 
 
 # ------------------------------------------------- absorb, append, combine
