@@ -493,6 +493,37 @@ def test_gqa_baseline_full_size_sampled(name):
     assert torch.isfinite(o).all()
 
 
+@pytest.mark.slow
+def test_one_gib_value_stream():
+    # a single value stream of 2^22 rows x 128 bf16 = 1 GiB (the layout
+    # allows up to 2 GiB - 16 MiB per stream): the 32-bit buffer offsets
+    # near the top of the stream, one workgroup streaming all of it, even
+    # splits and fixed chunks, a length just short of capacity, and the
+    # current row appended at row 2^22 - 6
+    T = 1 << 22
+    w = gva_inputs.Workload("one_gib", 1, T, 2, 1, 128, 64, 16)
+    lens = torch.tensor([T - 5], dtype=torch.int32)
+    note("one GiB stream: drawing inputs")
+    inp = gva_inputs.make_inputs(w, 81, lens=lens)
+    seq = torch.zeros(1, dtype=torch.int32)
+    pos = (lens - 1).to(torch.int32)
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], seq, pos, w.rope_base)
+    note("one GiB stream: oracle")
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, lens)
+    del v_ref, k_ref
+    d = dims_of(w)
+    for S, rows in ((1, 0), (64, 0), (64, 65536)):
+        note(f"one GiB stream: S={S} split_rows={rows}")
+        dev = upload(inp)
+        o, lse = gva.decode(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S,
+                            v_new=dev["v_new"], kr_new=dev["kr_new"], split_rows=rows)
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"one GiB/S{S}/rows{rows}")
+        del dev
+        torch.cuda.empty_cache()
+
+
 # ------------------------------------------- fixed-chunk splits (ragged batches)
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("fused", [True, False])
