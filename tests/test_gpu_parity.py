@@ -806,6 +806,27 @@ def test_paged_decode_matches_oracle(page_rows):
         _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"paged/{page_rows}/S{S}/rows{rows}/fused={fused}")
 
 
+def test_paged_at_max_pages():
+    # a sequence of GVA_MAX_PAGES = 4096 pages of 32 rows (131,072 rows), in
+    # random pool order with NaN in the unused pages: one split holds all
+    # 4096 page ids in LDS; also 7 even splits and fixed chunks of 4096 rows
+    page_rows = 32
+    w = gva_inputs.Workload("paged_max", 2, gva.GVA_MAX_PAGES * page_rows, 4, 1, 128, 64, 16)
+    lens = torch.tensor([w.t_max - 3, 40000], dtype=torch.int32)
+    inp, d, pg, bt = _paged_setup(w, 43, lens, page_rows)
+    assert pg.max_pages == gva.GVA_MAX_PAGES
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"])
+    vp, kp = gva.to_pages(gva.tiled(inp["v"]), gva.tiled(inp["kr"]), bt, pg, fill=float("nan"))
+    dev = upload({k: inp[k] for k in ("q", "m", "lens")})
+    vp, kp, btd = vp.cuda(), kp.cuda(), bt.cuda()
+    for S, rows, fused in ((1, 0, True), (7, 0, False), (32, 4096, True)):
+        note(f"paged max pages S={S} split_rows={rows} fused={fused}")
+        o, lse = gva.paged_decode(d, pg, dev["q"], dev["m"], vp, kp, btd, dev["lens"], S, fused=fused,
+                                  split_rows=rows)
+        torch.cuda.synchronize()
+        _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"paged max/S{S}/rows{rows}/fused={fused}")
+
+
 def test_paged_append_and_current_row():
     # the paged append and the current row appended in the attention launch
     # write exactly what the contiguous append writes, at the right pages
