@@ -308,7 +308,9 @@ struct DecodeCfg {
 // the two kernels differ only in the bytes they must stream.
 // PAGED reads the caches from page pools through a block table: only the
 // addressing of a tile (and of the current row) changes.
-template <int HPG, int DV, int NRC, bool GQA, bool FUSED, bool PAGED>
+// KR_STREAM loads the positional-key tiles with the non-temporal policy too
+// (decode_kr_stream decides).
+template <int HPG, int DV, int NRC, bool GQA, bool FUSED, bool PAGED, bool KR_STREAM = false>
 __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
   static_assert(!(GQA && FUSED), "the GQA baseline takes the raw query");
   static_assert(!(GQA && PAGED), "the GQA baseline reads contiguous caches");
@@ -519,7 +521,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       const int ksoff = (lt + hf) * k_tile_bytes;
 #pragma unroll
       for (int rc = 0; rc < NRC; ++rc)
-        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(tk, k_lane[rc], ksoff, 0));
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(tk, k_lane[rc], ksoff, KR_STREAM ? kAuxNT : 0));
     }
   };
   TileT buf[DEPTH];
@@ -1205,26 +1207,30 @@ int device_cu_count() {
 using DecodeFn = void (*)(DecodeParams);
 
 template <int HPG, int DV, bool FUSED, bool PAGED>
-DecodeFn pick_nrc(int nrc) {
+DecodeFn pick_nrc(int nrc, bool kr_stream) {
+  // the streaming positional-key variant exists for contiguous caches
+  constexpr bool KRS = !PAGED;
   switch (nrc) {
     case 0: return decode_bf16_kernel<HPG, DV, 0, false, FUSED, PAGED>;
-    case 1: return decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED>;
-    case 2: return decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED>;
+    case 1: return KRS && kr_stream ? decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED, KRS>
+                                    : decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED>;
+    case 2: return KRS && kr_stream ? decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED, KRS>
+                                    : decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED>;
   }
   return nullptr;
 }
 
 template <int HPG, int DV>
-DecodeFn pick_mode(int nrc, bool fused, bool paged) {
-  if (paged) return fused ? pick_nrc<HPG, DV, true, true>(nrc) : pick_nrc<HPG, DV, false, true>(nrc);
-  return fused ? pick_nrc<HPG, DV, true, false>(nrc) : pick_nrc<HPG, DV, false, false>(nrc);
+DecodeFn pick_mode(int nrc, bool fused, bool paged, bool kr_stream) {
+  if (paged) return fused ? pick_nrc<HPG, DV, true, true>(nrc, false) : pick_nrc<HPG, DV, false, true>(nrc, false);
+  return fused ? pick_nrc<HPG, DV, true, false>(nrc, kr_stream) : pick_nrc<HPG, DV, false, false>(nrc, kr_stream);
 }
 
 template <int HPG>
-DecodeFn pick_dv(int dv, int nrc, bool fused, bool paged) {
+DecodeFn pick_dv(int dv, int nrc, bool fused, bool paged, bool kr_stream) {
   switch (dv) {
-    case 64: return pick_mode<HPG, 64>(nrc, fused, paged);
-    case 128: return pick_mode<HPG, 128>(nrc, fused, paged);
+    case 64: return pick_mode<HPG, 64>(nrc, fused, paged, kr_stream);
+    case 128: return pick_mode<HPG, 128>(nrc, fused, paged, kr_stream);
   }
   return nullptr;
 }
@@ -1248,14 +1254,24 @@ DecodeFn pick_gqa_decode(int hpg, int dv) {
   return nullptr;
 }
 
-DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged) {
+DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged, bool kr_stream) {
   switch (hpg) {
-    case 1: return pick_dv<1>(dv, nrc, fused, paged);
-    case 2: return pick_dv<2>(dv, nrc, fused, paged);
-    case 4: return pick_dv<4>(dv, nrc, fused, paged);
-    case 8: return pick_dv<8>(dv, nrc, fused, paged);
+    case 1: return pick_dv<1>(dv, nrc, fused, paged, kr_stream);
+    case 2: return pick_dv<2>(dv, nrc, fused, paged, kr_stream);
+    case 4: return pick_dv<4>(dv, nrc, fused, paged, kr_stream);
+    case 8: return pick_dv<8>(dv, nrc, fused, paged, kr_stream);
   }
   return nullptr;
+}
+
+// The positional-key tiles are read by the G groups of a split through one
+// L2, so they are normally cached.  With at least as many (sequence, group)
+// streams as CUs, every L2 holds many sequences' keys at once and streaming
+// them (non-temporal, like the value tiles) measured faster: B = 32, G = 8
+// on 256 CUs gained 0.7-2.0 us per launch, while four long sequences
+// (32 streams) lost 2.6-3 us.
+bool decode_kr_stream(const gva_dims* d) {
+  return (long long)d->batch * d->n_groups >= device_cu_count();
 }
 
 int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* m, const int32_t* lens,
@@ -1423,7 +1439,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
     if (dims->d_c % 32 != 0 || dims->d_c > 512 || dims->d_r % 8 != 0 || dims->d_r > 64)
       return GVA_ERR_UNSUPPORTED;
     const int nrc = (dims->d_r + 31) / 32;
-    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr);
+    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr, decode_kr_stream(dims));
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
     hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   } else {
