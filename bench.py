@@ -36,13 +36,27 @@ sys.path.insert(0, ROOT)
 import gva_inputs  # noqa: E402
 from paper_2609_13285_amd import gva, traffic  # noqa: E402
 
-METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s, B=32 T=8K bf16"
+METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD's published figure
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, AMD's published figure
 # the decode kernel's sources (the traffic record is valid only for these)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_13285_amd", "csrc", f)
                for f in ("gva_common.h", "gva_decode.hip")]
 TRAFFIC_FILE = os.path.join(ROOT, "profiles", "traffic_decode_b32_t8k.json")
+
+
+def metric_label(w) -> str:
+    """The metric named for the workload it is measured on: batch, cached
+    rows (K = 1024) and storage dtype, e.g. "B=32 T=8K bf16"."""
+    def rows(n):
+        return f"{n // 1024}K" if n % 1024 == 0 else str(n)
+    if w.lengths == "full":
+        span = rows(w.t_max)
+    elif w.lengths == "uniform_half":
+        span = f"{rows(w.t_max // 2)}..{rows(w.t_max)}"
+    else:
+        span = f"{rows(w.len_min)}..{rows(w.t_max)}"
+    return f"{METRIC}, B={w.batch} T={span} {w.dtype}"
 
 
 def kernel_sha() -> str:
@@ -331,28 +345,19 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
                                      q_abs=q_abs, split_rows=split_rows, stream=stream)
         combine()
 
-    def rope(i, ev_a=None, ev_b=None):
-        if ev_a is not None:
-            ev_a.record(stream)
+    def rope(i, with_combine=True):
         gva.gva_rope_decode_attention(d0, q0, dev["m"], caches[i % n][0], dev["lens"], S,
                                       bufs.o_part, bufs.lse_part, split_rows=split_rows, stream=stream)
-        if ev_b is not None:
-            ev_b.record(stream)
-        combine()
+        if with_combine:
+            combine()
 
     for i in range(args.warmup):
         absorbed(i)
         rope(i)
     t_abs = timed(absorbed, args.steps, stream)
     t_rope = timed(rope, args.steps, stream)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i, (a, b) in enumerate(evs):
-        rope(i, a, b)
-    torch.cuda.synchronize()
-    kt = sorted(a.elapsed_time(b) for a, b in evs)
-    k_ms = sum(kt) / len(kt)
+    # the contrast kernel alone, its launches back to back
+    k_ms = t_rope if S == 1 else timed(lambda i: rope(i, with_combine=False), args.steps, stream)
     rows = int(inp["lens"].clamp(min=0).sum())
     flops = traffic.rope_decode_flops(rows, w.n_heads, w.d_v, w.d_c)
     bytes_ = traffic.decode_bytes(inp["lens"], w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, 0, 2)
@@ -366,7 +371,7 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(tflops / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
                          "algorithmic_flops_per_launch": flops, "avg_launch_ms": round(k_ms, 5),
-                         "median_launch_ms": round(kt[len(kt) // 2], 5)}}
+                         "avg_launch_timing": "launches back to back between two events"}}
 
 
 def prefill_comparison(args, w, caches, dev, stream):
@@ -395,12 +400,8 @@ def prefill_comparison(args, w, caches, dev, stream):
     def absorb(i):
         gva.gva_prefill_absorb(d1, N, q, dev["m"], lens1, q_abs, qr, stream)
 
-    def attend(i, ev_a=None, ev_b=None):
-        if ev_a is not None:
-            ev_a.record(stream)
+    def attend(i):
         gva.gva_prefill_attention(d1, N, q_abs, qr, v1, krc, lens1, o, lse, stream)
-        if ev_b is not None:
-            ev_b.record(stream)
 
     def gqa(i):
         gva.gva_gqa_prefill_attention(d1, N, qg, kg, v1, lens1, o, lse, stream)
@@ -413,13 +414,7 @@ def prefill_comparison(args, w, caches, dev, stream):
     t_abs = timed(absorb, steps, stream)
     t_att = timed(attend, steps, stream)
     t_gqa = timed(gqa, steps, stream)
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)) for _ in range(steps)]
-    torch.cuda.synchronize()
-    for i, (a, b) in enumerate(evs):
-        attend(i, a, b)
-    torch.cuda.synchronize()
-    kt = sorted(a.elapsed_time(b) for a, b in evs)
-    k_ms = sum(kt) / len(kt)
+    k_ms = t_att
     f_gva = traffic.prefill_flops(N, N, w.n_heads, w.d_v, w.d_r)
     f_gqa = traffic.prefill_flops(N, N, w.n_heads, w.d_v, 0)
     tf = f_gva / (k_ms * 1e-3) / 1e12
@@ -435,7 +430,7 @@ def prefill_comparison(args, w, caches, dev, stream):
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
                          "algorithmic_flops_per_launch": f_gva, "avg_launch_ms": round(k_ms, 5),
-                         "median_launch_ms": round(kt[len(kt) // 2], 5)}}
+                         "avg_launch_timing": "launches back to back between two events"}}
 
 
 def main():
@@ -532,14 +527,12 @@ def main():
     pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"] if w.d_r > 0 else None,
                 split_rows=split_rows)
 
-    def step(i, ev_a=None, ev_b=None, attention_only=False):
+    def step(i, attention_only=False):
         # Algorithm 1: the attention call appends the current token's rows to
         # the caches and attends over them in the same launch.
         vc, kc = caches[i % n_copies]
         if not fused and not attention_only:
             gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
-        if ev_a is not None:
-            ev_a.record(stream)
         qkw = dict(q=dev["q"], m=dev["m"]) if fused else \
             dict(q_abs=q_abs, q_rot=q_rot if w.d_r > 0 else None)
         if paging is not None:
@@ -548,8 +541,6 @@ def main():
         else:
             gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
                                      stream=stream, **qkw, **pend)
-        if ev_b is not None:
-            ev_b.record(stream)
         if S > 1 and not attention_only:   # with one split the attention kernel's partial is the output
             gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
@@ -558,21 +549,19 @@ def main():
     torch.cuda.synchronize()
     ms_per_step = timed(step, args.steps, stream)
 
-    # timed region 2: the attention launch alone, the same steps' launches
-    # back to back between two events (an event pair around every launch
-    # adds ~2 us of its own at b32_t8k); the absorption and the combine
-    # launches of the separate path are left out, their inputs being in place
-    decode_ms = timed(lambda i: step(i, attention_only=True), args.steps, stream)
-
-    # timed region 3: the same steps with events around the attention kernel,
-    # for the spread of single launches
-    evs = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-           for _ in range(args.steps)]
-    torch.cuda.synchronize()
-    for i, (a, b) in enumerate(evs):
-        step(i, a, b)
-    torch.cuda.synchronize()
-    kt = sorted(a.elapsed_time(b) for a, b in evs)
+    # The roofline's launch time.  A step of one launch (one split, the
+    # absorption fused) is that launch: its time is the timed steps' own, so
+    # value and roofline come from one measurement.  Otherwise the attention
+    # launches are timed alone, the same steps' launches back to back between
+    # two events (the absorption and combine launches left out, their inputs
+    # being in place).
+    single_launch = S == 1 and fused
+    if single_launch:
+        decode_ms = ms_per_step
+        launch_timing = f"the {args.steps} timed steps (each step is this one launch)"
+    else:
+        decode_ms = timed(lambda i: step(i, attention_only=True), args.steps, stream)
+        launch_timing = f"{args.steps} attention launches back to back between two events on the launch stream"
     achievable, probe_wg = gva.probe_read_bandwidth(stream=stream)
     # a plain streaming read of the launch's algorithmic bytes, rotating over
     # as many buffers as the caches: the same start-up and tail, no compute
@@ -580,11 +569,15 @@ def main():
 
     step_b = traffic.step_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
                                 appended_rows=w.batch)
+    # the attention launch appends the current rows; with one split it also
+    # writes the output
+    launch_b = traffic.launch_bytes(lens, w.batch, w.n_heads, w.n_groups, w.d_v, w.d_c, w.d_r, elem,
+                                    appended_rows=w.batch, writes_output=S == 1)
     value = step_b / (ms_per_step * 1e-3) / 1e9
-    achieved = dec_b / (decode_ms * 1e-3) / 1e9
+    achieved = launch_b / (decode_ms * 1e-3) / 1e9
 
     out = {
-        "metric": METRIC,
+        "metric": metric_label(w),
         "value": round(value, 2),
         "unit": "GB/s",
         "n_gpus": 1,
@@ -613,19 +606,14 @@ def main():
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": measured_traffic(w.name, S),
-            "algorithmic_bytes_per_launch": dec_b,
+            "algorithmic_bytes_per_launch": launch_b,
             "avg_launch_ms": round(decode_ms, 5),
-            "avg_launch_timing": f"{args.steps} attention launches back to back between two events "
-                                 "on the launch stream",
-            "single_launch_events_ms": {"mean": round(sum(kt) / len(kt), 5),
-                                        "median": round(kt[len(kt) // 2], 5),
-                                        "p10": round(kt[len(kt) // 10], 5),
-                                        "p90": round(kt[(9 * len(kt)) // 10], 5)},
+            "avg_launch_timing": launch_timing,
             "achievable_read_GBps": round(achievable, 1),
             "frac_of_achievable": round(achieved / achievable, 4),
             "achievable_probe": f"gva_probe_read, 2 GiB, {probe_wg} workgroups",
             "same_bytes_read_ms": round(same_ms, 5),
-            "frac_of_same_bytes_read": round(same_ms / decode_ms, 4),
+            "frac_of_same_bytes_read": round(same_ms * launch_b / dec_b / decode_ms, 4),
             "same_bytes_probe": f"gva_probe_read over the launch's algorithmic bytes, {n_copies} buffers "
                                 f"in rotation, {same_wg} workgroups, 50 launches back to back",
         },

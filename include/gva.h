@@ -85,9 +85,9 @@ extern "C" {
 
 typedef enum gva_status {
   GVA_OK = 0,
-  GVA_ERR_INVALID_ARG = 1,  /* null/misaligned pointer, bad dims or split count */
-  GVA_ERR_UNSUPPORTED = 2,  /* valid shape this build has no kernel for */
-  GVA_ERR_HIP = 3           /* the HIP runtime reported an error */
+  GVA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad dims or split count */
+  GVA_ERR_UNSUPPORTED = -2, /* valid shape this build has no kernel for */
+  GVA_ERR_HIP = -3          /* the HIP runtime reported an error */
 } gva_status;
 
 typedef enum gva_dtype { GVA_DTYPE_F32 = 0, GVA_DTYPE_BF16 = 1 } gva_dtype;

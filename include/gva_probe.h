@@ -20,7 +20,8 @@ extern "C" {
  * device unsigned the kernel may write (it never does for realistic data;
  * the write only keeps the loads alive).  Time it with events on `stream`.
  * buf 16-byte aligned, sink 4-byte aligned.  The caller owns both.
- * Returns 0 (ok), 1 (invalid argument) or 3 (HIP launch error).
+ * Returns 0 (ok), -1 (invalid argument) or -3 (HIP launch error), the
+ * gva_status values of gva.h.
  */
 int gva_probe_read(const void* buf, int64_t bytes, int32_t workgroups, unsigned* sink, void* stream);
 

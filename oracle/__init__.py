@@ -20,7 +20,9 @@ import torch
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "gva_oracle.c")
-LIB_PATH = os.path.join(_HERE, "libgva_oracle.so")
+# GVA_ORACLE_LIB names another build of gva_oracle.c to load (the
+# sanitizer test runs the pins against an address/UB-sanitized build)
+LIB_PATH = os.environ.get("GVA_ORACLE_LIB") or os.path.join(_HERE, "libgva_oracle.so")
 
 _F64, _F32, _BF16 = 0, 1, 2
 _lib = None
@@ -239,25 +241,3 @@ def prefill(q: torch.Tensor, m: torch.Tensor, v: torch.Tensor, kr: torch.Tensor,
                                _ptr(vc), _ptr(kc), _code(vc), _ptr(lc), float(scale), float(rope_base),
                                int(n_threads), _ptr(o), _ptr(lse))
     return o, lse
-
-
-def split_bounds(lens: torch.Tensor, num_splits: int, tile: int = 32, split_rows: int = 0):
-    """Row ranges [begin, end) of every split, per sequence: [S][B] each.
-
-    Split s of a sequence with L rows covers [s*c, min(L, (s+1)*c)), except
-    that the last split ends at L.  c = split_rows when it is positive,
-    else c = tile * ceil(ceil(L / S) / tile).  Trailing splits may be empty.
-    """
-    L = lens.to(torch.int64).clamp(min=0)
-    if split_rows > 0:
-        chunk = torch.full_like(L, int(split_rows))
-    else:
-        per = (L + num_splits - 1) // num_splits
-        chunk = ((per + tile - 1) // tile) * tile
-    begins, ends = [], []
-    for s in range(num_splits):
-        b = torch.minimum(chunk * s, L)
-        e = L if s == num_splits - 1 else torch.minimum(chunk * (s + 1), L)
-        begins.append(b.to(torch.int32))
-        ends.append(e.to(torch.int32))
-    return begins, ends

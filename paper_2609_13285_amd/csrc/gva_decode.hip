@@ -1438,6 +1438,8 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
   if (dims->dtype == GVA_DTYPE_BF16) {
     if (dims->d_c % 32 != 0 || dims->d_c > 512 || dims->d_r % 8 != 0 || dims->d_r > 64)
       return GVA_ERR_UNSUPPORTED;
+    // the fused prologue absorbs at least one 32-column chunk of the query
+    if (fused && dims->d_c == 0) return GVA_ERR_UNSUPPORTED;
     const int nrc = (dims->d_r + 31) / 32;
     DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr, decode_kr_stream(dims));
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
@@ -1456,7 +1458,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
 extern "C" {
 
 
-int gva_version(void) { return 10700; }
+int gva_version(void) { return 20000; }
 
 const char* gva_status_string(int status) {
   switch (status) {

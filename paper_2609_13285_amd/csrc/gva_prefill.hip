@@ -16,17 +16,26 @@ namespace {
 // heads that share the group's value rows; C = 64, or 32 at d_v = 128 to
 // stay within 256 registers -- and its four waves split the key tiles up to
 // the block's last position.  Per 32-row key tile a wave forms the scores
-// of all C columns on the matrix cores (keys = [V | k_r] rows as stored,
-// the absorbed and rotated queries as bf16 B operands), masks rows past
-// each column's position, updates the online softmax and accumulates P.V
-// (V transposed once per tile with the identity MFMA, shared by the
-// column blocks).  P.V runs in fp16: the transposed rows come out of the
-// identity product in fp32 and every bf16 value of N(0, 1)-scale data is
-// exact in fp16, while the weights in [0, 1] keep 3 more bits than bf16.
+// of all C columns on the matrix cores (keys = [V | k_r] rows as stored),
+// masks rows past each column's position, updates the online softmax and
+// accumulates P.V (V transposed once per tile with the identity MFMA,
+// shared by the column blocks).
+// Precision.  The absorbed and rotated queries enter the score product as
+// bf16 high + low pairs (x = hi + lo to ~2^-16 of x, as in the decode
+// kernel): a single bf16 query moves every logit by up to 2^-9 of its size,
+// an error that grows with the sharpness of the scores.  The high parts
+// stay in registers; the low parts, the same for every tile and every wave
+// of the workgroup, are read from LDS each tile (registers are the limit).
+// A positional slice of at most 16 entries fills half of its 32-wide
+// K-chunk, so its low part rides in the other half of the same product.
+// P.V runs in fp16: the transposed rows come out of the identity product in
+// fp32 and every bf16 value of magnitude 2^-14 .. 65504 is exact in fp16,
+// while the weights in [0, 1] keep 3 more bits than bf16.
 // The waves merge through LDS.
 // Query blocks are dealt longest first, so the triangle's tail is short.
 // GQA = true is the matched grouped-query prefill the paper compares
-// against: scores read an explicit key stream, no positional term.
+// against: scores read an explicit key stream, no positional term; its
+// queries take the same high + low pairs.
 // (position, head) columns per workgroup: 64, fewer where a wider value
 // row (or the baseline's separate key tile) needs the registers
 __host__ __device__ constexpr int prefill_cols(int dv, bool gqa) { return dv >= 128 ? (gqa ? 16 : 32) : 64; }
@@ -49,13 +58,22 @@ constexpr float kLazyMax = 8.f;
 // Two workgroups per CU where the registers allow it without spilling.
 constexpr int prefill_min_blocks(int nrc) { return nrc >= 2 ? 1 : 2; }
 
-template <int HPG, int DV, int NRC, bool GQA>
+// KPACK: the positional slice has at most 16 entries (one K-chunk, half
+// used), so its low part shares that chunk.
+template <int HPG, int DV, int NRC, bool GQA, bool KPACK>
 __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf16_kernel(PrefillParams p) {
+  static_assert(!KPACK || NRC == 1, "a packed positional chunk is a single chunk");
   constexpr int COLS = prefill_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = COLS / 16;
   constexpr int QB = COLS / HPG;               // positions per workgroup
   constexpr int DEPTH = 2;
   constexpr int RS = DV + 2;                   // per-(wave, column) record: [m, l, o[DV]]
-  __shared__ __attribute__((aligned(16))) float red[kWaves * COLS * RS];
+  constexpr int NLO = NC + (KPACK ? 0 : NRC);  // low-part K-chunks read from LDS per column block
+  constexpr int RED_FLOATS = kWaves * COLS * RS;
+  constexpr int LO_FLOATS = CB * NLO * 64 * 4; // bf16x8 per lane, [cb][chunk][lane]
+  // the low parts are read during the key loop, the records only after it
+  __shared__ __attribute__((aligned(16))) float lds[RED_FLOATS > LO_FLOATS ? RED_FLOATS : LO_FLOATS];
+  float* red = lds;
+  bf16x8* lo_lds = reinterpret_cast<bf16x8*>(lds);
 
   const int nbg = p.B * p.G;
   const int x = blockIdx.x;
@@ -82,45 +100,6 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
   }
   const int p_first = L - p.N + qb * QB;       // the block's first position
 
-  // ---- the queries as bf16 B operands (zero for columns with no position)
-  bf16x8 bq[CB][NC];
-  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
-#pragma unroll
-  for (int cb = 0; cb < CB; ++cb) {
-    const int col = 16 * cb + n;
-    const int i = min(qb * QB + col / HPG, p.N - 1);
-    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
-    const float* qa = p.q_abs + qrow * DV + 8 * qd;
-#pragma unroll
-    for (int c = 0; c < NC; ++c) {
-      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
-      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
-      float xv[8];
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        xv[j] = u0[j] * p.scale_log2;
-        xv[4 + j] = u1[j] * p.scale_log2;
-      }
-      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
-    }
-#pragma unroll
-    for (int rc = 0; rc < NRC; ++rc) {
-      const int j0 = 32 * rc + 8 * qd;
-      float xv[8];
-      if (j0 < p.d_r) {
-        const float* qr = p.q_rot + qrow * p.d_r + j0;
-        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
-        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          xv[j] = u0[j] * p.scale_log2;
-          xv[4 + j] = u1[j] * p.scale_log2;
-        }
-      }
-      bk[cb][rc] = (pos[cb] >= 0 && j0 < p.d_r) ? split_hi_lo(xv, false) : zero8;
-    }
-  }
-
   // ---- key tiles: rows [0, kend), read through descriptors that end at
   // the last layout tile (reads past it return zeros)
   const int kend16 = kend > 0 ? ((kend + kLayoutRows - 1) / kLayoutRows) * kLayoutRows : 0;
@@ -137,9 +116,15 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
       (short)0, kend16 * DV * 2, kBufferWord3);
   const int kpieces = p.d_r / 8;
   const int v_lane = qd * 256 + n * 16;
+  // positional K-slots: piece qd of the row (lanes past d_r re-read a valid
+  // piece against a zero query); packed, slots kpieces .. 2 kpieces - 1
+  // repeat the row's pieces for the query's low part
   int k_lane[NRC > 0 ? NRC : 1];
 #pragma unroll
-  for (int rc = 0; rc < NRC; ++rc) k_lane[rc] = min(4 * rc + qd, kpieces - 1) * 256 + n * 16;
+  for (int rc = 0; rc < NRC; ++rc) {
+    const int piece = KPACK ? (qd < 2 * kpieces ? qd % kpieces : 0) : min(4 * rc + qd, kpieces - 1);
+    k_lane[rc] = piece * 256 + n * 16;
+  }
   const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
   const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
   const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
@@ -169,6 +154,57 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
     load_tile(buf[d], tile_row(d));
     __builtin_amdgcn_sched_barrier(0);
   }
+
+  // ---- the queries as bf16 high + low B operands (zero for columns with
+  // no position).  Every wave forms the high parts of all the workgroup's
+  // columns; the low parts go to LDS, each chunk written by one wave.
+  bf16x8 bq[CB][NC];
+  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
+  auto put_lo = [&](int cb, int c, const float* xv, bool live) {
+    if ((cb * NLO + c) % kWaves == w) lo_lds[(cb * NLO + c) * 64 + lane] = live ? split_hi_lo(xv, true) : zero8;
+  };
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = 16 * cb + n;
+    const int i = min(qb * QB + col / HPG, p.N - 1);
+    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
+    const float* qa = p.q_abs + qrow * DV + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+      float xv[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[j] = u0[j] * p.scale_log2;
+        xv[4 + j] = u1[j] * p.scale_log2;
+      }
+      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
+      put_lo(cb, c, xv, pos[cb] >= 0);
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      // the positional piece this lane's K-slot carries: high part of piece
+      // 4 rc + qd, or (packed) the low part of piece qd - kpieces
+      const bool hi_slot = KPACK ? qd < kpieces : 32 * rc + 8 * qd < p.d_r;
+      const bool lo_slot = KPACK && qd >= kpieces && qd < 2 * kpieces;
+      const int j0 = KPACK ? 8 * (lo_slot ? qd - kpieces : qd) : 32 * rc + 8 * qd;
+      float xv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (hi_slot || lo_slot) {
+        const float* qr = p.q_rot + qrow * p.d_r + j0;
+        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
+        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xv[j] = u0[j] * p.scale_log2;
+          xv[4 + j] = u1[j] * p.scale_log2;
+        }
+      }
+      bk[cb][rc] = (pos[cb] >= 0 && (hi_slot || lo_slot)) ? split_hi_lo(xv, lo_slot) : zero8;
+      if constexpr (!KPACK) put_lo(cb, NC + rc, xv, pos[cb] >= 0 && hi_slot);
+    }
+  }
+  __syncthreads();                             // the low parts are in LDS
 
   bf16x8 esel[2];
 #pragma unroll
@@ -206,17 +242,32 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
       }
     }
     const bool masked = row0 + kTileRows - 1 > p_first;   // some column may not see every row
+    // the LDS offset is opaque to the compiler, so the low parts are read
+    // here, tile by tile, instead of being hoisted into registers
+    int lo_off = lane;
+    asm volatile("" : "+v"(lo_off));
     f16x8 bp[CB];
 #pragma unroll
     for (int cb = 0; cb < CB; ++cb) {
+      bf16x8 lo[NLO];
+#pragma unroll
+      for (int c = 0; c < NLO; ++c) lo[c] = lo_lds[(cb * NLO + c) * 64 + lo_off];
+      // scores: the high and the low query parts accumulate into one sum
+      // per 16-row half
       f32x4 sc[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int c = 0; c < NC; ++c) sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
+        for (int c = 0; c < NC; ++c) {
+          sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
+          sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], lo[c], sc[hf]);
+        }
 #pragma unroll
-        for (int rc = 0; rc < NRC; ++rc) sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
+        for (int rc = 0; rc < NRC; ++rc) {
+          sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
+          if constexpr (!KPACK) sc[hf] = mfma16(t.k[hf][rc], lo[NC + rc], sc[hf]);
+        }
       }
       float xv[8];
 #pragma unroll
@@ -278,6 +329,7 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
   }
 
   // ---- merge the waves: per column the records (m, l, o) of the 4 waves
+  __syncthreads();                             // every wave is done with the low parts
 #pragma unroll
   for (int cb = 0; cb < CB; ++cb) {
     const float l = sum_over_rows(l_run[cb]);
@@ -322,31 +374,30 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
 using PrefillFn = void (*)(PrefillParams);
 
 template <int HPG, int DV>
-PrefillFn pick_prefill_nrc(int nrc, bool gqa) {
-  if (gqa) return prefill_bf16_kernel<HPG, DV, 0, true>;
-  switch (nrc) {
-    case 0: return prefill_bf16_kernel<HPG, DV, 0, false>;
-    case 1: return prefill_bf16_kernel<HPG, DV, 1, false>;
-    case 2: return prefill_bf16_kernel<HPG, DV, 2, false>;
-  }
+PrefillFn pick_prefill_nrc(int d_r, bool gqa) {
+  if (gqa) return prefill_bf16_kernel<HPG, DV, 0, true, false>;
+  if (d_r == 0) return prefill_bf16_kernel<HPG, DV, 0, false, false>;
+  if (d_r <= 16) return prefill_bf16_kernel<HPG, DV, 1, false, true>;
+  if (d_r <= 32) return prefill_bf16_kernel<HPG, DV, 1, false, false>;
+  if (d_r <= 64) return prefill_bf16_kernel<HPG, DV, 2, false, false>;
   return nullptr;
 }
 
 template <int HPG>
-PrefillFn pick_prefill_dv(int dv, int nrc, bool gqa) {
+PrefillFn pick_prefill_dv(int dv, int d_r, bool gqa) {
   switch (dv) {
-    case 64: return pick_prefill_nrc<HPG, 64>(nrc, gqa);
-    case 128: return pick_prefill_nrc<HPG, 128>(nrc, gqa);
+    case 64: return pick_prefill_nrc<HPG, 64>(d_r, gqa);
+    case 128: return pick_prefill_nrc<HPG, 128>(d_r, gqa);
   }
   return nullptr;
 }
 
-PrefillFn pick_prefill(int hpg, int dv, int nrc, bool gqa) {
+PrefillFn pick_prefill(int hpg, int dv, int d_r, bool gqa) {
   switch (hpg) {
-    case 1: return pick_prefill_dv<1>(dv, nrc, gqa);
-    case 2: return pick_prefill_dv<2>(dv, nrc, gqa);
-    case 4: return pick_prefill_dv<4>(dv, nrc, gqa);
-    case 8: return pick_prefill_dv<8>(dv, nrc, gqa);
+    case 1: return pick_prefill_dv<1>(dv, d_r, gqa);
+    case 2: return pick_prefill_dv<2>(dv, d_r, gqa);
+    case 4: return pick_prefill_dv<4>(dv, d_r, gqa);
+    case 8: return pick_prefill_dv<8>(dv, d_r, gqa);
   }
   return nullptr;
 }
@@ -372,7 +423,7 @@ int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const 
   if (st != GVA_OK) return st;
   if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
   const int hpg = dims->n_heads / dims->n_groups;
-  PrefillFn fn = pick_prefill(hpg, dims->d_v, (d_r + 31) / 32, gqa);
+  PrefillFn fn = pick_prefill(hpg, dims->d_v, d_r, gqa);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
   const int qb_rows = prefill_cols(dims->d_v, gqa) / hpg;
   const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;

@@ -39,9 +39,9 @@ __global__ void __launch_bounds__(kThreads) stream_read_kernel(const u32x4* __re
 
 extern "C" int gva_probe_read(const void* buf, int64_t bytes, int32_t workgroups, unsigned* sink,
                               void* stream) {
-  if (buf == nullptr || sink == nullptr || bytes < 16 || workgroups < 1) return 1;
-  if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0 || (reinterpret_cast<uintptr_t>(sink) & 3) != 0) return 1;
+  if (buf == nullptr || sink == nullptr || bytes < 16 || workgroups < 1) return -1;
+  if ((reinterpret_cast<uintptr_t>(buf) & 15) != 0 || (reinterpret_cast<uintptr_t>(sink) & 3) != 0) return -1;
   hipLaunchKernelGGL(stream_read_kernel, dim3(workgroups), dim3(kThreads), 0, static_cast<hipStream_t>(stream),
                      static_cast<const u32x4*>(buf), bytes / 16, sink);
-  return hipGetLastError() == hipSuccess ? 0 : 3;
+  return hipGetLastError() == hipSuccess ? 0 : -3;
 }

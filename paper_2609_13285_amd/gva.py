@@ -18,7 +18,7 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgva.so")
 
-GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, 1, 2, 3
+GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, -1, -2, -3
 GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
@@ -116,6 +116,20 @@ def _stream(stream) -> Optional[int]:
     if isinstance(stream, torch.cuda.Stream):
         return stream.cuda_stream
     return int(stream)
+
+
+def _in_use_on(stream, *tensors):
+    """Tell torch's caching allocator that ``tensors``, allocated on the
+    current stream, are also read by kernels enqueued on ``stream``, so their
+    memory is not handed out again before that work is done."""
+    if stream is None:
+        return
+    s = stream if isinstance(stream, torch.cuda.Stream) else torch.cuda.ExternalStream(int(stream))
+    if s.cuda_stream == torch.cuda.current_stream().cuda_stream:
+        return
+    for t in tensors:
+        if t is not None:
+            t.record_stream(s)
 
 
 def _ptr(t: Optional[torch.Tensor], name: str, dtype=None, shape=None):
@@ -477,6 +491,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
         fused = gva_prefer_fused(dims, S, split_rows)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
+        _in_use_on(stream, bufs.o_part, bufs.lse_part, bufs.o, bufs.lse)
     pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)
     if fused:
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
@@ -484,6 +499,7 @@ def decode(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int,
     else:
         q_abs = torch.empty(dims.batch, dims.n_heads, dims.d_v, dtype=torch.float32, device=v_cache.device)
         q_rot = torch.empty(dims.batch, dims.n_heads, dims.d_r, dtype=torch.float32, device=v_cache.device)
+        _in_use_on(stream, q_abs, q_rot)
         gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
         gva_decode_attention(dims, v_cache, kr_cache, lens, S, bufs.o_part, bufs.lse_part,
                              q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None, stream=stream, **pend)
@@ -500,6 +516,7 @@ def gqa_decode(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int,
     S = int(num_splits)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
+        _in_use_on(stream, bufs.o_part, bufs.lse_part, bufs.o, bufs.lse)
     gva_gqa_decode_attention(dims, q, k_cache, v_cache, lens, S, bufs.o_part, bufs.lse_part,
                              split_rows=split_rows, stream=stream)
     if S == 1:
@@ -515,6 +532,7 @@ def rope_decode(dims: GvaDims, q, m, v_cache, lens, num_splits: int,
     S = int(num_splits)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_cache.device)
+        _in_use_on(stream, bufs.o_part, bufs.lse_part, bufs.o, bufs.lse)
     gva_rope_decode_attention(dims, q, m, v_cache, lens, S, bufs.o_part, bufs.lse_part,
                               split_rows=split_rows, stream=stream)
     if S == 1:
@@ -533,6 +551,7 @@ def prefill(dims: GvaDims, q, m, v_cache, kr_cache, lens, stream=None) -> Tuple[
     q_rot = torch.empty(B, N, d.n_heads, d.d_r, dtype=torch.float32, device=dev)
     o = torch.empty(B, N, d.n_heads, d.d_v, dtype=torch.float32, device=dev)
     lse = torch.empty(B, N, d.n_heads, dtype=torch.float32, device=dev)
+    _in_use_on(stream, q_abs, q_rot, o, lse)
     gva_prefill_absorb(d, N, q, m, lens, q_abs, q_rot, stream=stream)
     gva_prefill_attention(d, N, q_abs, q_rot, v_cache, kr_cache, lens, o, lse, stream=stream)
     return o, lse
@@ -607,6 +626,7 @@ def paged_decode(dims: GvaDims, paging: GvaPaging, q, m, v_pool, kr_pool, block_
         fused = gva_prefer_fused(dims, S, split_rows)
     if bufs is None or bufs.num_splits != S:
         bufs = DecodeBuffers(dims, S, device=v_pool.device)
+        _in_use_on(stream, bufs.o_part, bufs.lse_part, bufs.o, bufs.lse)
     pend = dict(v_new=v_new, kr_new=kr_new if dims.d_r > 0 else None, split_rows=split_rows)
     if fused:
         gva_paged_decode_attention(dims, paging, v_pool, kr_pool, block_table, lens, S, bufs.o_part,
@@ -614,6 +634,7 @@ def paged_decode(dims: GvaDims, paging: GvaPaging, q, m, v_pool, kr_pool, block_
     else:
         q_abs = torch.empty(dims.batch, dims.n_heads, dims.d_v, dtype=torch.float32, device=v_pool.device)
         q_rot = torch.empty(dims.batch, dims.n_heads, dims.d_r, dtype=torch.float32, device=v_pool.device)
+        _in_use_on(stream, q_abs, q_rot)
         gva_absorb_query(dims, q, m, lens, q_abs, q_rot, stream=stream)
         gva_paged_decode_attention(dims, paging, v_pool, kr_pool, block_table, lens, S, bufs.o_part,
                                    bufs.lse_part, q_abs=q_abs, q_rot=q_rot if dims.d_r > 0 else None,

@@ -67,6 +67,18 @@ def step_bytes(lens: IntSeq, B: int, H: int, G: int, d_v: int, d_c: int, d_r: in
     return decode_bytes(lens, B, H, G, d_v, d_c, d_r, elem) + append + B * H * d_v * 4
 
 
+def launch_bytes(lens: IntSeq, B: int, H: int, G: int, d_v: int, d_c: int, d_r: int, elem: int,
+                 appended_rows: int = 0, writes_output: bool = False) -> int:
+    """Algorithmic bytes of one attention launch: the streams, M and q
+    (decode_bytes), plus the current token's rows when the launch appends
+    them (read once from the new rows, written once into the caches), plus
+    the fp32 output when the launch writes it (one split: its partial is
+    the output; with several, the combine writes it)."""
+    append = 2 * appended_rows * (G * d_v + d_r) * elem
+    out = B * H * d_v * 4 if writes_output else 0
+    return decode_bytes(lens, B, H, G, d_v, d_c, d_r, elem) + append + out
+
+
 def gqa_decode_bytes(lens: IntSeq, B: int, H: int, G: int, d_v: int, elem: int) -> int:
     """Algorithmic bytes of one matched-GQA decode launch (K and V streams)."""
     return _total_len(lens) * 2 * G * d_v * elem + B * H * d_v * elem

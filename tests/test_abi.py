@@ -38,14 +38,15 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(lib, name), name
     # every header under include/ is one of the two
     assert sorted(os.listdir(os.path.join(ROOT, "include"))) == ["gva.h", "gva_probe.h"]
-    assert gva.gva_version() == 10700
+    assert gva.gva_version() == 20000
 
 
 def test_status_strings():
     assert gva.status_string(0) == "ok"
-    assert "invalid" in gva.status_string(1)
-    assert "unsupported" in gva.status_string(2)
-    assert "HIP" in gva.status_string(3)
+    assert "invalid" in gva.status_string(-1)
+    assert "unsupported" in gva.status_string(-2)
+    assert "HIP" in gva.status_string(-3)
+    assert (gva.GVA_ERR_INVALID_ARG, gva.GVA_ERR_UNSUPPORTED, gva.GVA_ERR_HIP) == (-1, -2, -3)
     assert gva.status_string(99) == "unknown status"
 
 
@@ -111,6 +112,8 @@ def test_unsupported_shapes_reported():
     assert decode_status(dims(d_r=66)) == gva.GVA_ERR_UNSUPPORTED           # > 32 RoPE pairs
     assert decode_status(dims(t_max=40)) == gva.GVA_ERR_UNSUPPORTED         # tiled layout: T % 16
     assert decode_status(dims(dtype="f32", d_r=6)) == gva.GVA_ERR_UNSUPPORTED  # fp32 pieces of 4
+    # the fused bf16 prologue needs a content slice to absorb
+    assert decode_status(dims(d_c=0)) == gva.GVA_ERR_UNSUPPORTED
 
 
 def test_append_validation():
@@ -272,10 +275,10 @@ def test_prefill_validation():
 
 def test_probe_validation():
     lib = gva.lib()
-    assert lib.gva_probe_read(None, 1 << 20, 8, A, None) == 1
-    assert lib.gva_probe_read(A, 8, 8, A, None) == 1            # under one 16-byte piece
-    assert lib.gva_probe_read(A, 1 << 20, 0, A, None) == 1
-    assert lib.gva_probe_read(A + 4, 1 << 20, 8, A, None) == 1
+    assert lib.gva_probe_read(None, 1 << 20, 8, A, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_probe_read(A, 8, 8, A, None) == gva.GVA_ERR_INVALID_ARG    # under one 16-byte piece
+    assert lib.gva_probe_read(A, 1 << 20, 0, A, None) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_probe_read(A + 4, 1 << 20, 8, A, None) == gva.GVA_ERR_INVALID_ARG
 
 
 def paged_status(d, pg, v=A, kr=A, bt=A, lens=A, S=2, rows=0, op=A, lp=A):

@@ -98,3 +98,25 @@ def test_gqa_keys_recipe():
     assert not torch.equal(a, gva_inputs.gqa_keys(w, 4))
     x = a.float()
     assert abs(float(x.mean())) < 0.1 and abs(float(x.std()) - 1.0) < 0.1
+
+
+def test_metric_label_names_the_workload():
+    # the bench workload's label is the headline metric verbatim
+    w = gva_inputs.WORKLOADS["b32_t8k"]
+    assert bench.metric_label(w) == "decode attention GB/s (fraction of HBM peak) and tokens/s, B=32 T=8K bf16"
+    assert bench.metric_label(gva_inputs.WORKLOADS["ragged_b64"]).endswith("B=64 T=128..32K bf16")
+    assert bench.metric_label(gva_inputs.WORKLOADS["long_b4_t128k"]).endswith("B=4 T=64K..128K bf16")
+    assert bench.metric_label(gva_inputs.WORKLOADS["tiny_f32"]).endswith("B=1 T=256 f32")
+
+
+def test_launch_bytes_of_the_single_launch_step():
+    # one split, the current rows appended in the launch: the launch moves
+    # exactly the step's algorithmic bytes (append and fp32 output included)
+    w = gva_inputs.WORKLOADS["b32_t8k"]
+    lens = torch.full((w.batch,), w.t_max, dtype=torch.int32)
+    args = (lens, 32, 32, 8, 128, 128, 16, 2)
+    step = traffic.step_bytes(*args, appended_rows=32)
+    assert traffic.launch_bytes(*args, appended_rows=32, writes_output=True) == step == 547_260_416
+    # several splits: the combine writes the output, not the attention launch
+    assert traffic.launch_bytes(*args, appended_rows=32) == step - 32 * 32 * 128 * 4
+    assert traffic.launch_bytes(*args) == traffic.decode_bytes(*args)

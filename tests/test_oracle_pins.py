@@ -15,6 +15,8 @@ import pytest
 import torch
 import torch.nn.functional as F
 
+from splits import split_bounds
+
 GOLDEN = os.path.join(os.path.dirname(__file__), "golden")
 
 
@@ -265,7 +267,7 @@ def test_split_and_combine_equals_unsplit(orc, S, rows):
     # last split takes every remaining row)
     q, m, v, kr, lens = tiny_inputs(47, T=150, lens=[150, 61])
     o, lse = orc.decode(q, m, v, kr, lens)
-    begins, ends = orc.split_bounds(lens, S, tile=8, split_rows=rows)
+    begins, ends = split_bounds(lens, S, tile=8, split_rows=rows)
     parts = [orc.decode(q, m, v, kr, lens, t_begin=bg, t_end=en) for bg, en in zip(begins, ends)]
     o_part = torch.stack([p[0] for p in parts], dim=2)     # [B,H,S,dv]
     lse_part = torch.stack([p[1] for p in parts], dim=2)   # [B,H,S]
@@ -278,7 +280,7 @@ def test_split_and_combine_equals_unsplit(orc, S, rows):
 def test_split_bounds_cover_each_sequence(orc, rows):
     lens = torch.tensor([0, 1, 31, 32, 33, 1000, 8192], dtype=torch.int32)
     for S in (1, 2, 5, 16):
-        begins, ends = orc.split_bounds(lens, S, tile=32, split_rows=rows)
+        begins, ends = split_bounds(lens, S, tile=32, split_rows=rows)
         for b in range(lens.numel()):
             covered = []
             for s in range(S):
