@@ -77,6 +77,7 @@
 #ifndef GVA_H_
 #define GVA_H_
 
+#include <stddef.h>
 #include <stdint.h>
 
 #ifdef __cplusplus
@@ -356,6 +357,37 @@ int gva_gqa_prefill_attention(const gva_dims* dims, int32_t n_new, const float* 
  */
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part,
                 int32_t num_splits, float* o, float* lse, void* stream);
+
+/*
+ * gva_decode_workspace_size, gva_decode_step -- one whole decode step of
+ * Algorithm 1 in one call: the current token's rows appended (optional, as
+ * in gva_decode_attention), the query absorbed and rotated (eq. absorb,
+ * Section 3.2), the attention over every cached row in num_splits splits
+ * (Section 3.3) and the log-sum-exp merge of the splits, for every (b, h):
+ *   o[b][h][:] = sum_{t < L_b} softmax(x)_t v_cache[b][g(h)][t][:]
+ *   lse[b][h]  = log sum_{t < L_b} exp(x_t)
+ * with x_t as in gva_decode_attention (L_b = 0: o = 0, lse = -inf).  The
+ * result equals, bit for bit, the calls gva_prefer_fused chooses for the
+ * same plan on the current device: gva_decode_attention with the raw query,
+ * or gva_absorb_query and then gva_decode_attention with its output; then
+ * gva_combine when num_splits > 1.
+ * The intermediate buffers -- the absorbed queries of the separate path and
+ * the split partials -- live in `workspace`, a caller-owned device buffer of
+ * at least the bytes gva_decode_workspace_size reports for the same dims,
+ * num_splits and split_rows on the current device, 256-byte aligned (0
+ * bytes for one split with the absorption fused: workspace may then be
+ * NULL).  Its contents are scratch: nothing needs clearing before a call and
+ * nothing of it is used after one.  q, m, the caches, lens, v_new, kr_new,
+ * num_splits and split_rows as for gva_decode_attention (the raw query is
+ * required); o [B][H][d_v] fp32 and lse [B][H] fp32, both required.  Every
+ * launch is validated before the first is enqueued; a workspace that is
+ * missing, short or misaligned: GVA_ERR_INVALID_ARG.
+ */
+int gva_decode_workspace_size(const gva_dims* dims, int32_t num_splits, int32_t split_rows, size_t* bytes);
+int gva_decode_step(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
+                    const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
+                    int32_t split_rows, void* workspace, size_t workspace_bytes, float* o, float* lse,
+                    void* stream);
 
 /*
  * gva_pick_splits -- host heuristic: the split plan for a batch whose

@@ -1274,8 +1274,9 @@ bool decode_kr_stream(const gva_dims* d) {
   return (long long)d->batch * d->n_groups >= device_cu_count();
 }
 
+// With launch = false every argument is checked and nothing is enqueued.
 int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* m, const int32_t* lens,
-                float* q_abs, float* q_rot, void* stream) {
+                float* q_abs, float* q_rot, void* stream, bool launch = true) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (n_per_seq < 1) return GVA_ERR_INVALID_ARG;
@@ -1305,8 +1306,10 @@ int absorb_impl(const gva_dims* dims, int n_per_seq, const void* q, const void* 
   p.row_blocks = rows >= 4096 ? 4 : 1;
   fill_inv_freq(dims, p.inv_freq);
   hipStream_t s = static_cast<hipStream_t>(stream);
+  if (dims->dtype == GVA_DTYPE_BF16 && (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0))
+    return GVA_ERR_UNSUPPORTED;
+  if (!launch) return GVA_OK;
   if (dims->dtype == GVA_DTYPE_BF16) {
-    if (dims->d_v % 16 != 0 || dims->d_c % 32 != 0 || dims->d_r % 8 != 0) return GVA_ERR_UNSUPPORTED;
     const long long rows_per_wg = 16LL * p.row_blocks;
     const dim3 grid(dims->n_heads, (unsigned)((rows + rows_per_wg - 1) / rows_per_wg));
     hipLaunchKernelGGL(absorb_bf16_kernel, grid, dim3(kThreads), 0, s, p);
@@ -1375,7 +1378,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
                           const void* q, const void* m, const float* q_abs, const float* q_rot,
                           void* v_cache, void* kr_cache, const int32_t* lens, const void* v_new,
                           const void* kr_new, int32_t num_splits, int32_t split_rows, float* o_part,
-                          float* lse_part, void* stream) {
+                          float* lse_part, void* stream, bool launch = true) {
   int st = check_dims(dims);
   if (st != GVA_OK) return st;
   if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
@@ -1443,14 +1446,105 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
     const int nrc = (dims->d_r + 31) / 32;
     DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr, decode_kr_stream(dims));
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
+    if (!launch) return GVA_OK;
     hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   } else {
     if (paging != nullptr) return GVA_ERR_UNSUPPORTED;       // paged caches: bf16 only
     if (dims->d_v > kF32MaxDv || dims->d_c > 512 || dims->d_r > kF32MaxDr || hpg > kF32MaxHpg)
       return GVA_ERR_UNSUPPORTED;
+    if (!launch) return GVA_OK;
     hipLaunchKernelGGL(decode_f32_kernel, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
   }
   return launch_status();
+}
+
+int combine_impl(const gva_dims* dims, const float* o_part, const float* lse_part, int32_t num_splits,
+                 float* o, float* lse, void* stream, bool launch) {
+  int st = check_dims(dims);
+  if (st != GVA_OK) return st;
+  if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
+  if (!o_part || !lse_part || !o) return GVA_ERR_INVALID_ARG;
+  if (!aligned(o_part, 4) || !aligned(lse_part, 4) || !aligned(o, 4) || (lse && !aligned(lse, 4)))
+    return GVA_ERR_INVALID_ARG;
+  if (dims->d_v > kCombineMaxDv) return GVA_ERR_UNSUPPORTED;
+  if (!launch) return GVA_OK;
+  CombineParams p{};
+  p.o_part = o_part;
+  p.lse_part = lse_part;
+  p.o = o;
+  p.lse = lse;
+  p.rows = dims->batch * dims->n_heads;
+  p.S = num_splits;
+  p.d_v = dims->d_v;
+  const dim3 grid((p.rows + kWaves - 1) / kWaves);
+  hipLaunchKernelGGL(combine_kernel, grid, dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
+  return launch_status();
+}
+
+// ---------------------------------------------------------- whole step
+// One decode step in one call: the absorption (inside the attention launch,
+// or its own launch, as gva_prefer_fused decides), the attention, and the
+// combine when there are several splits.  The intermediate buffers -- the
+// absorbed queries of the separate path and the split partials -- live in
+// a workspace; with one split the attention writes o and lse directly.
+constexpr size_t kWorkspaceAlign = 256;
+
+struct StepLayout {
+  bool fused;
+  size_t q_abs, q_rot, o_part, lse_part;   // byte offsets into the workspace
+  size_t bytes;                            // workspace bytes the step uses
+};
+
+inline size_t ws_round(size_t x) { return (x + kWorkspaceAlign - 1) / kWorkspaceAlign * kWorkspaceAlign; }
+
+int step_layout(const gva_dims* d, int32_t num_splits, int32_t split_rows, StepLayout& L) {
+  const int st = check_dims(d);
+  if (st != GVA_OK) return st;
+  if (num_splits < 1 || num_splits > GVA_MAX_SPLITS || split_rows < 0) return GVA_ERR_INVALID_ARG;
+  L = StepLayout{};
+  L.fused = gva_prefer_fused(d, num_splits, split_rows, 0) != 0;
+  const size_t rows = (size_t)d->batch * (size_t)d->n_heads;
+  size_t off = 0;
+  if (!L.fused) {
+    L.q_abs = off;
+    off += ws_round(rows * (size_t)d->d_v * 4);
+    L.q_rot = off;
+    off += ws_round(rows * (size_t)d->d_r * 4);
+  }
+  if (num_splits > 1) {
+    L.o_part = off;
+    off += ws_round(rows * (size_t)num_splits * (size_t)d->d_v * 4);
+    L.lse_part = off;
+    off += ws_round(rows * (size_t)num_splits * 4);
+  }
+  L.bytes = off;
+  return GVA_OK;
+}
+
+// The step's launches on workspace ws (L.bytes bytes, 256-byte aligned).
+// Every launch is validated before the first is enqueued.
+int decode_step_impl(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
+                     const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
+                     int32_t split_rows, char* ws, const StepLayout& L, float* o, float* lse, void* stream) {
+  if (!q || !m || !o || !lse) return GVA_ERR_INVALID_ARG;
+  const int S = num_splits;
+  float* q_abs = L.fused ? nullptr : reinterpret_cast<float*>(ws + L.q_abs);
+  float* q_rot = (L.fused || dims->d_r == 0) ? nullptr : reinterpret_cast<float*>(ws + L.q_rot);
+  float* o_part = S > 1 ? reinterpret_cast<float*>(ws + L.o_part) : o;
+  float* lse_part = S > 1 ? reinterpret_cast<float*>(ws + L.lse_part) : lse;
+  const void* fq = L.fused ? q : nullptr;
+  const void* fm = L.fused ? m : nullptr;
+  for (int pass = 0; pass < 2; ++pass) {       // pass 0 checks, pass 1 launches
+    const bool launch = pass == 1;
+    int st = GVA_OK;
+    if (!L.fused) st = absorb_impl(dims, 1, q, m, lens, q_abs, q_rot, stream, launch);
+    if (st == GVA_OK)
+      st = decode_attention_impl(dims, nullptr, nullptr, fq, fm, q_abs, q_rot, v_cache, kr_cache, lens, v_new,
+                                 kr_new, S, split_rows, o_part, lse_part, stream, launch);
+    if (st == GVA_OK && S > 1) st = combine_impl(dims, o_part, lse_part, S, o, lse, stream, launch);
+    if (st != GVA_OK) return st;
+  }
+  return GVA_OK;
 }
 
 }  // namespace
@@ -1568,24 +1662,29 @@ int gva_prefill_absorb(const gva_dims* dims, int32_t n_new, const void* q, const
 
 int gva_combine(const gva_dims* dims, const float* o_part, const float* lse_part, int32_t num_splits,
                 float* o, float* lse, void* stream) {
-  int st = check_dims(dims);
+  return combine_impl(dims, o_part, lse_part, num_splits, o, lse, stream, true);
+}
+
+int gva_decode_workspace_size(const gva_dims* dims, int32_t num_splits, int32_t split_rows, size_t* bytes) {
+  if (bytes == nullptr) return GVA_ERR_INVALID_ARG;
+  StepLayout L;
+  const int st = step_layout(dims, num_splits, split_rows, L);
   if (st != GVA_OK) return st;
-  if (num_splits < 1 || num_splits > GVA_MAX_SPLITS) return GVA_ERR_INVALID_ARG;
-  if (!o_part || !lse_part || !o) return GVA_ERR_INVALID_ARG;
-  if (!aligned(o_part, 4) || !aligned(lse_part, 4) || !aligned(o, 4) || (lse && !aligned(lse, 4)))
+  *bytes = L.bytes;
+  return GVA_OK;
+}
+
+int gva_decode_step(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
+                    const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
+                    int32_t split_rows, void* workspace, size_t workspace_bytes, float* o, float* lse,
+                    void* stream) {
+  StepLayout L;
+  const int st = step_layout(dims, num_splits, split_rows, L);
+  if (st != GVA_OK) return st;
+  if (L.bytes > 0 && (workspace == nullptr || workspace_bytes < L.bytes || !aligned(workspace, kWorkspaceAlign)))
     return GVA_ERR_INVALID_ARG;
-  if (dims->d_v > kCombineMaxDv) return GVA_ERR_UNSUPPORTED;
-  CombineParams p{};
-  p.o_part = o_part;
-  p.lse_part = lse_part;
-  p.o = o;
-  p.lse = lse;
-  p.rows = dims->batch * dims->n_heads;
-  p.S = num_splits;
-  p.d_v = dims->d_v;
-  const dim3 grid((p.rows + kWaves - 1) / kWaves);
-  hipLaunchKernelGGL(combine_kernel, grid, dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
-  return launch_status();
+  return decode_step_impl(dims, q, m, v_cache, kr_cache, lens, v_new, kr_new, num_splits, split_rows,
+                          static_cast<char*>(workspace), L, o, lse, stream);
 }
 
 int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu) {

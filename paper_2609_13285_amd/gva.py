@@ -25,7 +25,7 @@ EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_com
            "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
            "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
            "gva_gqa_prefill_attention", "gva_pick_splits", "gva_prefer_fused", "gva_status_string",
-           "gva_version")
+           "gva_version", "gva_decode_workspace_size", "gva_decode_step")
 GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
@@ -82,6 +82,8 @@ def lib() -> ctypes.CDLL:
         L.gva_paged_decode_attention.argtypes = [D, PG, P, P, P, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_pick_splits.argtypes = [D, I32, ctypes.c_int64, I32, ctypes.POINTER(I32)]
         L.gva_prefer_fused.argtypes = [D, I32, I32, I32]
+        L.gva_decode_workspace_size.argtypes = [D, I32, I32, ctypes.POINTER(ctypes.c_size_t)]
+        L.gva_decode_step.argtypes = [D, P, P, P, P, P, P, P, I32, I32, P, ctypes.c_size_t, P, P, P]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
@@ -89,7 +91,8 @@ def lib() -> ctypes.CDLL:
         for name in ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
                      "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
                      "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
-                     "gva_gqa_prefill_attention", "gva_pick_splits", "gva_version", "gva_probe_read"):
+                     "gva_gqa_prefill_attention", "gva_pick_splits", "gva_version", "gva_probe_read",
+                     "gva_decode_workspace_size", "gva_decode_step"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -219,6 +222,47 @@ def gva_combine(dims: GvaDims, o_part, lse_part, num_splits: int, o, lse=None, s
         _ptr(lse, "lse", torch.float32, (d.batch, d.n_heads)),
         _stream(stream))
     _check("gva_combine", st)
+
+
+def gva_decode_workspace_size(dims: GvaDims, num_splits: int, split_rows: int = 0) -> int:
+    """Workspace bytes gva_decode_step needs for this plan on the current device."""
+    n = ctypes.c_size_t(0)
+    _check("gva_decode_workspace_size",
+           lib().gva_decode_workspace_size(ctypes.byref(dims), int(num_splits), int(split_rows), ctypes.byref(n)))
+    return int(n.value)
+
+
+def workspace_for(dims: GvaDims, num_splits: int, split_rows: int = 0, device="cuda") -> Optional[torch.Tensor]:
+    """A device buffer for gva_decode_step (None when the plan needs none);
+    torch's allocator aligns it to 256 bytes or more."""
+    n = gva_decode_workspace_size(dims, num_splits, split_rows)
+    return torch.empty(n, dtype=torch.uint8, device=device) if n else None
+
+
+def gva_decode_step(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int, o, lse, workspace=None,
+                    v_new=None, kr_new=None, split_rows: int = 0, stream=None):
+    """One whole decode step (absorb + attention + combine) into o / lse."""
+    d = dims
+    dt = d.torch_dtype
+    S = int(num_splits)
+    if workspace is not None and (workspace.dtype != torch.uint8 or workspace.dim() != 1):
+        raise ValueError("workspace must be a 1-D uint8 tensor")
+    st = lib().gva_decode_step(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(v_new, "v_new", dt, (d.batch, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (d.batch, d.d_r)),
+        S, int(split_rows),
+        _ptr(workspace, "workspace"),
+        0 if workspace is None else workspace.numel(),
+        _ptr(o, "o", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(lse, "lse", torch.float32, (d.batch, d.n_heads)),
+        _stream(stream))
+    _check("gva_decode_step", st)
 
 
 def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int, o_part,

@@ -322,3 +322,54 @@ def test_page_plumbing_round_trip():
     # a page block is the tiled layout of that page's rows
     page = int(bt[1, 2])
     assert torch.equal(gva.untiled(vp[page]), v[1, :, 128:192])
+
+
+def _ws_round(n):
+    return (n + 255) // 256 * 256
+
+
+def test_decode_workspace_size():
+    # one split with the absorption fused: no workspace at all
+    big = dims(batch=32, n_heads=32, n_groups=8, t_max=8192)
+    assert gva.gva_decode_workspace_size(big, 1) == 0
+    # several splits, absorption still fused (B G S <= 2 per CU on 256 CUs)
+    S = 2
+    assert gva.gva_prefer_fused(big, S, 0, 256)
+    rows = 32 * 32
+    assert gva.gva_decode_workspace_size(big, S) == _ws_round(rows * S * 128 * 4) + _ws_round(rows * S * 4)
+    # ragged batch, fixed chunks: separate absorption (q~ and the rotated
+    # positional query) plus the partials
+    rag = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
+    S, c = 16, 1696
+    assert not gva.gva_prefer_fused(rag, S, c, 256)
+    rows = 64 * 16
+    expect = (_ws_round(rows * 128 * 4) + _ws_round(rows * 16 * 4) + _ws_round(rows * S * 128 * 4)
+              + _ws_round(rows * S * 4))
+    assert gva.gva_decode_workspace_size(rag, S, c) == expect
+    lib = gva.lib()
+    n = ctypes.c_size_t(7)
+    assert lib.gva_decode_workspace_size(ctypes.byref(rag), 0, 0, ctypes.byref(n)) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_decode_workspace_size(ctypes.byref(rag), 2, -32, ctypes.byref(n)) == gva.GVA_ERR_INVALID_ARG
+    assert lib.gva_decode_workspace_size(ctypes.byref(rag), 2, 0, None) == gva.GVA_ERR_INVALID_ARG
+    assert n.value == 7
+
+
+def step_status(d, S=4, rows=0, q=A, m=A, ws=A, nbytes=1 << 30, o=A, lse=A, vn=None, kn=None):
+    return gva.lib().gva_decode_step(ctypes.byref(d), q, m, A, A, A, vn, kn, S, rows, ws, nbytes, o, lse, None)
+
+
+def test_decode_step_validation():
+    rag = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
+    need = gva.gva_decode_workspace_size(rag, 16, 1696)
+    ok = dict(S=16, rows=1696)
+    assert step_status(rag, ws=None, **ok) == gva.GVA_ERR_INVALID_ARG              # workspace needed
+    assert step_status(rag, nbytes=need - 1, **ok) == gva.GVA_ERR_INVALID_ARG      # too short
+    assert step_status(rag, ws=A + 128, **ok) == gva.GVA_ERR_INVALID_ARG           # not 256-byte aligned
+    assert step_status(rag, q=None, **ok) == gva.GVA_ERR_INVALID_ARG               # raw query required
+    assert step_status(rag, o=None, **ok) == gva.GVA_ERR_INVALID_ARG
+    assert step_status(rag, lse=None, **ok) == gva.GVA_ERR_INVALID_ARG
+    assert step_status(rag, S=0) == gva.GVA_ERR_INVALID_ARG
+    assert step_status(rag, S=2, rows=48) == gva.GVA_ERR_INVALID_ARG                # not whole tiles
+    assert step_status(rag, vn=None, kn=A, **ok) == gva.GVA_ERR_INVALID_ARG
+    assert step_status(dims(d_v=96), S=1, ws=None) == gva.GVA_ERR_UNSUPPORTED
+    assert step_status(dims(d_c=0), S=1, ws=None) == gva.GVA_ERR_UNSUPPORTED       # fused, nothing to absorb

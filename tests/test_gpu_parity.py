@@ -353,6 +353,56 @@ def test_decode_on_a_side_stream():
     assert torch.equal(o, o_ref) and torch.equal(lse, lse_ref)
 
 
+STEP_CASES = [
+    # (workload, lengths, num_splits, split_rows): one split fused; several
+    # splits fused; fixed chunks over a grid past two workgroups per CU, so
+    # the absorption runs as its own launch into the workspace; fp32
+    (gva_inputs.workload("gva350m_b8_t2k"), None, 1, 0),
+    (gva_inputs.workload("gva350m_b8_t2k"), None, 3, 0),
+    (gva_inputs.Workload("step_ragged", 40, 2048, 16, 2, 128, 128, 16), "ragged", 8, 256),
+    (gva_inputs.workload("tiny_f32"), None, 2, 0),
+]
+
+
+@pytest.mark.parametrize("case", STEP_CASES, ids=lambda c: f"{c[0].name}-S{c[2]}-r{c[3]}")
+@pytest.mark.parametrize("append", [False, True])
+def test_decode_step_matches_the_separate_calls(case, append):
+    w, lens_kind, S, rows = case
+    lens = None
+    if lens_kind == "ragged":
+        g = torch.Generator().manual_seed(17)
+        lens = torch.randint(1, w.t_max + 1, (w.batch,), generator=g, dtype=torch.int32)
+        lens[:3] = torch.tensor([0, 1, w.t_max], dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 13, lens=lens)
+    d = dims_of(w)
+    dev = upload(inp)
+    v2, kr2 = dev["v"].clone(), dev["kr"].clone()
+    pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"]) if append else {}
+    fused = gva.gva_prefer_fused(d, S, rows)
+    note(f"decode step {w.name} S={S} rows={rows} append={append} fused={fused}")
+    ws = gva.workspace_for(d, S, rows)
+    assert (ws is None) == (S == 1 and fused)
+    o = torch.full((w.batch, w.n_heads, w.d_v), float("nan"), device="cuda")
+    lse = torch.full((w.batch, w.n_heads), float("nan"), device="cuda")
+    gva.gva_decode_step(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S, o, lse, workspace=ws,
+                        split_rows=rows, **pend)
+    pend2 = dict(v_new=dev["v_new"], kr_new=dev["kr_new"]) if append else {}
+    o2, lse2 = gva.decode(d, dev["q"], dev["m"], v2, kr2, dev["lens"], S, fused=fused, split_rows=rows, **pend2)
+    torch.cuda.synchronize()
+    assert torch.equal(o, o2) and torch.equal(lse, lse2)
+    assert torch.equal(dev["v"], v2) and torch.equal(dev["kr"], kr2)
+    v_ref, k_ref = inp["v"], inp["kr"]
+    if append:
+        v_ref, k_ref = v_ref.clone(), k_ref.clone()
+        seq = torch.arange(w.batch, dtype=torch.int32)
+        L = inp["lens"].clamp(0, w.t_max)
+        live = L > 0
+        oracle.append(v_ref, k_ref, inp["v_new"][live], inp["kr_new"][live], seq[live], (L - 1)[live].to(torch.int32),
+                      w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"], rope_base=w.rope_base)
+    _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"step {w.name} S{S}")
+
+
 # ----------------------------------------------- full-size workloads
 def full_size_picks(lens: torch.Tensor, n_spread: int = 12):
     """The sequences a full-size test checks against the oracle: every one of
