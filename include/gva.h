@@ -88,7 +88,8 @@ typedef enum gva_status {
   GVA_OK = 0,
   GVA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad dims or split count */
   GVA_ERR_UNSUPPORTED = -2, /* valid shape this build has no kernel for */
-  GVA_ERR_HIP = -3          /* the HIP runtime reported an error */
+  GVA_ERR_HIP = -3,         /* the HIP runtime reported an error */
+  GVA_ERR_SCRATCH = -4      /* gva_decode_step_static: more than GVA_STATIC_SCRATCH_BYTES needed */
 } gva_status;
 
 typedef enum gva_dtype { GVA_DTYPE_F32 = 0, GVA_DTYPE_BF16 = 1 } gva_dtype;
@@ -388,6 +389,26 @@ int gva_decode_step(const gva_dims* dims, const void* q, const void* m, void* v_
                     const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
                     int32_t split_rows, void* workspace, size_t workspace_bytes, float* o, float* lse,
                     void* stream);
+
+/*
+ * gva_decode_step_static -- gva_decode_step for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving
+ * loops, harnesses that forbid allocation): the same launches, bit for bit
+ * the same results, with the workspace taken from the library's static
+ * scratch buffer instead of an argument.  The buffer is a file-scope device
+ * array of GVA_STATIC_SCRATCH_BYTES, one on every GPU the library runs on,
+ * held until the process ends; its address is looked up on the first call
+ * on each device.  The call allocates, frees and clears nothing.  A plan
+ * whose workspace (gva_decode_workspace_size) exceeds the buffer returns
+ * GVA_ERR_SCRATCH and enqueues nothing.  Every call on a GPU shares that
+ * GPU's buffer: calls that may run at the same time on one GPU (different
+ * streams, or host threads) race and must be ordered by the caller; calls
+ * in one stream are ordered already.  Arguments as for gva_decode_step.
+ */
+#define GVA_STATIC_SCRATCH_BYTES (16u << 20)
+int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
+                           const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
+                           int32_t split_rows, float* o, float* lse, void* stream);
 
 /*
  * gva_pick_splits -- host heuristic: the split plan for a batch whose

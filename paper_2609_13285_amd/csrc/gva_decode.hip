@@ -42,6 +42,8 @@
 // exactly the B-operand layout of the P.V product, so the softmax needs no
 // cross-lane traffic except the max over the four 16-lane rows.
 
+#include <mutex>
+
 #include "gva_common.h"
 
 namespace {
@@ -1523,9 +1525,11 @@ int step_layout(const gva_dims* d, int32_t num_splits, int32_t split_rows, StepL
 
 // The step's launches on workspace ws (L.bytes bytes, 256-byte aligned).
 // Every launch is validated before the first is enqueued.
+// With launch = false only the checks run.
 int decode_step_impl(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
                      const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
-                     int32_t split_rows, char* ws, const StepLayout& L, float* o, float* lse, void* stream) {
+                     int32_t split_rows, char* ws, const StepLayout& L, float* o, float* lse, void* stream,
+                     bool launch = true) {
   if (!q || !m || !o || !lse) return GVA_ERR_INVALID_ARG;
   const int S = num_splits;
   float* q_abs = L.fused ? nullptr : reinterpret_cast<float*>(ws + L.q_abs);
@@ -1534,16 +1538,46 @@ int decode_step_impl(const gva_dims* dims, const void* q, const void* m, void* v
   float* lse_part = S > 1 ? reinterpret_cast<float*>(ws + L.lse_part) : lse;
   const void* fq = L.fused ? q : nullptr;
   const void* fm = L.fused ? m : nullptr;
-  for (int pass = 0; pass < 2; ++pass) {       // pass 0 checks, pass 1 launches
-    const bool launch = pass == 1;
+  for (int pass = 0; pass < (launch ? 2 : 1); ++pass) {   // pass 0 checks, pass 1 launches
+    const bool go = pass == 1;
     int st = GVA_OK;
-    if (!L.fused) st = absorb_impl(dims, 1, q, m, lens, q_abs, q_rot, stream, launch);
+    if (!L.fused) st = absorb_impl(dims, 1, q, m, lens, q_abs, q_rot, stream, go);
     if (st == GVA_OK)
       st = decode_attention_impl(dims, nullptr, nullptr, fq, fm, q_abs, q_rot, v_cache, kr_cache, lens, v_new,
-                                 kr_new, S, split_rows, o_part, lse_part, stream, launch);
-    if (st == GVA_OK && S > 1) st = combine_impl(dims, o_part, lse_part, S, o, lse, stream, launch);
+                                 kr_new, S, split_rows, o_part, lse_part, stream, go);
+    if (st == GVA_OK && S > 1) st = combine_impl(dims, o_part, lse_part, S, o, lse, stream, go);
     if (st != GVA_OK) return st;
   }
+  return GVA_OK;
+}
+
+}  // namespace
+
+// ------------------------------------------------------- static scratch
+// The workspace of gva_decode_step_static, for callers that cannot
+// allocate: a file-scope device array, one copy on every GPU the library
+// runs on, held until the process ends.  In host code `scratch` names a
+// host-side stand-in, never the device memory: its device address is
+// looked up once per device (hipGetSymbolAddress, with that device current)
+// and only that address is passed to the kernels.
+static __device__ __align__(256) unsigned char scratch[GVA_STATIC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex scratch_mu;
+void* scratch_dev[kMaxDevices];   // per device: the address of its copy of scratch
+
+int static_scratch(char** out) {
+  int dev = -1;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= kMaxDevices) return GVA_ERR_HIP;
+  std::lock_guard<std::mutex> lock(scratch_mu);
+  if (scratch_dev[dev] == nullptr) {
+    void* ptr = nullptr;
+    if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || ptr == nullptr) return GVA_ERR_HIP;
+    scratch_dev[dev] = ptr;
+  }
+  *out = static_cast<char*>(scratch_dev[dev]);
   return GVA_OK;
 }
 
@@ -1560,6 +1594,7 @@ const char* gva_status_string(int status) {
     case GVA_ERR_INVALID_ARG: return "invalid argument";
     case GVA_ERR_UNSUPPORTED: return "unsupported shape";
     case GVA_ERR_HIP: return "HIP runtime error";
+    case GVA_ERR_SCRATCH: return "the step needs more than the static scratch buffer (GVA_STATIC_SCRATCH_BYTES)";
   }
   return "unknown status";
 }
@@ -1685,6 +1720,29 @@ int gva_decode_step(const gva_dims* dims, const void* q, const void* m, void* v_
     return GVA_ERR_INVALID_ARG;
   return decode_step_impl(dims, q, m, v_cache, kr_cache, lens, v_new, kr_new, num_splits, split_rows,
                           static_cast<char*>(workspace), L, o, lse, stream);
+}
+
+int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, void* v_cache, void* kr_cache,
+                           const int32_t* lens, const void* v_new, const void* kr_new, int32_t num_splits,
+                           int32_t split_rows, float* o, float* lse, void* stream) {
+  StepLayout L;
+  int st = step_layout(dims, num_splits, split_rows, L);
+  if (st != GVA_OK) return st;
+  if (L.bytes > (size_t)GVA_STATIC_SCRATCH_BYTES) return GVA_ERR_SCRATCH;
+  // every check before the first runtime call (the checks see a stand-in
+  // workspace address, aligned like the buffer, that nothing dereferences);
+  // then the device's scratch
+  char* const stand_in = reinterpret_cast<char*>(kWorkspaceAlign);
+  st = decode_step_impl(dims, q, m, v_cache, kr_cache, lens, v_new, kr_new, num_splits, split_rows, stand_in, L, o,
+                        lse, stream, false);
+  if (st != GVA_OK) return st;
+  char* ws = nullptr;
+  if (L.bytes > 0) {
+    st = static_scratch(&ws);
+    if (st != GVA_OK) return st;
+  }
+  return decode_step_impl(dims, q, m, v_cache, kr_cache, lens, v_new, kr_new, num_splits, split_rows, ws, L, o, lse,
+                          stream);
 }
 
 int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu) {

@@ -18,14 +18,15 @@ import torch
 
 LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libgva.so")
 
-GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP = 0, -1, -2, -3
+GVA_OK, GVA_ERR_INVALID_ARG, GVA_ERR_UNSUPPORTED, GVA_ERR_HIP, GVA_ERR_SCRATCH = 0, -1, -2, -3, -4
+GVA_STATIC_SCRATCH_BYTES = 16 << 20
 GVA_DTYPE_F32, GVA_DTYPE_BF16 = 0, 1
 GVA_MAX_SPLITS = 256
 EXPORTS = ("gva_append_kv", "gva_absorb_query", "gva_decode_attention", "gva_combine",
            "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
            "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
            "gva_gqa_prefill_attention", "gva_pick_splits", "gva_prefer_fused", "gva_status_string",
-           "gva_version", "gva_decode_workspace_size", "gva_decode_step")
+           "gva_version", "gva_decode_workspace_size", "gva_decode_step", "gva_decode_step_static")
 GVA_MAX_PAGES = 4096
 PROBE_EXPORTS = ("gva_probe_read",)      # include/gva_probe.h
 
@@ -84,6 +85,7 @@ def lib() -> ctypes.CDLL:
         L.gva_prefer_fused.argtypes = [D, I32, I32, I32]
         L.gva_decode_workspace_size.argtypes = [D, I32, I32, ctypes.POINTER(ctypes.c_size_t)]
         L.gva_decode_step.argtypes = [D, P, P, P, P, P, P, P, I32, I32, P, ctypes.c_size_t, P, P, P]
+        L.gva_decode_step_static.argtypes = [D, P, P, P, P, P, P, P, I32, I32, P, P, P]
         L.gva_status_string.argtypes = [ctypes.c_int]
         L.gva_status_string.restype = ctypes.c_char_p
         L.gva_version.argtypes = []
@@ -92,7 +94,7 @@ def lib() -> ctypes.CDLL:
                      "gva_gqa_decode_attention", "gva_paged_append_kv", "gva_paged_decode_attention",
                      "gva_rope_decode_attention", "gva_prefill_absorb", "gva_prefill_attention",
                      "gva_gqa_prefill_attention", "gva_pick_splits", "gva_version", "gva_probe_read",
-                     "gva_decode_workspace_size", "gva_decode_step"):
+                     "gva_decode_workspace_size", "gva_decode_step", "gva_decode_step_static"):
             getattr(L, name).restype = ctypes.c_int
         _lib = L
     return _lib
@@ -263,6 +265,28 @@ def gva_decode_step(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: in
         _ptr(lse, "lse", torch.float32, (d.batch, d.n_heads)),
         _stream(stream))
     _check("gva_decode_step", st)
+
+
+def gva_decode_step_static(dims: GvaDims, q, m, v_cache, kr_cache, lens, num_splits: int, o, lse,
+                           v_new=None, kr_new=None, split_rows: int = 0, stream=None):
+    """gva_decode_step with its workspace in the library's static per-device
+    scratch buffer: for callers that cannot allocate."""
+    d = dims
+    dt = d.torch_dtype
+    st = lib().gva_decode_step_static(
+        ctypes.byref(d),
+        _ptr(q, "q", dt, (d.batch, d.n_heads, d.d_c + d.d_r)),
+        _ptr(m, "m", dt, (d.n_heads, d.d_v, d.d_c)),
+        _ptr(v_cache, "v_cache", dt, (d.batch, d.n_groups, d.t_max, d.d_v)),
+        _ptr(kr_cache, "kr_cache", dt, (d.batch, d.t_max, d.d_r)),
+        _ptr(lens, "lens", torch.int32, (d.batch,)),
+        _ptr(v_new, "v_new", dt, (d.batch, d.n_groups, d.d_v)),
+        _ptr(kr_new, "kr_new", dt, (d.batch, d.d_r)),
+        int(num_splits), int(split_rows),
+        _ptr(o, "o", torch.float32, (d.batch, d.n_heads, d.d_v)),
+        _ptr(lse, "lse", torch.float32, (d.batch, d.n_heads)),
+        _stream(stream))
+    _check("gva_decode_step_static", st)
 
 
 def gva_gqa_decode_attention(dims: GvaDims, q, k_cache, v_cache, lens, num_splits: int, o_part,

@@ -373,3 +373,23 @@ def test_decode_step_validation():
     assert step_status(rag, vn=None, kn=A, **ok) == gva.GVA_ERR_INVALID_ARG
     assert step_status(dims(d_v=96), S=1, ws=None) == gva.GVA_ERR_UNSUPPORTED
     assert step_status(dims(d_c=0), S=1, ws=None) == gva.GVA_ERR_UNSUPPORTED       # fused, nothing to absorb
+
+
+def test_decode_step_static_validation():
+    # checked on the host before any runtime call: a plan past the static
+    # scratch buffer is refused with its own status
+    lib = gva.lib()
+    assert "static scratch" in gva.status_string(gva.GVA_ERR_SCRATCH)
+
+    def st(d, S=4, rows=0, q=A, o=A, lse=A):
+        return lib.gva_decode_step_static(ctypes.byref(d), q, A, A, A, A, None, None, S, rows, o, lse, None)
+
+    huge = dims(batch=64, n_heads=64, n_groups=8, t_max=65536)
+    assert gva.gva_decode_workspace_size(huge, 256) > gva.GVA_STATIC_SCRATCH_BYTES
+    assert st(huge, S=256) == gva.GVA_ERR_SCRATCH
+    rag = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
+    assert 0 < gva.gva_decode_workspace_size(rag, 16, 1696) <= gva.GVA_STATIC_SCRATCH_BYTES
+    assert st(rag, S=16, rows=1696, q=None) == gva.GVA_ERR_INVALID_ARG
+    assert st(rag, S=16, rows=1696, lse=None) == gva.GVA_ERR_INVALID_ARG
+    assert st(rag, S=0) == gva.GVA_ERR_INVALID_ARG
+    assert st(dims(d_v=96), S=1) == gva.GVA_ERR_UNSUPPORTED
