@@ -171,12 +171,13 @@ int gva_absorb_query(const gva_dims* dims, const void* q, const void* m,
 /*
  * gva_decode_attention -- the attention steps of Algorithm 1 over split s
  * of every sequence, for every (b, h, s):
- *   rows    P = [s*c_b, e),  e = min(L_b, (s+1)*c_b) for s < S-1, e = L_b
- *           for s = S-1;  L_b = lens[b] (clamped to [0, T]),  S = num_splits,
- *           c_b = split_rows when split_rows > 0 (fixed chunks: every
- *           split of every sequence gets the same rows, for ragged
- *           batches), else c_b = 32 * ceil(ceil(L_b / S) / 32) (even
- *           splits per sequence)
+ *   rows    P = [s*c_b, min(L_b, (s+1)*c_b)),  L_b = lens[b] (clamped to
+ *           [0, T]),  S = num_splits,  c_b = 32 * ceil(ceil(L_b / n_b) / 32):
+ *           the first n_b splits share the rows evenly and the rest are
+ *           empty, with n_b = S when split_rows == 0 (even splits), else
+ *           n_b = ceil(L_b / split_rows) clamped to [1, S] (bounded chunks:
+ *           no split of more than split_rows rows unless S such splits
+ *           cannot cover L_b, for batches of unequal lengths)
  *   score   x_t = scale * ( q~_h . v_cache[b][g(h)][t] + q^rope_h . kr_cache[b][t] )
  *   o_part[b][h][s][:] = sum_{t in P} softmax(x)_t v_cache[b][g(h)][t][:]
  *   lse_part[b][h][s]  = log sum_{t in P} exp(x_t)       (natural log)
@@ -416,7 +417,7 @@ int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, v
  * (0 = unknown: every sequence taken as max_len), on a device with n_cu
  * compute units (0 = ask the current device).  Returns num_splits in
  * [1, GVA_MAX_SPLITS]; when split_rows is non-NULL it receives the
- * split_rows to pass with it (0 = even splits; fixed chunks are chosen for
+ * split_rows to pass with it (0 = even splits; bounded chunks are chosen for
  * widely spread lengths).  With split_rows NULL the plan uses even splits
  * only.  Pure host code; enqueues nothing.
  */
@@ -428,10 +429,13 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
  * num_splits splits (split_rows as for that call) should take the raw query
  * and absorb it in the attention kernel (the fused path), 0 if one
  * gva_absorb_query call ahead of it costs less.  The fused path pays for an
- * absorption in every workgroup; it wins while all B * G * splits
- * workgroups (fixed chunks: B * splits rounded up to 8, times G) are resident at once,
- * two per CU on a device with n_cu compute units (0 = ask the current
- * device).  Returns 0 for invalid dims.  Pure host code; enqueues nothing.
+ * absorption in every workgroup (H/G maps of d_v x d_c, read from the
+ * L2): it wins while all the launch's workgroups (B * splits rounded up to
+ * 8, times G) are resident at once, two per CU on a device with n_cu
+ * compute units (0 = ask the current device), or, with bounded chunks,
+ * while a chunk's split_rows value rows are at least as many as the map
+ * rows a workgroup reads (split_rows >= (H/G) d_c).  Returns 0 for
+ * invalid dims.  Pure host code; enqueues nothing.
  */
 int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu);
 

@@ -146,41 +146,39 @@ __device__ __forceinline__ int clamp_len(const int32_t* lens, int b, int t_max) 
   return L < 0 ? 0 : (L > t_max ? t_max : L);
 }
 
-// Split s of a sequence with L rows covers [s*c, e): e = min(L, (s+1)*c)
-// for s < S-1 and e = L for the last split.  c is the caller's fixed chunk
-// when positive (a multiple of kTileRows), else the even rule
-// c = kTileRows * ceil(ceil(L / S) / kTileRows), under which the last split
-// ends at L anyway.
-__device__ __forceinline__ void split_rows(int L, int S, int fixed, int s, int& r0, int& r1) {
-  int chunk = fixed;
-  if (chunk <= 0) {
-    const int per = (L + S - 1) / S;
-    chunk = ((per + kTileRows - 1) / kTileRows) * kTileRows;
-  }
-  const long long a = (long long)chunk * s;
-  const long long e = s == S - 1 ? (long long)L : (long long)chunk * (s + 1);
+// Splits of a sequence with L rows: the first n of its S splits hold its
+// rows, evenly: split s covers [s*k, min(L, (s+1)*k)) with
+// k = kTileRows * ceil(ceil(L / n) / kTileRows), and splits from n on are
+// empty.  Even splits (split_rows = 0): n = S.  Bounded chunks (split_rows
+// = c > 0, a multiple of kTileRows): n = ceil(L / c), at least 1 and at
+// most S, so every split holds at most c rows (unless S splits of c rows
+// cannot cover L) and the splits of one sequence are equal.
+__device__ __forceinline__ int split_count(int L, int S, int c) {
+  if (c <= 0) return S;
+  const int n = (L + c - 1) / c;
+  return n < 1 ? 1 : (n > S ? S : n);
+}
+
+__device__ __forceinline__ void split_rows(int L, int S, int c, int s, int& r0, int& r1) {
+  const int n = split_count(L, S, c);
+  const int per = (L + n - 1) / n;
+  const long long k = (long long)((per + kTileRows - 1) / kTileRows) * kTileRows;
+  const long long a = k * s, e = k * (s + 1);
   r0 = (int)(a < L ? a : L);
   r1 = (int)(e < L ? e : L);
 }
 
-// Workgroup index -> logical work item, XCD-aware.  The dispatcher deals
-// consecutive workgroup ids round-robin over the 8 XCDs; this mapping gives
-// each XCD one contiguous range of logical items, in order, so neighbouring
-// items (the G groups of one (sequence, split), which read the same shared
-// positional-key rows) run together on one XCD and share its L2.
-__device__ __forceinline__ int xcd_remap(int x, int n) {
-  const int per = n / 8, rem = n % 8;
-  const int xcd = x % 8, slot = x / 8;
-  return xcd * per + (xcd < rem ? xcd : rem) + slot;
-}
-
-// Workgroup -> (sequence b, split s, group g).  The G groups of one
-// (b, s) always land on one XCD, next to each other.
-//  - Even splits: XCD-contiguous items (xcd_remap), B * S * G workgroups.
-//  - Fixed chunks (see chunk_item): the (b, s) slots in the order full
-//    chunks, then partial chunks, then empty slots, dealt round-robin over
-//    the XCDs; the grid is B * S rounded up to 8, times G, and workgroups
-//    past B * S are padding and return false.
+// Workgroup -> (sequence b, split s, group g).  The dispatcher deals
+// consecutive workgroup ids round-robin over the 8 XCDs, and each XCD
+// reaches HBM through its own share of the fabric: an XCD given more bytes
+// than the others finishes last and sets the launch time.  So the (b, s)
+// slots, numbered k = b S + s (even splits) or in chunk_item's order
+// (bounded chunks), are dealt round-robin over the XCDs, slot k to XCD k mod 8: with
+// even splits an XCD then holds every eighth split of every sequence, the
+// same share of each whatever the lengths.  The G groups of one slot land
+// on one XCD, next to each other, and share the slot's positional-key rows
+// in its L2.  The grid is B * S rounded up to 8, times G; workgroups past
+// B * S are padding and return false.
 // Every scalar argument the decode prologue needs, requested here in one
 // round trip: left to itself the compiler fetches them where first used,
 // several dependent kernel-argument round trips deep.  The memory clobber
@@ -194,15 +192,12 @@ __device__ __forceinline__ void request_args(const DecodeArgs& a) {
                : "memory");
 }
 
-// Fixed-chunk split sizes of sequence bb (0 past the batch): nfull splits
-// of at least c rows, npart (0 or 1) shorter one after them; the other
-// S - nfull - npart splits are empty.
-__device__ __forceinline__ void chunk_counts(const DecodeArgs& p, int bb, int& nfull, int& npart) {
+// Bounded chunks: the splits of sequence bb that hold rows (0 past the
+// batch and for an empty sequence).
+__device__ __forceinline__ int chunk_count(const DecodeArgs& p, int bb) {
   int L = bb < p.B ? p.lens[bb] : 0;
   L = L < 0 ? 0 : (L > p.t_max ? p.t_max : L);
-  const int q = L / p.split_rows;
-  nfull = q < p.S ? q : p.S;
-  npart = (q < p.S && L > q * p.split_rows) ? 1 : 0;
+  return L > 0 ? split_count(L, p.S, p.split_rows) : 0;
 }
 
 __device__ __forceinline__ int wave_sum_int(int v) {
@@ -221,82 +216,76 @@ __device__ __forceinline__ int wave_incl_scan(int v) {
   return v;
 }
 
-// Fixed chunks: slot i of the B * S (sequence, split) slots.  Slots are
-// numbered full chunks first (sequence-major), then the partial chunks,
-// then the empty splits, so the dispatcher hands out every chunk with rows
-// before any workgroup that only records an empty split, and the longer
-// chunks before the shorter ones.  The map is a bijection of [0, B S) onto
-// the slots, found by every wave of the workgroup from the lengths in two
-// levels: lane l first sums the counts of the k = ceil(B / 64) sequences
-// [l k, l k + k) (independent loads), a scan over the lanes finds the block
-// holding slot i, and for k > 1 a second scan over that block's sequences
-// (64 at a time) finds the sequence.  empty: the slot has no rows.
+// Bounded chunks: slot i of the B * S (sequence, split) slots.  Slots are
+// numbered splits with rows first (sequence-major), then the empty splits,
+// so the dispatcher hands out every chunk with rows before any workgroup
+// that only records an empty split.  The map is a bijection of [0, B S)
+// onto the slots, found by every wave of the workgroup from the lengths in
+// two levels: lane l first sums the counts of the k = ceil(B / 64)
+// sequences [l k, l k + k) (independent loads), a scan over the lanes
+// finds the block holding slot i, and for k > 1 a second scan over that
+// block's sequences (64 at a time) finds the sequence.  empty: the slot
+// has no rows.
 __device__ __forceinline__ void chunk_item(const DecodeArgs& p, int i, int& b, int& s, bool& empty) {
   const int lane = threadIdx.x & 63;
   const int k = (p.B + 63) >> 6;
-  int nf_sum = 0, np_sum = 0, nb = 0;
+  int n_sum = 0, nb = 0;
 #pragma unroll 4
   for (int j = 0; j < k; ++j) {
-    int nf, np;
-    chunk_counts(p, lane * k + j, nf, np);
-    nf_sum += nf;
-    np_sum += np;
+    n_sum += chunk_count(p, lane * k + j);
     nb += lane * k + j < p.B ? 1 : 0;
   }
-  const int F = wave_sum_int(nf_sum), P = wave_sum_int(np_sum);
-  const int cat = i < F ? 0 : (i < F + P ? 1 : 2);
-  const int kk = cat == 0 ? i : (cat == 1 ? i - F : i - F - P);
-  auto pick = [&](int nf, int np, int valid) { return cat == 0 ? nf : (cat == 1 ? np : valid * p.S - nf - np); };
-  const int cnt1 = pick(nf_sum, np_sum, nb);
+  const int F = wave_sum_int(n_sum);
+  const bool full = i < F;                     // a split with rows
+  const int kk = full ? i : i - F;
+  // slots of the category per sequence: its splits with rows, or the rest
+  auto pick = [&](int n, int valid) { return full ? n : valid * p.S - n; };
+  const int cnt1 = pick(n_sum, nb);
   const int incl1 = wave_incl_scan(cnt1);
   const int j1 = min(__popcll(__ballot(incl1 <= kk)), 63);   // < 64 whenever i < B S
   int base = __shfl(incl1 - cnt1, j1, 64);
-  // the slot's position within its sequence: full chunk (k - excl), the
-  // partial chunk (after the nf full ones), or an empty split after both
-  auto split_of = [&](int nf, int np, int local) { return cat == 0 ? local : (cat == 1 ? nf : nf + np + local); };
+  // the slot's split within its sequence: the local-th with rows, or the
+  // local-th empty one after those
+  auto split_of = [&](int n, int local) { return full ? local : n + local; };
   b = 0;
   s = 0;
   if (k == 1) {                                // one sequence per lane: found
     b = __builtin_amdgcn_readfirstlane(j1);
-    s = __builtin_amdgcn_readfirstlane(split_of(__shfl(nf_sum, j1, 64), __shfl(np_sum, j1, 64), kk - base));
+    s = __builtin_amdgcn_readfirstlane(split_of(__shfl(n_sum, j1, 64), kk - base));
   } else {
     const int first = j1 * k;
     for (int c = 0; c < k; c += 64) {
       const int bb = first + c + lane;
       const bool in_blk = c + lane < k && bb < p.B;
-      int nf, np;
-      chunk_counts(p, in_blk ? bb : p.B, nf, np);
-      const int cnt = in_blk ? pick(nf, np, 1) : 0;
+      const int n = chunk_count(p, in_blk ? bb : p.B);
+      const int cnt = in_blk ? pick(n, 1) : 0;
       const int incl = base + wave_incl_scan(cnt);
       const int j = __popcll(__ballot(incl <= kk));
       if (j < 64) {
         const int excl = __shfl(incl - cnt, j, 64);
         b = __builtin_amdgcn_readfirstlane(first + c + j);
-        s = __builtin_amdgcn_readfirstlane(split_of(__shfl(nf, j, 64), __shfl(np, j, 64), kk - excl));
+        s = __builtin_amdgcn_readfirstlane(split_of(__shfl(n, j, 64), kk - excl));
         break;
       }
       base = __shfl(incl, 63, 64);
     }
   }
-  empty = cat == 2;
+  empty = !full;
 }
 
 __device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g, bool& empty) {
   const int x = blockIdx.x;
   empty = false;
+  const int slot = x >> 3;                     // the workgroup's place on its XCD (x mod 8)
+  g = slot % p.G;
+  const int i = 8 * (slot / p.G) + (x & 7);
+  if (i >= p.B * p.S) return false;
   if (p.split_rows > 0) {
-    const int slot = x >> 3;
-    g = slot % p.G;
-    const int i = 8 * (slot / p.G) + (x & 7);
-    if (i >= p.B * p.S) return false;
     chunk_item(p, i, b, s, empty);
     return true;
   }
-  const int item = xcd_remap(x, gridDim.x);
-  g = item % p.G;
-  const int bs = item / p.G;
-  b = bs / p.S;
-  s = bs % p.S;
+  b = i / p.S;
+  s = i % p.S;
   return true;
 }
 
@@ -485,9 +474,9 @@ inline float scale_log2(const gva_dims* d) {
 }
 
 // Workgroups of a decode launch (see work_item).
-inline long long decode_grid(const gva_dims* d, int num_splits, int split_rows) {
+inline long long decode_grid(const gva_dims* d, int num_splits) {
   const long long slots = (long long)d->batch * num_splits;
-  return d->n_groups * (split_rows > 0 ? (slots + 7LL) & ~7LL : slots);
+  return d->n_groups * ((slots + 7LL) & ~7LL);
 }
 
 inline int launch_status() {

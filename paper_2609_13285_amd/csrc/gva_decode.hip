@@ -288,18 +288,18 @@ __global__ void __launch_bounds__(128) absorb_f32_kernel(AbsorbParams p) {
 // ========================================================= decode (bf16)
 // HPG heads per group, DV value width, NRC = ceil(d_r / 32) positional
 // K-chunks, DEPTH tiles of V held in registers (DEPTH-1 loads in flight).
-template <int HPG, int DV, int NRC>
+template <int HPG, int DV, int NRC, int NW>
 struct DecodeCfg {
   static constexpr int NC = DV / 32;                         // K-chunks per V row
   static constexpr int NB = DV / 16;                         // 16-wide i-blocks of the output
-  static constexpr int DEPTH = DV >= 128 ? 2 : 3;
+  static constexpr int DEPTH = DV >= 128 ? 2 : (NW > kWaves ? 4 : 3);
   // fused absorption: 16-byte pieces of M_h per lane and load round, one
   // round of 32 where the registers allow it (no spills), else rounds of 16
-  static constexpr int AR = (DV >= 128 && NRC < 2) ? 32 : 16;
+  static constexpr int AR = (DV >= 128 && NRC < 2 && NW <= 8) ? 32 : 16;
   static constexpr int QS_STRIDE = DV + 4;                   // padded LDS rows (floats)
   static constexpr int QR_STRIDE = 32 * NRC + 4;
   static constexpr int LDS_PRO = HPG * (QS_STRIDE + QR_STRIDE);
-  static constexpr int LDS_RED = kWaves * HPG * (DV + 2);
+  static constexpr int LDS_RED = NW * HPG * (DV + 2);
   static constexpr int LDS_FLOATS = LDS_PRO > LDS_RED ? LDS_PRO : LDS_RED;
 };
 
@@ -312,20 +312,21 @@ struct DecodeCfg {
 // addressing of a tile (and of the current row) changes.
 // KR_STREAM loads the positional-key tiles with the non-temporal policy too
 // (decode_kr_stream decides).
-template <int HPG, int DV, int NRC, bool GQA, bool FUSED, bool PAGED, bool KR_STREAM = false>
-__global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p) {
+template <int HPG, int DV, int NRC, bool GQA, bool FUSED, bool PAGED, bool KR_STREAM = false, int NW = kWaves>
+__global__ void __launch_bounds__(64 * NW, NW == kWaves ? 2 : 1) decode_bf16_kernel(DecodeParams p) {
   static_assert(!(GQA && FUSED), "the GQA baseline takes the raw query");
   static_assert(!(GQA && PAGED), "the GQA baseline reads contiguous caches");
   const DecodeArgs a = p.a;
   request_args<FUSED || GQA>(a);
-  using Cfg = DecodeCfg<HPG, DV, NRC>;
+  using Cfg = DecodeCfg<HPG, DV, NRC, NW>;
+  constexpr int NT = 64 * NW;                  // threads per workgroup
   using TileT = Tile<DV, NRC, GQA>;
   constexpr int NC = Cfg::NC, NB = Cfg::NB, DEPTH = Cfg::DEPTH, AR = Cfg::AR;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
 
   int b, s, g;
   bool empty_slot;
-  if (!work_item(a, b, s, g, empty_slot)) return;   // grid padding (fixed chunks)
+  if (!work_item(a, b, s, g, empty_slot)) return;   // grid padding
   const int tid = threadIdx.x, lane = tid & 63;
   const int w = __builtin_amdgcn_readfirstlane(tid >> 6);   // wave index, uniform (SGPR)
   const int n = lane & 15, qd = lane >> 4;     // MFMA column / row slot and 16-lane row
@@ -353,7 +354,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   auto write_empty = [&]() {                   // an empty split past the first: lse only
     if (tid < HPG) a.lse_part[((int64_t)b * a.H + h0 + tid) * a.S + s] = -INFINITY;
   };
-  if (empty_slot && s > 0) {                   // fixed chunks: a split with no rows
+  if (empty_slot && s > 0) {                   // bounded chunks: a split with no rows
     write_empty();
     return;
   }
@@ -396,7 +397,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int nrounds = ((a.d_c + 127) / 128) * ARB;
   const int a_row = lane >> 4, a_col = 8 * (lane & 15);
   const int npair = a.d_r / 2;
-  const int ptid = kThreads - 1 - tid;
+  const int ptid = NT - 1 - tid;
   const bool has_pair = FUSED && ptid < HPG * npair;
   const int pair_h = npair > 0 ? ptid / npair : 0, pair_i = npair > 0 ? ptid % npair : 0;
   uint32_t rq_bits = 0u;                       // the raw positional pair (bf16 x 2)
@@ -449,7 +450,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   if constexpr (PAGED) {
     const int npg = (r1 + PR - 1) / PR - pg0;
     const int32_t* bt = a.block_table + (int64_t)b * a.max_pages + pg0;
-    for (int i = tid; i < npg; i += kThreads) {
+    for (int i = tid; i < npg; i += NT) {
       const int id = bt[i];
       split_pages[i] = id < 0 ? 0 : (id >= a.n_pages ? a.n_pages - 1 : id);
     }
@@ -489,8 +490,8 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
   const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * a.d_r * 2;
 
   const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
-  const int my_tiles = ntiles > w ? (ntiles - w + kWaves - 1) / kWaves : 0;
-  auto tile_row = [&](int j) { return r0 + (w + kWaves * j) * kTileRows; };
+  const int my_tiles = ntiles > w ? (ntiles - w + NW - 1) / NW : 0;
+  auto tile_row = [&](int j) { return r0 + (w + NW * j) * kTileRows; };
   // Paged: the descriptors of the page holding a tile (a tile never spans
   // pages: pages are whole multiples of 32 rows), ending at the split's last
   // layout tile like the contiguous ones; a tile past it gets empty ones.
@@ -644,7 +645,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
     // the first round (loaded before the tiles) in straight-line code, so
     // its waits count only its own loads; then the rest
     if (w < HPG) absorb_round(w, 0);
-    for (int hl = w; hl < HPG; hl += kWaves)
+    for (int hl = w; hl < HPG; hl += NW)
       for (int ro = hl == w ? 1 : 0; ro < nrounds; ++ro) {
         load_round(hl, ro);
         absorb_round(hl, ro);
@@ -661,7 +662,7 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       qrs[pair_h * Cfg::QR_STRIDE + 2 * pair_i + 1] = y1;
     }
     if constexpr (NRC > 0) {
-      for (int idx = tid; idx < HPG * 32 * NRC; idx += kThreads) {
+      for (int idx = tid; idx < HPG * 32 * NRC; idx += NT) {
         const int j = idx % (32 * NRC);
         if (j >= a.d_r) qrs[(idx / (32 * NRC)) * Cfg::QR_STRIDE + j] = 0.f;
       }
@@ -836,15 +837,15 @@ __global__ void __launch_bounds__(kThreads, 2) decode_bf16_kernel(DecodeParams p
       for (int jj = 0; jj < 4; ++jj) rec[2 + 16 * ib + 4 * qd + jj] = acc[ib][jj];
   }
   __syncthreads();
-  for (int idx = tid; idx < HPG * DV; idx += kThreads) {
+  for (int idx = tid; idx < HPG * DV; idx += NT) {
     const int hl = idx / DV, i = idx % DV;
     float mx = -INFINITY;
 #pragma unroll
-    for (int ww = 0; ww < kWaves; ++ww) mx = fmaxf(mx, red[(ww * HPG + hl) * RS]);
+    for (int ww = 0; ww < NW; ++ww) mx = fmaxf(mx, red[(ww * HPG + hl) * RS]);
     float o = 0.f, lsum = 0.f;
     if (mx != -INFINITY) {
 #pragma unroll
-      for (int ww = 0; ww < kWaves; ++ww) {
+      for (int ww = 0; ww < NW; ++ww) {
         const float* rec = red + (ww * HPG + hl) * RS;
         const float sc = rec[0] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(rec[0] - mx);
         lsum += rec[1] * sc;
@@ -875,7 +876,7 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 
   int b, s, g;
   bool empty_slot;
-  if (!work_item(p.a, b, s, g, empty_slot)) return;   // grid padding (fixed chunks)
+  if (!work_item(p.a, b, s, g, empty_slot)) return;   // grid padding
   const int tid = threadIdx.x, lane = tid & 63, w = tid >> 6;
   const int hpg = p.a.H / p.a.G, h0 = g * hpg;
   const int DV = p.a.d_v, DR = p.a.d_r;
@@ -1101,8 +1102,8 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 // single pass keeps a running log-sum-exp and rescales the running sum;
 // the split loads do not depend on each other, so they overlap.
 constexpr int kCombineMaxDv = 256;
-constexpr long long kChunkItemsPerCu = 2;         // fixed-chunk splits: chunks per CU
-constexpr long long kMinChunkBytes = 128 << 10;   // fixed-chunk splits: value bytes per chunk
+constexpr long long kChunkItemsPerCu = 2;         // bounded chunks: chunks per CU
+constexpr long long kMinChunkBytes = 128 << 10;   // bounded chunks: value bytes per chunk
 
 __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   const int lane = threadIdx.x & 63;
@@ -1237,26 +1238,67 @@ DecodeFn pick_dv(int dv, int nrc, bool fused, bool paged, bool kr_stream) {
   return nullptr;
 }
 
-template <int DV>
+template <int DV, int NW>
 DecodeFn pick_gqa_hpg(int hpg) {
   switch (hpg) {
-    case 1: return decode_bf16_kernel<1, DV, 0, true, false, false>;
-    case 2: return decode_bf16_kernel<2, DV, 0, true, false, false>;
-    case 4: return decode_bf16_kernel<4, DV, 0, true, false, false>;
-    case 8: return decode_bf16_kernel<8, DV, 0, true, false, false>;
+    case 1: return decode_bf16_kernel<1, DV, 0, true, false, false, false, NW>;
+    case 2: return decode_bf16_kernel<2, DV, 0, true, false, false, false, NW>;
+    case 4: return decode_bf16_kernel<4, DV, 0, true, false, false, false, NW>;
+    case 8: return decode_bf16_kernel<8, DV, 0, true, false, false, false, NW>;
   }
   return nullptr;
 }
 
-DecodeFn pick_gqa_decode(int hpg, int dv) {
-  switch (dv) {
-    case 64: return pick_gqa_hpg<64>(hpg);
-    case 128: return pick_gqa_hpg<128>(hpg);
+// Waves per decode workgroup.  A launch with few workgroups leaves most CUs
+// idle and is bound by each stream's chain of memory round trips, not by
+// HBM: its workgroups take eight waves, so twice as many of each stream's
+// tiles are in flight at once (one such workgroup per CU; sixteen waves
+// would leave 128 registers per wave, too few for the tiles in flight).
+int decode_waves(long long grid, int n_cu) {
+  return 2 * grid <= n_cu ? 8 : kWaves;
+}
+
+DecodeFn pick_gqa_decode(int hpg, int dv, int nw) {
+  switch (dv * 100 + nw) {
+    case 6404: return pick_gqa_hpg<64, 4>(hpg);
+    case 6408: return pick_gqa_hpg<64, 8>(hpg);
+    case 12804: return pick_gqa_hpg<128, 4>(hpg);
+    case 12808: return pick_gqa_hpg<128, 8>(hpg);
   }
   return nullptr;
 }
 
-DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged, bool kr_stream) {
+// fused absorption, contiguous caches, NW waves (the few-workgroup launches)
+template <int HPG, int DV, int NW>
+DecodeFn pick_wide_nrc(int nrc) {
+  switch (nrc) {
+    case 0: return decode_bf16_kernel<HPG, DV, 0, false, true, false, false, NW>;
+    case 1: return decode_bf16_kernel<HPG, DV, 1, false, true, false, false, NW>;
+    case 2: return decode_bf16_kernel<HPG, DV, 2, false, true, false, false, NW>;
+  }
+  return nullptr;
+}
+
+template <int HPG>
+DecodeFn pick_wide(int dv, int nrc, int nw) {
+  switch (dv * 100 + nw) {
+    case 6408: return pick_wide_nrc<HPG, 64, 8>(nrc);
+    case 12808: return pick_wide_nrc<HPG, 128, 8>(nrc);
+  }
+  return nullptr;
+}
+
+DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged, bool kr_stream, int nw) {
+  if (nw != kWaves) {
+    if (!fused || paged) return nullptr;
+    switch (hpg) {
+      case 1: return pick_wide<1>(dv, nrc, nw);
+      case 2: return pick_wide<2>(dv, nrc, nw);
+      case 4: return pick_wide<4>(dv, nrc, nw);
+      case 8: return pick_wide<8>(dv, nrc, nw);
+    }
+    return nullptr;
+  }
   switch (hpg) {
     case 1: return pick_dv<1>(dv, nrc, fused, paged, kr_stream);
     case 2: return pick_dv<2>(dv, nrc, fused, paged, kr_stream);
@@ -1405,7 +1447,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
   if (st != GVA_OK) return st;
 
   const int hpg = dims->n_heads / dims->n_groups;
-  const long long n_items = decode_grid(dims, num_splits, split_rows);
+  const long long n_items = decode_grid(dims, num_splits);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p{};
@@ -1446,10 +1488,11 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
     // the fused prologue absorbs at least one 32-column chunk of the query
     if (fused && dims->d_c == 0) return GVA_ERR_UNSUPPORTED;
     const int nrc = (dims->d_r + 31) / 32;
-    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr, decode_kr_stream(dims));
+    const int nw = fused && paging == nullptr ? decode_waves(n_items, device_cu_count()) : kWaves;
+    DecodeFn fn = pick_bf16_decode(hpg, dims->d_v, nrc, fused, paging != nullptr, decode_kr_stream(dims), nw);
     if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
     if (!launch) return GVA_OK;
-    hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, s, p);
+    hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(64 * nw), 0, s, p);
   } else {
     if (paging != nullptr) return GVA_ERR_UNSUPPORTED;       // paged caches: bf16 only
     if (dims->d_v > kF32MaxDv || dims->d_c > 512 || dims->d_r > kF32MaxDr || hpg > kF32MaxHpg)
@@ -1660,10 +1703,11 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   if (dims->t_max % kLayoutRows != 0) return GVA_ERR_UNSUPPORTED;
   if ((double)dims->t_max * dims->d_v * 2.0 >= 2147483648.0 - 16777216.0) return GVA_ERR_UNSUPPORTED;
   const int hpg = dims->n_heads / dims->n_groups;
-  DecodeFn fn = pick_gqa_decode(hpg, dims->d_v);
-  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const long long n_items = decode_grid(dims, num_splits, split_rows);
+  const long long n_items = decode_grid(dims, num_splits);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
+  const int nw = decode_waves(n_items, device_cu_count());
+  DecodeFn fn = pick_gqa_decode(hpg, dims->d_v, nw);
+  if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p{};
   memset(&p, 0, sizeof(p));
@@ -1685,7 +1729,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   p.a.split_rows = split_rows;
   const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
   p.a.scale_log2 = (float)(sc * kLog2e);
-  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
+  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(64 * nw), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
 }
 
@@ -1748,7 +1792,11 @@ int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, v
 int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu) {
   if (check_dims(dims) != GVA_OK || num_splits < 1 || split_rows < 0) return 0;
   if (n_cu <= 0) n_cu = device_cu_count();
-  return decode_grid(dims, num_splits, split_rows) <= 2LL * n_cu ? 1 : 0;
+  if (decode_grid(dims, num_splits) <= 2LL * n_cu) return 1;
+  // bounded chunks: each workgroup streams up to split_rows value rows
+  // against the (H/G) d_c map rows of its absorption
+  const long long map_rows = (long long)(dims->n_heads / dims->n_groups) * dims->d_c;
+  return split_rows > 0 && split_rows >= map_rows ? 1 : 0;
 }
 
 int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
@@ -1762,9 +1810,9 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
   const long long row_bytes = (long long)dims->d_v * (long long)elem_size(dims);
   const bool spread = 2 * total_len < (long long)dims->batch * max_len;
   if (spread && split_rows != nullptr) {
-    // Ragged lengths: fixed chunks, so every workgroup streams about the
+    // Ragged lengths: bounded chunks, so every workgroup streams about the
     // same bytes whatever its sequence's length.  Chunks with rows number
-    // at most stream_rows / c + streams (one partial chunk per stream);
+    // at most stream_rows / c + streams (ceil(L / c) < L / c + 1);
     // c is chosen so that they fit the kChunkItemsPerCu resident
     // workgroups per CU, one dispatch round with no tail, when the streams
     // leave room for that; none shorter than kMinChunkBytes of value rows.

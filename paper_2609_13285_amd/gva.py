@@ -100,6 +100,50 @@ def lib() -> ctypes.CDLL:
     return _lib
 
 
+class _Recorder:
+    """Stands in for the loaded library while prepare() runs a binding call:
+    records each C call with its marshalled arguments instead of making it."""
+
+    def __init__(self, real):
+        self._real = real
+        self.calls = []
+
+    def __getattr__(self, name):
+        fn = getattr(self._real, name)
+
+        def record(*args):
+            self.calls.append((name, fn, args))
+            return GVA_OK
+        return record
+
+
+def prepare(call, *args, **kwargs):
+    """Check and marshal one binding call now (``call`` is one of this
+    module's gva_* functions, with its usual arguments) and return a
+    zero-argument function that makes the same C calls again -- the same
+    device pointers, sizes and stream -- without the per-call Python checks.
+    For loops whose tensors stay where they are (timing, serving); the
+    caller keeps the tensors alive.  Each re-issue still checks the status
+    the library returns."""
+    global _lib
+    real = lib()
+    rec = _Recorder(real)
+    _lib = rec
+    try:
+        call(*args, **kwargs)
+    finally:
+        _lib = real
+    calls = tuple(rec.calls)
+
+    def run():
+        for name, fn, a in calls:
+            st = fn(*a)
+            if st != GVA_OK:
+                raise GvaError(name, st)
+    run.calls = calls
+    return run
+
+
 def status_string(status: int) -> str:
     return lib().gva_status_string(int(status)).decode()
 

@@ -12,20 +12,21 @@ import torch
 def split_bounds(lens: torch.Tensor, num_splits: int, tile: int = 32, split_rows: int = 0):
     """Row ranges [begin, end) of every split, per sequence: [S][B] each.
 
-    Split s of a sequence with L rows covers [s*c, min(L, (s+1)*c)), except
-    that the last split ends at L.  c = split_rows when it is positive,
-    else c = tile * ceil(ceil(L / S) / tile).  Trailing splits may be empty.
+    The first n splits of a sequence with L rows share them evenly: split s
+    covers [s*c, min(L, (s+1)*c)) with c = tile * ceil(ceil(L / n) / tile),
+    and splits from n on are empty.  n = S for even splits (split_rows = 0);
+    with split_rows > 0 (bounded chunks) n = ceil(L / split_rows), clamped
+    to [1, S].
     """
     L = lens.to(torch.int64).clamp(min=0)
     if split_rows > 0:
-        chunk = torch.full_like(L, int(split_rows))
+        n = ((L + split_rows - 1) // split_rows).clamp(min=1, max=num_splits)
     else:
-        per = (L + num_splits - 1) // num_splits
-        chunk = ((per + tile - 1) // tile) * tile
+        n = torch.full_like(L, num_splits)
+    per = (L + n - 1) // n
+    chunk = ((per + tile - 1) // tile) * tile
     begins, ends = [], []
     for s in range(num_splits):
-        b = torch.minimum(chunk * s, L)
-        e = L if s == num_splits - 1 else torch.minimum(chunk * (s + 1), L)
-        begins.append(b.to(torch.int32))
-        ends.append(e.to(torch.int32))
+        begins.append(torch.minimum(chunk * s, L).to(torch.int32))
+        ends.append(torch.minimum(chunk * (s + 1), L).to(torch.int32))
     return begins, ends

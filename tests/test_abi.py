@@ -152,12 +152,16 @@ def test_pick_splits_is_host_only_and_bounded():
     # fused only while the B * G * S workgroups are all resident (two per CU)
     assert gva.gva_prefer_fused(d, 2, 0, 256) and not gva.gva_prefer_fused(d, 3, 0, 256)
     assert gva.gva_prefer_fused(d3, 16, 0, 256) and not gva.gva_prefer_fused(d3, 17, 0, 256)
-    # fixed chunks pad the splits to a multiple of 8
+    # bounded chunks pad the splits to a multiple of 8
     assert gva.gva_prefer_fused(d3, 16, 64, 256) and not gva.gva_prefer_fused(d3, 9, 64, 128)
     assert not gva.gva_prefer_fused(d3, 0, 0, 256) and not gva.gva_prefer_fused(d3, 2, -32, 256)
+    # bounded chunks of at least (H/G) d_c rows stay fused past the resident grid
+    rag = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)    # 8 heads x d_c 128 = 1024 map rows
+    assert gva.gva_prefer_fused(rag, 16, 1024, 256) and gva.gva_prefer_fused(rag, 16, 1696, 256)
+    assert not gva.gva_prefer_fused(rag, 16, 992, 256) and not gva.gva_prefer_fused(rag, 16, 0, 256)
 
 
-def test_pick_splits_fixed_chunks_for_ragged_lengths():
+def test_pick_splits_bounded_chunks_for_ragged_lengths():
     d4 = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
     S, rows = gva.gva_pick_splits(d4, 32768, 64 * 6000, 256)
     assert rows > 0 and rows % 32 == 0
@@ -337,10 +341,11 @@ def test_decode_workspace_size():
     assert gva.gva_prefer_fused(big, S, 0, 256)
     rows = 32 * 32
     assert gva.gva_decode_workspace_size(big, S) == _ws_round(rows * S * 128 * 4) + _ws_round(rows * S * 4)
-    # ragged batch, fixed chunks: separate absorption (q~ and the rotated
-    # positional query) plus the partials
+    # ragged batch, bounded chunks shorter than a group's map rows (8 heads
+    # x d_c = 1024): separate absorption (q~ and the rotated positional
+    # query) plus the partials
     rag = dims(batch=64, n_heads=16, n_groups=2, t_max=32768)
-    S, c = 16, 1696
+    S, c = 16, 992
     assert not gva.gva_prefer_fused(rag, S, c, 256)
     rows = 64 * 16
     expect = (_ws_round(rows * 128 * 4) + _ws_round(rows * 16 * 4) + _ws_round(rows * S * 128 * 4)

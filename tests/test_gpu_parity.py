@@ -73,7 +73,7 @@ def test_split_partials_match_oracle(name):
 def test_random_shapes_sweep():
     # 40 seeded random cases over the supported shape space: H/G, G, d_v,
     # d_c (incl. widths that are not powers of two), d_r (incl. 0), batch,
-    # capacity, lengths (0, 1, capacity and random), even and fixed-chunk
+    # capacity, lengths (0, 1, capacity and random), even and bounded-chunk
     # splits, fused and separate absorption, bf16 and fp32 storage
     rng = torch.Generator().manual_seed(2609)
     pick = lambda xs: xs[int(torch.randint(len(xs), (1,), generator=rng))]
@@ -199,7 +199,7 @@ def test_split_count_invariance_and_determinism():
     # up to GVA_MAX_SPLITS: 256 even splits of 2048 rows are 64 of 32 rows
     # and 192 empty ones
     outs = {S: run_decode(w, dev, S)[0] for S in (1, 2, 7, 64, gva.GVA_MAX_SPLITS)}
-    outs["chunks"] = run_decode(w, dev, 64, split_rows=32)[0]     # 64 fixed chunks of 32 rows
+    outs["chunks"] = run_decode(w, dev, 64, split_rows=32)[0]     # 64 bounded chunks of 32 rows
     for S, o in outs.items():
         assert max_abs(o, outs[1]) <= 2 * QUALITY["bf16"], S
     again = run_decode(w, dev, 7)[0]
@@ -355,7 +355,7 @@ def test_decode_on_a_side_stream():
 
 STEP_CASES = [
     # (workload, lengths, num_splits, split_rows): one split fused; several
-    # splits fused; fixed chunks over a grid past two workgroups per CU, so
+    # splits fused; bounded chunks over a grid past two workgroups per CU, so
     # the absorption runs as its own launch into the workspace; fp32
     (gva_inputs.workload("gva350m_b8_t2k"), None, 1, 0),
     (gva_inputs.workload("gva350m_b8_t2k"), None, 3, 0),
@@ -581,7 +581,7 @@ def test_one_gib_value_stream():
     # a single value stream of 2^22 rows x 128 bf16 = 1 GiB (the layout
     # allows up to 2 GiB - 16 MiB per stream): the 32-bit buffer offsets
     # near the top of the stream, one workgroup streaming all of it, even
-    # splits and fixed chunks, a length just short of capacity, and the
+    # splits and bounded chunks, a length just short of capacity, and the
     # current row appended at row 2^22 - 6
     T = 1 << 22
     w = gva_inputs.Workload("one_gib", 1, T, 2, 1, 128, 64, 16)
@@ -607,12 +607,12 @@ def test_one_gib_value_stream():
         torch.cuda.empty_cache()
 
 
-# ------------------------------------------- fixed-chunk splits (ragged batches)
+# ------------------------------------------- bounded-chunk splits (ragged batches)
 @pytest.mark.parametrize("dtype", ["bf16", "f32"])
 @pytest.mark.parametrize("fused", [True, False])
-def test_fixed_chunk_splits_match_oracle(dtype, fused):
-    # every split of every sequence gets split_rows rows; too few splits
-    # leave the remainder to the last one; empty splits write only their lse
+def test_bounded_chunk_splits_match_oracle(dtype, fused):
+    # no split of more than split_rows rows, a sequence's splits even; too
+    # few splits share the rows evenly; empty splits write only their lse
     w = gva_inputs.Workload("chunks", 6, 1024, 16, 2, 128 if dtype == "bf16" else 64, 64, 16,
                             dtype=dtype)
     lens = torch.tensor([1024, 1, 0, 333, 64, 700], dtype=torch.int32)
@@ -626,8 +626,8 @@ def test_fixed_chunk_splits_match_oracle(dtype, fused):
         _check(w, o, lse, o_ref, lse_ref, f"chunks/{dtype}/fused={fused}/S{S}/rows{rows}")
 
 
-def test_fixed_chunks_with_current_row():
-    # the append folded into the attention launch, with fixed chunks: the
+def test_bounded_chunks_with_current_row():
+    # the append folded into the attention launch, with bounded chunks: the
     # chunk holding row len-1 appends it
     w = gva_inputs.Workload("chunks_pending", 4, 512, 8, 2, 128, 128, 16)
     lens = torch.tensor([512, 97, 1, 256], dtype=torch.int32)
@@ -661,8 +661,8 @@ LARGE_BATCH_CHUNKS = [
 
 @pytest.mark.parametrize("fused", [True, False])
 @pytest.mark.parametrize("cfg", LARGE_BATCH_CHUNKS, ids=lambda c: f"B{c[0]}")
-def test_fixed_chunk_slots_large_batch(cfg, fused):
-    # fixed chunks over more than 64 sequences and B * S not a multiple of 8
+def test_bounded_chunk_slots_large_batch(cfg, fused):
+    # bounded chunks over more than 64 sequences and B * S not a multiple of 8
     # (padding workgroups): every (b, h, s) partial is written exactly as the
     # oracle's split says, the buffers having been filled with NaN first
     B, T, H, G, dv, dc, dr, plans = cfg
@@ -702,6 +702,51 @@ def test_fixed_chunk_slots_large_batch(cfg, fused):
             assert err <= QUALITY["bf16"], (S, rows, s, err)
 
 
+# Even splits with B * S not a multiple of 8: the (sequence, split) slots are
+# dealt round-robin over the XCDs and the grid is padded to whole rounds of
+# eight slots.  (B, H, G, S): 21 x 8 streams (>= half the CUs: four waves
+# per workgroup), and 5 x 8 x 3 (few workgroups: eight waves each).
+EVEN_PADDED = [(21, 32, 8, 1), (21, 32, 8, 3), (5, 32, 8, 3), (7, 16, 4, 2)]
+
+
+@pytest.mark.parametrize("fused", [True, False])
+@pytest.mark.parametrize("cfg", EVEN_PADDED, ids=lambda c: f"B{c[0]}H{c[1]}G{c[2]}S{c[3]}")
+def test_even_split_slots_padded_grid(cfg, fused):
+    # every (b, h, s) partial written exactly as the oracle's split says, the
+    # buffers filled with NaN first
+    B, H, G, S = cfg
+    w = gva_inputs.Workload(f"even_b{B}", B, 640, H, G, 128, 128, 16)
+    g = torch.Generator().manual_seed(41)
+    lens = torch.randint(0, w.t_max + 1, (w.batch,), generator=g, dtype=torch.int32)
+    lens[0], lens[-1] = w.t_max, 0
+    inp = gva_inputs.make_inputs(w, 43, lens=lens)
+    d = dims_of(w)
+    dev = upload(inp)
+    assert (w.batch * S) % 8 != 0
+    note(f"even slots B{B} H{H} G{G} S={S} fused={fused}")
+    q_abs = q_rot = None
+    if not fused:
+        q_abs = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
+        q_rot = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+        gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot)
+    o_part = torch.full((w.batch, w.n_heads, S, w.d_v), math.nan, device="cuda")
+    lse_part = torch.full((w.batch, w.n_heads, S), math.nan, device="cuda")
+    gva.gva_decode_attention(d, dev["v"], dev["kr"], dev["lens"], S, o_part, lse_part,
+                             q=dev["q"] if fused else None, m=dev["m"] if fused else None,
+                             q_abs=q_abs, q_rot=q_rot)
+    torch.cuda.synchronize()
+    o_part, lse_part = o_part.cpu(), lse_part.cpu()
+    begins, ends = split_bounds(inp["lens"], S)
+    for s in range(S):
+        o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], inp["v"], inp["kr"], inp["lens"],
+                                       t_begin=begins[s], t_end=ends[s])
+        assert not torch.isnan(lse_part[:, :, s]).any(), (cfg, s, "lse not written")
+        assert lse_err(lse_part[:, :, s], lse_ref) <= 1e-3, (cfg, s)
+        live = (ends[s] > begins[s]) | (s == 0)
+        err = max_abs(o_part[live][:, :, s], o_ref[live])
+        assert err <= QUALITY["bf16"], (cfg, s, err)
+
+
 # ------------------------------------------------- writes stay in bounds
 _GUARD = 4096          # sentinel elements on each side of an output (16 KB of fp32)
 _SENTINEL = 0x7FC0DEAD  # a NaN bit pattern no kernel writes
@@ -721,7 +766,7 @@ def _guards_intact(big):
 
 def test_outputs_written_only_in_bounds():
     # every output buffer sits between two 16 KB runs of a sentinel; after
-    # absorption, attention (fused and separate, even and fixed-chunk
+    # absorption, attention (fused and separate, even and bounded-chunk
     # splits, bf16 and fp32), combine, the GQA baseline, the ordinary-RoPE
     # contrast and the prefill, the sentinels must be untouched
     for dtype in ("bf16", "f32"):
@@ -892,7 +937,7 @@ def test_paged_decode_matches_oracle(page_rows):
 def test_paged_at_max_pages():
     # a sequence of GVA_MAX_PAGES = 4096 pages of 32 rows (131,072 rows), in
     # random pool order with NaN in the unused pages: one split holds all
-    # 4096 page ids in LDS; also 7 even splits and fixed chunks of 4096 rows
+    # 4096 page ids in LDS; also 7 even splits and bounded chunks of 4096 rows
     page_rows = 32
     w = gva_inputs.Workload("paged_max", 2, gva.GVA_MAX_PAGES * page_rows, 4, 1, 128, 64, 16)
     lens = torch.tensor([w.t_max - 3, 40000], dtype=torch.int32)

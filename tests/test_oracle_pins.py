@@ -263,8 +263,8 @@ def test_position_shift_leaves_output_unchanged(orc):
 @pytest.mark.parametrize("S,rows", [(1, 0), (2, 0), (3, 0), (7, 0), (64, 0),
                                     (5, 32), (2, 32), (20, 8), (1, 64)])
 def test_split_and_combine_equals_unsplit(orc, S, rows):
-    # even splits, and fixed chunks (including too few splits, where the
-    # last split takes every remaining row)
+    # even splits, and bounded chunks (including too few splits, where the
+    # S splits share the rows evenly and exceed the bound)
     q, m, v, kr, lens = tiny_inputs(47, T=150, lens=[150, 61])
     o, lse = orc.decode(q, m, v, kr, lens)
     begins, ends = split_bounds(lens, S, tile=8, split_rows=rows)
@@ -282,14 +282,21 @@ def test_split_bounds_cover_each_sequence(orc, rows):
     for S in (1, 2, 5, 16):
         begins, ends = split_bounds(lens, S, tile=32, split_rows=rows)
         for b in range(lens.numel()):
-            covered = []
+            covered, sizes = [], []
+            L = int(lens[b])
             for s in range(S):
                 bg, en = int(begins[s][b]), int(ends[s][b])
-                assert bg % 32 == 0 or bg == int(lens[b])
-                if rows and s < S - 1:
-                    assert en - bg <= rows          # fixed chunks, the last takes the rest
+                assert bg % 32 == 0 or bg == L
+                if rows and -(-L // rows) <= S:
+                    assert en - bg <= rows          # bounded chunks
                 covered.extend(range(bg, en))
-            assert covered == list(range(int(lens[b])))
+                sizes.append(en - bg)
+            assert covered == list(range(L))
+            # the splits with rows come first, all of one size but the last
+            nz = [z for z in sizes if z > 0]
+            assert sizes[:len(nz)] == nz and len(set(nz[:-1])) <= 1 and (not nz or nz[-1] <= nz[0])
+            if rows and L > 0:
+                assert len(nz) == min(S, -(-L // rows))
 
 
 # ------------------------------------------------------------------ append

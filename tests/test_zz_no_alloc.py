@@ -17,7 +17,7 @@ from paper_2609_13285_amd import gva
 pytestmark = pytest.mark.gpu
 
 CASES = [
-    # ragged lengths, fixed chunks over a grid past two workgroups per CU:
+    # ragged lengths, bounded chunks over a grid past two workgroups per CU:
     # the absorbed queries and the split partials both live in the scratch
     (gva_inputs.Workload("static_ragged", 40, 2048, 16, 2, 128, 128, 16), 8, 256, 31),
     # smaller: three even splits, the absorption fused (partials only)
