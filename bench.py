@@ -546,10 +546,19 @@ def main():
     pend = dict(v_new=dev["v_new"], kr_new=dev["kr_new"] if w.d_r > 0 else None,
                 split_rows=split_rows)
 
+    ws = gva.workspace_for(d, S, split_rows) if paging is None else None
+    one_call = paging is None and args.absorb == "auto"
+
     def step_calls(i, attention_only=False):
-        # Algorithm 1: the attention call appends the current token's rows to
-        # the caches and attends over them in the same launch.
+        # Algorithm 1: the attention launch appends the current token's rows
+        # to the caches and attends over them.  With the library's own
+        # absorption choice the step is one gva_decode_step call (the same
+        # launches as below).
         vc, kc = caches[i]
+        if one_call and not attention_only:
+            gva.gva_decode_step(d, dev["q"], dev["m"], vc, kc, dev["lens"], S, bufs.o, bufs.lse, workspace=ws,
+                                stream=stream, **pend)
+            return
         if not fused and not attention_only:
             gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
         qkw = dict(q=dev["q"], m=dev["m"]) if fused else \
@@ -558,9 +567,10 @@ def main():
             gva.gva_paged_decode_attention(d, paging, vc, kc, dev["block_table"], dev["lens"], S,
                                            bufs.o_part, bufs.lse_part, stream=stream, **qkw, **pend)
         else:
-            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o_part, bufs.lse_part,
-                                     stream=stream, **qkw, **pend)
-        if S > 1 and not attention_only:   # with one split the attention kernel's partial is the output
+            gva.gva_decode_attention(d, vc, kc, dev["lens"], S, bufs.o.unsqueeze(2) if S == 1 else bufs.o_part,
+                                     bufs.lse.unsqueeze(2) if S == 1 else bufs.lse_part, stream=stream,
+                                     **qkw, **pend)
+        if S > 1 and not attention_only:   # one split: the attention writes the output
             gva.gva_combine(d, bufs.o_part, bufs.lse_part, S, bufs.o, bufs.lse, stream)
 
     # Each step's C calls are checked and marshalled once, per cache copy
@@ -584,11 +594,13 @@ def main():
     # launches are timed alone, the same steps' launches back to back between
     # two events (the absorption and combine launches left out, their inputs
     # being in place).
-    single_launch = S == 1 and fused
+    single_launch = fused and S == 1
     if single_launch:
         decode_ms = ms_per_step
         launch_timing = f"the {args.steps} timed steps (each step is this one launch)"
     else:
+        if not fused:    # the attention launches' absorbed queries
+            gva.gva_absorb_query(d, dev["q"], dev["m"], dev["lens"], q_abs, q_rot, stream)
         decode_ms = timed(lambda i: step(i, attention_only=True), args.steps, stream)
         launch_timing = f"{args.steps} attention launches back to back between two events on the launch stream"
     achievable, probe_wg = gva.probe_read_bandwidth(stream=stream)
@@ -649,7 +661,7 @@ def main():
         "cpu_baseline": None,
     }
 
-    o_gpu = (bufs.o_part[:, :, 0] if S == 1 else bufs.o).cpu()
+    o_gpu = (bufs.o_part[:, :, 0] if S == 1 and paging is not None else bufs.o).cpu()
     if paging is not None and args.layers > 0:
         raise SystemExit("--paged times the decode step only")
     if args.layers > 0:
