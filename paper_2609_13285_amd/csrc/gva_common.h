@@ -168,17 +168,31 @@ __device__ __forceinline__ void split_rows(int L, int S, int c, int s, int& r0, 
   r1 = (int)(e < L ? e : L);
 }
 
-// Workgroup -> (sequence b, split s, group g).  The dispatcher deals
-// consecutive workgroup ids round-robin over the 8 XCDs, and each XCD
-// reaches HBM through its own share of the fabric: an XCD given more bytes
-// than the others finishes last and sets the launch time.  So the (b, s)
-// slots, numbered k = b S + s (even splits) or in chunk_item's order
-// (bounded chunks), are dealt round-robin over the XCDs, slot k to XCD k mod 8: with
-// even splits an XCD then holds every eighth split of every sequence, the
-// same share of each whatever the lengths.  The G groups of one slot land
-// on one XCD, next to each other, and share the slot's positional-key rows
-// in its L2.  The grid is B * S rounded up to 8, times G; workgroups past
-// B * S are padding and return false.
+// Workgroup index -> logical work item, XCD-aware.  The dispatcher deals
+// consecutive workgroup ids round-robin over the 8 XCDs; this mapping gives
+// each XCD one contiguous range of logical items, in order.
+__device__ __forceinline__ int xcd_remap(int x, int n) {
+  const int per = n / 8, rem = n % 8;
+  const int xcd = x % 8, slot = x / 8;
+  return xcd * per + (xcd < rem ? xcd : rem) + slot;
+}
+
+// Workgroup -> (sequence b, split s, group g).  Each XCD reaches HBM
+// through its own share of the fabric, so a launch takes as long as its
+// busiest XCD: every XCD must get the same bytes.  The G groups of one
+// (b, s) slot always land on one XCD, next to each other, and share the
+// slot's positional-key rows in its L2.
+//  - Even splits: the slots in split-major order (k = s B + b), each XCD
+//    one contiguous range of them (xcd_remap), B * S * G workgroups.  An
+//    XCD then holds the same splits of consecutive sequences: with S a
+//    multiple of 8, split x of every sequence on XCD x, the same share of
+//    each sequence whatever the lengths; with S = 1, whole sequences that
+//    lie next to each other in memory.
+//  - Bounded chunks (see chunk_item): the (b, s) slots in the order
+//    chunks with rows, then empty slots, dealt round-robin over the XCDs
+//    (slot k to XCD k mod 8), so chunks of every length spread over all of
+//    them; the grid is B * S rounded up to 8, times G, and workgroups past
+//    B * S are padding and return false.
 // Every scalar argument the decode prologue needs, requested here in one
 // round trip: left to itself the compiler fetches them where first used,
 // several dependent kernel-argument round trips deep.  The memory clobber
@@ -276,16 +290,19 @@ __device__ __forceinline__ void chunk_item(const DecodeArgs& p, int i, int& b, i
 __device__ __forceinline__ bool work_item(const DecodeArgs& p, int& b, int& s, int& g, bool& empty) {
   const int x = blockIdx.x;
   empty = false;
-  const int slot = x >> 3;                     // the workgroup's place on its XCD (x mod 8)
-  g = slot % p.G;
-  const int i = 8 * (slot / p.G) + (x & 7);
-  if (i >= p.B * p.S) return false;
   if (p.split_rows > 0) {
+    const int slot = x >> 3;                   // the workgroup's place on its XCD (x mod 8)
+    g = slot % p.G;
+    const int i = 8 * (slot / p.G) + (x & 7);
+    if (i >= p.B * p.S) return false;
     chunk_item(p, i, b, s, empty);
     return true;
   }
-  b = i / p.S;
-  s = i % p.S;
+  const int item = xcd_remap(x, gridDim.x);
+  g = item % p.G;
+  const int k = item / p.G;
+  s = k / p.B;
+  b = k % p.B;
   return true;
 }
 
@@ -474,9 +491,9 @@ inline float scale_log2(const gva_dims* d) {
 }
 
 // Workgroups of a decode launch (see work_item).
-inline long long decode_grid(const gva_dims* d, int num_splits) {
+inline long long decode_grid(const gva_dims* d, int num_splits, int split_rows) {
   const long long slots = (long long)d->batch * num_splits;
-  return d->n_groups * ((slots + 7LL) & ~7LL);
+  return d->n_groups * (split_rows > 0 ? (slots + 7LL) & ~7LL : slots);
 }
 
 inline int launch_status() {

@@ -1449,7 +1449,7 @@ int decode_attention_impl(const gva_dims* dims, const gva_paging* paging, const 
   if (st != GVA_OK) return st;
 
   const int hpg = dims->n_heads / dims->n_groups;
-  const long long n_items = decode_grid(dims, num_splits);
+  const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p{};
@@ -1705,7 +1705,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   if (dims->t_max % kLayoutRows != 0) return GVA_ERR_UNSUPPORTED;
   if ((double)dims->t_max * dims->d_v * 2.0 >= 2147483648.0 - 16777216.0) return GVA_ERR_UNSUPPORTED;
   const int hpg = dims->n_heads / dims->n_groups;
-  const long long n_items = decode_grid(dims, num_splits);
+  const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
   const int nw = decode_waves(n_items, device_cu_count());
   DecodeFn fn = pick_gqa_decode(hpg, dims->d_v, nw);
@@ -1794,7 +1794,7 @@ int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, v
 int gva_prefer_fused(const gva_dims* dims, int32_t num_splits, int32_t split_rows, int32_t n_cu) {
   if (check_dims(dims) != GVA_OK || num_splits < 1 || split_rows < 0) return 0;
   if (n_cu <= 0) n_cu = device_cu_count();
-  if (decode_grid(dims, num_splits) <= 2LL * n_cu) return 1;
+  if (decode_grid(dims, num_splits, split_rows) <= 2LL * n_cu) return 1;
   // bounded chunks: each workgroup streams up to split_rows value rows
   // against the (H/G) d_c map rows of its absorption
   const long long map_rows = (long long)(dims->n_heads / dims->n_groups) * dims->d_c;

@@ -380,7 +380,7 @@ int gva_rope_decode_attention(const gva_dims* dims, const void* q, const void* m
   const int hpg = dims->n_heads / dims->n_groups;
   RopeDecodeFn fn = pick_rope_decode(hpg, dims->d_v, dims->d_c);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const long long n_items = decode_grid(dims, num_splits);
+  const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
 
   RopeDecodeParams p{};

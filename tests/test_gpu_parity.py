@@ -702,10 +702,10 @@ def test_bounded_chunk_slots_large_batch(cfg, fused):
             assert err <= QUALITY["bf16"], (S, rows, s, err)
 
 
-# Even splits with B * S not a multiple of 8: the (sequence, split) slots are
-# dealt round-robin over the XCDs and the grid is padded to whole rounds of
-# eight slots.  (B, H, G, S): 21 x 8 streams (>= half the CUs: four waves
-# per workgroup), and 5 x 8 x 3 (few workgroups: eight waves each).
+# Even splits with B * S not a multiple of 8: the split-major slots in
+# contiguous XCD ranges, some slot's groups on two XCDs.  (B, H, G, S):
+# 21 x 8 streams (>= half the CUs: four waves per workgroup), and 5 x 8 x 3
+# (few workgroups: eight waves each).
 EVEN_PADDED = [(21, 32, 8, 1), (21, 32, 8, 3), (5, 32, 8, 3), (7, 16, 4, 2)]
 
 
