@@ -171,9 +171,9 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
 #pragma unroll
     for (int hl = 0; hl < HPG; ++hl) sp[hl][0] = sp[hl][1] = 0.f;
     const double dw = (double)(row0 - P);
-#pragma unroll
-    for (int nb = 0; nb < NBC; ++nb) {
-      float tr[2][4];                            // [hf][jj]: cos, sin, cos, sin
+    // cos / sin of theta_i (t - P) for this lane's rows and the column
+    // block's pairs: [hf][jj] = cos, sin, cos, sin
+    auto trig = [&](int nb, float (&tr)[2][4]) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const double f = freq[8 * nb + 2 * qd + e];
@@ -187,22 +187,46 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
           tr[hf][2 * e + 1] = __builtin_amdgcn_sinf(rho);
         }
       }
+    };
+    // Software pipeline over the (column block, head) steps: while the
+    // matrix cores run one step's products, the LDS reads of the next
+    // step's W piece and the cos/sin weighting of the previous step's
+    // product issue (the order is pinned by scheduling barriers; left to
+    // itself the compiler serialised read, products and weighting).
+    constexpr int NIT = NBC * HPG;
+    bf16x8 wa[2][NC];
+    f32x4 gt[2][2];
+    float tr[2][2][4];
+    auto load_w = [&](int it, bf16x8 (&dst)[NC]) {
+      const int nb = it / HPG, hl = it % HPG;
 #pragma unroll
-      for (int hl = 0; hl < HPG; ++hl) {
-        bf16x8 wa[NC];
+      for (int c = 0; c < NC; ++c) dst[c] = as_bf16x8(wl[((hl * NC + c) * NBC + nb) * 64 + lane]);
+    };
+    auto weight = [&](int it, const f32x4 (&g)[2], const float (&tw)[2][4]) {
+      const int hl = it % HPG;
 #pragma unroll
-        for (int c = 0; c < NC; ++c) wa[c] = as_bf16x8(wl[((hl * NC + c) * NBC + nb) * 64 + lane]);
-        f32x4 gt[2] = {{0.f, 0.f, 0.f, 0.f}, {0.f, 0.f, 0.f, 0.f}};
+      for (int hf = 0; hf < 2; ++hf)
 #pragma unroll
-        for (int c = 0; c < NC; ++c)
+        for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(g[hf][jj], tw[hf][jj], sp[hl][hf]);
+    };
+    load_w(0, wa[0]);
+    trig(0, tr[0]);
 #pragma unroll
-          for (int hf = 0; hf < 2; ++hf) gt[hf] = mfma16(wa[c], t.v[hf][c], gt[hf]);
+    for (int it = 0; it < NIT; ++it) {
+      const int cur = it & 1;
+      gt[cur][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+      gt[cur][1] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf)
+      for (int c = 0; c < NC; ++c)
 #pragma unroll
-          for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(gt[hf][jj], tr[hf][jj], sp[hl][hf]);
-      }
+        for (int hf = 0; hf < 2; ++hf) gt[cur][hf] = mfma16(wa[cur][c], t.v[hf][c], gt[cur][hf]);
+      __builtin_amdgcn_sched_barrier(0);
+      if (it + 1 < NIT) load_w(it + 1, wa[cur ^ 1]);
+      if (it > 0) weight(it - 1, gt[cur ^ 1], tr[((it - 1) / HPG) & 1]);
+      if ((it + 1) % HPG == 0 && it + 1 < NIT) trig((it + 1) / HPG, tr[((it + 1) / HPG) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    weight(NIT - 1, gt[(NIT - 1) & 1], tr[((NIT - 1) / HPG) & 1]);
     // sum over the four 16-lane rows, then transpose through LDS: lane
     // (n, qd) takes head col_head's rows 16 hf + 4 qd + jj
 #pragma unroll
