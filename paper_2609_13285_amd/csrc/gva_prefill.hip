@@ -246,15 +246,12 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
     // here, tile by tile, instead of being hoisted into registers
     int lo_off = lane;
     asm volatile("" : "+v"(lo_off));
-    f16x8 bp[CB];
-#pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
+    // scores of one column block: the high and the low query parts
+    // accumulate into one sum per 16-row half
+    auto scores = [&](int cb, f32x4 (&sc)[2]) {
       bf16x8 lo[NLO];
 #pragma unroll
       for (int c = 0; c < NLO; ++c) lo[c] = lo_lds[(cb * NLO + c) * 64 + lo_off];
-      // scores: the high and the low query parts accumulate into one sum
-      // per 16-row half
-      f32x4 sc[2];
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
         sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
@@ -269,6 +266,9 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
           if constexpr (!KPACK) sc[hf] = mfma16(t.k[hf][rc], lo[NC + rc], sc[hf]);
         }
       }
+    };
+    // the online softmax of one column block, its weights as fp16
+    auto softmax = [&](int cb, const f32x4 (&sc)[2]) {
       float xv[8];
 #pragma unroll
       for (int k = 0; k < 8; ++k) xv[k] = sc[k >> 2][k & 3];
@@ -301,20 +301,43 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
         pr[k] = __builtin_amdgcn_exp2f(xv[k] - m_use);
         l_run[cb] += pr[k];
       }
-      bp[cb] = to_f16x8(pr);
+      return to_f16x8(pr);
+    };
+    // The next column block's score products are issued before this
+    // block's softmax, so the matrix cores run them while the vector units
+    // work (the order is pinned by scheduling barriers).
+    f16x8 bp[CB];
+    f32x4 sc[2][2];
+    scores(0, sc[0]);
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      if (cb + 1 < CB) scores(cb + 1, sc[(cb + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      bp[cb] = softmax(cb, sc[cb & 1]);
+      __builtin_amdgcn_sched_barrier(0);
     }
+    // P.V over the 2 NC 16-wide output blocks; the identity products that
+    // transpose block k + 1 of V are issued before block k's conversion to
+    // fp16 and its products
+    auto transpose = [&](int k, f32x4 (&tq)[2]) {
+      const int c = k >> 1, half = k & 1;
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      tq[0] = mfma16(t.v[0][c], esel[half], z);
+      tq[1] = mfma16(t.v[1][c], esel[half], z);
+    };
+    f32x4 tq[2][2];
+    transpose(0, tq[0]);
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
+    for (int k = 0; k < 2 * NC; ++k) {
+      if (k + 1 < 2 * NC) transpose(k + 1, tq[(k + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      const f32x4* tk = tq[k & 1];
+      const float tv[8] = {tk[0][0], tk[0][1], tk[0][2], tk[0][3], tk[1][0], tk[1][1], tk[1][2], tk[1][3]};
+      const f16x8 av = to_f16x8(tv);           // bf16 values: exact in fp16 at these magnitudes
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
-        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
-        const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
-        const f16x8 av = to_f16x8(tv);         // bf16 values: exact in fp16 at these magnitudes
-#pragma unroll
-        for (int cb = 0; cb < CB; ++cb) acc[cb][2 * c + half] = mfma16(av, bp[cb], acc[cb][2 * c + half]);
-      }
+      for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp[cb], acc[cb][k]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
   };
 
   for (int jt = 0; jt < my_tiles; jt += DEPTH) {
