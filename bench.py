@@ -370,6 +370,14 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
     def rope(i, with_combine=True):
         (rope_fns if with_combine else rope_only_fns)[i % n]()
 
+    try:                     # the group's W_h must fit one workgroup's LDS
+        rope(0)
+    except gva.GvaError as e:
+        if e.status != gva.GVA_ERR_UNSUPPORTED:
+            raise
+        return {"skipped": f"gva_rope_decode_attention: {gva.status_string(e.status)} at H/G = "
+                           f"{w.heads_per_group}, d_v = {w.d_v}, d_c = {w.d_c} (the W_h of a group's "
+                           f"heads, {w.heads_per_group * w.d_v * w.d_c * 2} bytes, exceed one workgroup's LDS)"}
     for i in range(args.warmup):
         absorbed(i)
         rope(i)
