@@ -206,11 +206,13 @@ def timed(step, steps: int, stream) -> float:
 
 def layer_stack(args, w, inp, d, S, split_rows, fused, dec_b):
     """An N-layer decode step (the step of one token through N attention
-    layers, each with its own caches, query and maps), timed eagerly and as
-    one captured HIP graph.  The library allocates, synchronises and clears
-    nothing, so its launches are captured as they are.  Sets of layer caches
-    rotate like the single-layer caches so no step finds its rows in the
-    MALL."""
+    layers, each with its own caches, query, maps and workspace): one
+    gva_decode_step call per layer, timed three ways -- through the Python
+    binding on every call, with the calls marshalled once (gva.prepare), and
+    as one captured HIP graph per step.  The library allocates, synchronises
+    and clears nothing, so its launches are captured as they are.  Sets of
+    layer caches rotate like the single-layer caches so no step finds its
+    rows in the MALL."""
     n = args.layers
     n_sets = min(8, max(2, math.ceil(2 * MALL_BYTES / (n * dec_b))))
     v_t, kr_t = gva.tiled(inp["v"]), gva.tiled(inp["kr"])
@@ -220,32 +222,26 @@ def layer_stack(args, w, inp, d, S, split_rows, fused, dec_b):
         layer = {k: t.clone() for k, t in small.items()}
         layer["caches"] = [(v_t.cuda(), kr_t.cuda()) for _ in range(n_sets)]
         layer["bufs"] = gva.DecodeBuffers(d, S)
-        layer["q_abs"] = torch.empty(w.batch, w.n_heads, w.d_v, dtype=torch.float32, device="cuda")
-        layer["q_rot"] = torch.empty(w.batch, w.n_heads, w.d_r, dtype=torch.float32, device="cuda")
+        layer["ws"] = gva.workspace_for(d, S, split_rows)
         layers.append(layer)
     del v_t, kr_t
 
-    def run(i):
-        st = torch.cuda.current_stream()      # the capture stream while capturing
+    def run(i, st=None):
+        st = st if st is not None else torch.cuda.current_stream()   # the capture stream while capturing
         for L in layers:
             vc, kc = L["caches"][i % n_sets]
-            pend = dict(v_new=L["v_new"], kr_new=L["kr_new"] if w.d_r > 0 else None,
-                        split_rows=split_rows)
-            if fused:
-                gva.gva_decode_attention(d, vc, kc, L["lens"], S, L["bufs"].o_part, L["bufs"].lse_part,
-                                         q=L["q"], m=L["m"], stream=st, **pend)
-            else:
-                gva.gva_absorb_query(d, L["q"], L["m"], L["lens"], L["q_abs"], L["q_rot"], st)
-                gva.gva_decode_attention(d, vc, kc, L["lens"], S, L["bufs"].o_part, L["bufs"].lse_part,
-                                         q_abs=L["q_abs"], q_rot=L["q_rot"] if w.d_r > 0 else None,
-                                         stream=st, **pend)
-            if S > 1:
-                gva.gva_combine(d, L["bufs"].o_part, L["bufs"].lse_part, S, L["bufs"].o, L["bufs"].lse, st)
+            gva.gva_decode_step(d, L["q"], L["m"], vc, kc, L["lens"], S, L["bufs"].o, L["bufs"].lse,
+                                workspace=L["ws"], v_new=L["v_new"],
+                                kr_new=L["kr_new"] if w.d_r > 0 else None, split_rows=split_rows, stream=st)
 
     stream = torch.cuda.current_stream()
     for i in range(args.warmup):
         run(i)
     eager_ms = timed(run, args.steps, stream)
+    prepared = [gva.prepare(run, c, stream) for c in range(n_sets)]
+    for i in range(args.warmup):
+        prepared[i % n_sets]()
+    prepared_ms = timed(lambda i: prepared[i % n_sets](), args.steps, stream)
     graphs = []
     for c in range(n_sets):
         g = torch.cuda.CUDAGraph()
@@ -257,8 +253,10 @@ def layer_stack(args, w, inp, d, S, split_rows, fused, dec_b):
     graph_ms = timed(lambda i: graphs[i % n_sets].replay(), args.steps, stream)
     launches = n * ((0 if fused else 1) + 1 + (1 if S > 1 else 0))
     return {"n_layers": n, "launches_per_step": launches, "cache_sets": n_sets,
-            "eager_ms_per_step": round(eager_ms, 5), "graph_ms_per_step": round(graph_ms, 5),
+            "eager_ms_per_step": round(eager_ms, 5), "prepared_ms_per_step": round(prepared_ms, 5),
+            "graph_ms_per_step": round(graph_ms, 5),
             "eager_us_per_layer": round(eager_ms * 1000 / n, 2),
+            "prepared_us_per_layer": round(prepared_ms * 1000 / n, 2),
             "graph_us_per_layer": round(graph_ms * 1000 / n, 2),
             "graph_GBps": round(n * dec_b / (graph_ms * 1e-3) / 1e9, 1)}
 
