@@ -51,7 +51,12 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
   constexpr int DEPTH = 2;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
   __shared__ __attribute__((aligned(16))) float xs_all[Cfg::XS_FLOATS];
-  __shared__ __attribute__((aligned(16))) double freq[DC / 2];
+  // RoPE angles in turns as 32-bit fractions (wrap-around is the reduction
+  // mod one turn): per wave, pair i's angle theta_i (row0 - P) / (2 pi) at
+  // the wave's first tile, and the step from one of its tiles to the next
+  __shared__ uint32_t ang_all[kRopeWaves * (DC / 2)];
+  __shared__ uint32_t ang_step[DC / 2];
+  __shared__ float freq_f[DC / 2];             // theta_i / (2 pi), fp32: offsets within a tile
 
   int b, s, g;
   bool empty_slot;
@@ -135,7 +140,19 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
       dst[0] = __builtin_bit_cast(u32x4, split_hi_lo(we, false));
       dst[1] = __builtin_bit_cast(u32x4, split_hi_lo(wo, false));
     }
-    for (int i = tid; i < DC / 2; i += kRopeThreads) freq[i] = p.freq_rev[i];
+    // angles of each wave's first tile, reduced exactly in fp64, and the
+    // per-tile step (the wave's tiles lie kRopeWaves * kTileRows rows apart)
+    auto turns_u32 = [](double r) {
+      return (uint32_t)(unsigned long long)((r - floor(r)) * 4294967296.0);
+    };
+    for (int i = tid; i < kRopeWaves * (DC / 2); i += kRopeThreads) {
+      const int ww = i / (DC / 2), pi = i % (DC / 2);
+      ang_all[i] = turns_u32(p.freq_rev[pi] * (double)(r0 + kTileRows * ww - P));
+    }
+    for (int i = tid; i < DC / 2; i += kRopeThreads) {
+      ang_step[i] = turns_u32(p.freq_rev[i] * (double)(kTileRows * kRopeWaves));
+      freq_f[i] = (float)p.freq_rev[i];
+    }
   }
   __syncthreads();                              // W and the frequencies are in LDS
 
@@ -170,16 +187,20 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
     float sp[HPG][2];
 #pragma unroll
     for (int hl = 0; hl < HPG; ++hl) sp[hl][0] = sp[hl][1] = 0.f;
-    const double dw = (double)(row0 - P);
     // cos / sin of theta_i (t - P) for this lane's rows and the column
-    // block's pairs: [hf][jj] = cos, sin, cos, sin
+    // block's pairs: [hf][jj] = cos, sin, cos, sin.  The tile's first row
+    // comes from the wave's 32-bit angle (exact to 2^-32 turns), the
+    // lane's row offset within the tile (< 32 rows) is added in fp32.
+    const uint32_t* ang = ang_all + w * (DC / 2);
+    // the wave's tile index: its tiles lie kRopeWaves tiles apart
+    const uint32_t jt = (uint32_t)((row0 - r0) / (kTileRows * kRopeWaves));
     auto trig = [&](int nb, float (&tr)[2][4]) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
-        const double f = freq[8 * nb + 2 * qd + e];
-        const double r = f * dw;
-        const float rb = (float)(r - floor(r));
-        const float ff = (float)f;
+        const int pi = 8 * nb + 2 * qd + e;
+        const uint32_t a = ang[pi] + jt * ang_step[pi];               // mod one turn
+        const float rb = (float)a * 2.3283064365386963e-10f;          // 2^-32
+        const float ff = freq_f[pi];
 #pragma unroll
         for (int hf = 0; hf < 2; ++hf) {
           const float rho = fmaf(ff, (float)(16 * hf + n), rb);
@@ -209,6 +230,23 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
 #pragma unroll
         for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(g[hf][jj], tw[hf][jj], sp[hl][hf]);
     };
+    // (eight heads of 128-wide values leave no registers for the second
+    // set of operands: those steps run in order)
+    constexpr bool PIPE = !(HPG >= 8 && DV >= 128);
+    if constexpr (!PIPE) {
+#pragma unroll
+      for (int it = 0; it < NIT; ++it) {
+        if (it % HPG == 0) trig(it / HPG, tr[0]);
+        load_w(it, wa[0]);
+        gt[0][0] = f32x4{0.f, 0.f, 0.f, 0.f};
+        gt[0][1] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+#pragma unroll
+          for (int hf = 0; hf < 2; ++hf) gt[0][hf] = mfma16(wa[0][c], t.v[hf][c], gt[0][hf]);
+        weight(it, gt[0], tr[0]);
+      }
+    } else {
     load_w(0, wa[0]);
     trig(0, tr[0]);
 #pragma unroll
@@ -227,6 +265,7 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
       __builtin_amdgcn_sched_barrier(0);
     }
     weight(NIT - 1, gt[(NIT - 1) & 1], tr[((NIT - 1) / HPG) & 1]);
+    }
     // sum over the four 16-lane rows, then transpose through LDS: lane
     // (n, qd) takes head col_head's rows 16 hf + 4 qd + jj
 #pragma unroll
