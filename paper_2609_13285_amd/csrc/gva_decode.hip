@@ -1240,32 +1240,33 @@ DecodeFn pick_dv(int dv, int nrc, bool fused, bool paged, bool kr_stream) {
   return nullptr;
 }
 
-template <int DV, int NW>
+template <int DV>
 DecodeFn pick_gqa_hpg(int hpg) {
   switch (hpg) {
-    case 1: return decode_bf16_kernel<1, DV, 0, true, false, false, false, NW>;
-    case 2: return decode_bf16_kernel<2, DV, 0, true, false, false, false, NW>;
-    case 4: return decode_bf16_kernel<4, DV, 0, true, false, false, false, NW>;
-    case 8: return decode_bf16_kernel<8, DV, 0, true, false, false, false, NW>;
+    case 1: return decode_bf16_kernel<1, DV, 0, true, false, false>;
+    case 2: return decode_bf16_kernel<2, DV, 0, true, false, false>;
+    case 4: return decode_bf16_kernel<4, DV, 0, true, false, false>;
+    case 8: return decode_bf16_kernel<8, DV, 0, true, false, false>;
   }
   return nullptr;
 }
 
-// Waves per decode workgroup.  A launch with few workgroups leaves most CUs
-// idle and is bound by each stream's chain of memory round trips, not by
-// HBM: its workgroups take eight waves, so twice as many of each stream's
+// Waves per GVA decode workgroup.  A launch with few workgroups leaves most
+// CUs idle and is bound by each stream's chain of memory round trips, not
+// by HBM: its workgroups take eight waves, so twice as many of each stream's
 // tiles are in flight at once (one such workgroup per CU; sixteen waves
 // would leave 128 registers per wave, too few for the tiles in flight).
+// (The matched-GQA baseline, whose tiles carry a key row beside each value
+// row, measured slower with eight waves at the 350M shape -- 14.5 against
+// 13.2 us -- and keeps four.)
 int decode_waves(long long grid, int n_cu) {
   return 2 * grid <= n_cu ? 8 : kWaves;
 }
 
-DecodeFn pick_gqa_decode(int hpg, int dv, int nw) {
-  switch (dv * 100 + nw) {
-    case 6404: return pick_gqa_hpg<64, 4>(hpg);
-    case 6408: return pick_gqa_hpg<64, 8>(hpg);
-    case 12804: return pick_gqa_hpg<128, 4>(hpg);
-    case 12808: return pick_gqa_hpg<128, 8>(hpg);
+DecodeFn pick_gqa_decode(int hpg, int dv) {
+  switch (dv) {
+    case 64: return pick_gqa_hpg<64>(hpg);
+    case 128: return pick_gqa_hpg<128>(hpg);
   }
   return nullptr;
 }
@@ -1707,8 +1708,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   const int hpg = dims->n_heads / dims->n_groups;
   const long long n_items = decode_grid(dims, num_splits, split_rows);
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;
-  const int nw = decode_waves(n_items, device_cu_count());
-  DecodeFn fn = pick_gqa_decode(hpg, dims->d_v, nw);
+  DecodeFn fn = pick_gqa_decode(hpg, dims->d_v);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
 
   DecodeParams p{};
@@ -1731,7 +1731,7 @@ int gva_gqa_decode_attention(const gva_dims* dims, const void* q, int32_t q_stri
   p.a.split_rows = split_rows;
   const double sc = dims->scale > 0.0 ? dims->scale : 1.0 / sqrt((double)dims->d_v);
   p.a.scale_log2 = (float)(sc * kLog2e);
-  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(64 * nw), 0, static_cast<hipStream_t>(stream), p);
+  hipLaunchKernelGGL(fn, dim3((unsigned)n_items), dim3(kThreads), 0, static_cast<hipStream_t>(stream), p);
   return launch_status();
 }
 
