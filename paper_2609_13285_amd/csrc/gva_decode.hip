@@ -1106,6 +1106,9 @@ __global__ void __launch_bounds__(kThreads) decode_f32_kernel(DecodeParams p) {
 constexpr int kCombineMaxDv = 256;
 constexpr long long kChunkItemsPerCu = 2;         // bounded chunks: chunks per CU
 constexpr long long kMinChunkBytes = 128 << 10;   // bounded chunks: value bytes per chunk
+constexpr long long kMinSplitStream = 192 << 10;  // even splits: a stream's value bytes worth splitting
+constexpr long long kMinSplitBytes = 32 << 10;    // even splits: value bytes per split
+constexpr long long kMaxEvenSplits = 16;
 
 __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   const int lane = threadIdx.x & 63;
@@ -1835,13 +1838,22 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
       return (int)s;
     }
   }
-  // Even splits.  One resident workgroup per CU already streams close to
-  // the HBM ceiling, and every split adds a fixed prologue/merge cost of a
-  // few microseconds, so: enough splits to give each CU one workgroup, but
-  // no split shorter than ~1 MB of value rows.
-  long long s = (n_cu + streams - 1) / streams;
-  const long long max_by_bytes = ((long long)max_len * row_bytes + (1 << 20) - 1) >> 20;
-  if (s > max_by_bytes) s = max_by_bytes;
+  // Even splits.  A workgroup streams its rows at the pace of its own chain
+  // of memory round trips, so a launch of fewer workgroups than CUs is
+  // bound by that chain, not by HBM; splitting the streams over more CUs
+  // shortens it, but adds the combine launch and a prologue per split
+  // (~3.5 us).  So: one split while a stream holds less than
+  // kMinSplitStream bytes of value rows; else enough splits to give each
+  // CU one workgroup (one resident workgroup per CU already streams close
+  // to the HBM ceiling), none shorter than kMinSplitBytes, at most
+  // kMaxEvenSplits (more partials cost the combine more than they save).
+  long long s = 1;
+  const long long stream_bytes = (long long)max_len * row_bytes;
+  if (stream_bytes >= kMinSplitStream) {
+    s = (n_cu + streams - 1) / streams;
+    if (s > stream_bytes / kMinSplitBytes) s = stream_bytes / kMinSplitBytes;
+    if (s > kMaxEvenSplits) s = kMaxEvenSplits;
+  }
   // Lengths spread widely (mean below half the longest): the longest
   // sequences set the tail, so cut them finer.
   if (spread) s *= 2;

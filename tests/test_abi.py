@@ -149,6 +149,16 @@ def test_pick_splits_is_host_only_and_bounded():
     assert spread == 2 * even                                   # widely spread lengths
     for S in (even, spread):
         assert 1 <= S <= gva.GVA_MAX_SPLITS
+    # fewer streams than CUs: split once a stream holds 192 KiB of value
+    # rows, then one workgroup per CU, no split under 32 KiB, at most 16
+    d350 = dims(batch=8, n_heads=16, n_groups=4, t_max=8192, d_v=64, d_c=64)
+    assert gva.gva_pick_splits(d350, 2048, 0, 256) == (8, 0)    # 256 KiB streams: 32 x 8 workgroups
+    assert gva.gva_pick_splits(d350, 1024, 0, 256) == (1, 0)    # 128 KiB streams: no split
+    assert gva.gva_pick_splits(d350, 1536, 0, 256) == (6, 0)    # 192 KiB: six splits of 32 KiB
+    d1 = dims(batch=1, n_heads=32, n_groups=8, t_max=8192)
+    assert gva.gva_pick_splits(d1, 8192, 0, 256) == (16, 0)     # 32 would fill the CUs: capped
+    d16 = dims(batch=16, n_heads=32, n_groups=8, t_max=4096)
+    assert gva.gva_pick_splits(d16, 4096, 0, 256) == (2, 0)     # 128 streams: two each
     # fused only while the B * G * S workgroups are all resident (two per CU)
     assert gva.gva_prefer_fused(d, 2, 0, 256) and not gva.gva_prefer_fused(d, 3, 0, 256)
     assert gva.gva_prefer_fused(d3, 16, 0, 256) and not gva.gva_prefer_fused(d3, 17, 0, 256)
