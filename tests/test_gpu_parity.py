@@ -403,6 +403,43 @@ def test_decode_step_matches_the_separate_calls(case, append):
     _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"step {w.name} S{S}")
 
 
+# Shapes on both sides of the split planner's thresholds for uniform
+# lengths: (B, H, G, d_v = d_c, T) and the plan it must pick there.
+PLANNER_CASES = [
+    ((8, 16, 4, 64, 1024), 1),       # 128 KiB of value rows per stream: no split
+    ((8, 16, 4, 64, 1536), 6),       # 192 KiB: six splits of 32 KiB
+    ((1, 32, 8, 128, 8192), 16),     # eight streams: 32 would fill the CUs, capped at 16
+    ((16, 32, 8, 128, 4096), 2),     # 128 streams: two splits each
+]
+
+
+@pytest.mark.parametrize("shape,S_expected", PLANNER_CASES)
+def test_planner_choice_step_matches_oracle(shape, S_expected):
+    # the plan gva_pick_splits makes for the shape, run as one
+    # gva_decode_step with the current token's rows, against the oracle's
+    # append + decode of every sequence
+    B, H, G, D, T = shape
+    w = gva_inputs.Workload("planner", B, T, H, G, D, D, 16, dtype="bf16")
+    inp = gva_inputs.make_inputs(w, 61)
+    d = dims_of(w)
+    S, rows = gva.plan_for(d, inp["lens"], n_cu=256)
+    assert (S, rows) == (S_expected, 0)
+    dev = upload(inp)
+    ws = gva.workspace_for(d, S, rows)
+    o = torch.full((B, H, D), float("nan"), device="cuda")
+    lse = torch.full((B, H), float("nan"), device="cuda")
+    note(f"planner {shape}: step S={S}")
+    gva.gva_decode_step(d, dev["q"], dev["m"], dev["v"], dev["kr"], dev["lens"], S, o, lse, workspace=ws,
+                        split_rows=rows, v_new=dev["v_new"], kr_new=dev["kr_new"])
+    torch.cuda.synchronize()
+    v_ref, k_ref = inp["v"].clone(), inp["kr"].clone()
+    L = inp["lens"].clamp(0, T)
+    oracle.append(v_ref, k_ref, inp["v_new"], inp["kr_new"], torch.arange(B, dtype=torch.int32),
+                  (L - 1).to(torch.int32), w.rope_base)
+    o_ref, lse_ref = oracle.decode(inp["q"], inp["m"], v_ref, k_ref, inp["lens"], rope_base=w.rope_base)
+    _check(w, o.cpu(), lse.cpu(), o_ref, lse_ref, f"planner {shape} S{S}")
+
+
 # ----------------------------------------------- full-size workloads
 def full_size_picks(lens: torch.Tensor, n_spread: int = 12):
     """The sequences a full-size test checks against the oracle: every one of
