@@ -1216,21 +1216,19 @@ using DecodeFn = void (*)(DecodeParams);
 
 template <int HPG, int DV, bool FUSED, bool PAGED>
 DecodeFn pick_nrc(int nrc, bool kr_stream) {
-  // the streaming positional-key variant exists for contiguous caches
-  constexpr bool KRS = !PAGED;
   switch (nrc) {
     case 0: return decode_bf16_kernel<HPG, DV, 0, false, FUSED, PAGED>;
-    case 1: return KRS && kr_stream ? decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED, KRS>
-                                    : decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED>;
-    case 2: return KRS && kr_stream ? decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED, KRS>
-                                    : decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED>;
+    case 1: return kr_stream ? decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED, true>
+                             : decode_bf16_kernel<HPG, DV, 1, false, FUSED, PAGED>;
+    case 2: return kr_stream ? decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED, true>
+                             : decode_bf16_kernel<HPG, DV, 2, false, FUSED, PAGED>;
   }
   return nullptr;
 }
 
 template <int HPG, int DV>
 DecodeFn pick_mode(int nrc, bool fused, bool paged, bool kr_stream) {
-  if (paged) return fused ? pick_nrc<HPG, DV, true, true>(nrc, false) : pick_nrc<HPG, DV, false, true>(nrc, false);
+  if (paged) return fused ? pick_nrc<HPG, DV, true, true>(nrc, kr_stream) : pick_nrc<HPG, DV, false, true>(nrc, kr_stream);
   return fused ? pick_nrc<HPG, DV, true, false>(nrc, kr_stream) : pick_nrc<HPG, DV, false, false>(nrc, kr_stream);
 }
 
@@ -1319,7 +1317,8 @@ DecodeFn pick_bf16_decode(int hpg, int dv, int nrc, bool fused, bool paged, bool
 // streams as CUs, every L2 holds many sequences' keys at once and streaming
 // them (non-temporal, like the value tiles) measured faster: B = 32, G = 8
 // on 256 CUs gained 0.7-2.0 us per launch, while four long sequences
-// (32 streams) lost 2.6-3 us.
+// (32 streams) lost 2.6-3 us.  Paged caches the same: 2.1-2.7 us per
+// launch at B = 32, G = 8 with pages of 64 or 256 rows.
 bool decode_kr_stream(const gva_dims* d) {
   return (long long)d->batch * d->n_groups >= device_cu_count();
 }
