@@ -87,7 +87,7 @@ extern "C" {
 typedef enum gva_status {
   GVA_OK = 0,
   GVA_ERR_INVALID_ARG = -1, /* null/misaligned pointer, bad dims or split count */
-  GVA_ERR_UNSUPPORTED = -2, /* valid shape this build has no kernel for */
+  GVA_ERR_UNSUPPORTED = -2, /* valid shape the library has no kernel for */
   GVA_ERR_HIP = -3,         /* the HIP runtime reported an error */
   GVA_ERR_SCRATCH = -4      /* gva_decode_step_static: more than GVA_STATIC_SCRATCH_BYTES needed */
 } gva_status;
