@@ -1854,8 +1854,9 @@ int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, in
     if (s > kMaxEvenSplits) s = kMaxEvenSplits;
   }
   // Lengths spread widely (mean below half the longest): the longest
-  // sequences set the tail, so cut them finer.
-  if (spread) s *= 2;
+  // sequences set the tail, so cut them finer -- where they are split at
+  // all (below kMinSplitStream the combine costs more than a split saves).
+  if (spread && s > 1) s *= 2;
   if (s < 1) s = 1;
   if (s > GVA_MAX_SPLITS) s = GVA_MAX_SPLITS;
   return (int)s;

@@ -159,6 +159,10 @@ def test_pick_splits_is_host_only_and_bounded():
     assert gva.gva_pick_splits(d1, 8192, 0, 256) == (16, 0)     # 32 would fill the CUs: capped
     d16 = dims(batch=16, n_heads=32, n_groups=8, t_max=4096)
     assert gva.gva_pick_splits(d16, 4096, 0, 256) == (2, 0)     # 128 streams: two each
+    # widely spread lengths whose longest stream is below 192 KiB: no split
+    # (bounded chunks or even), as for uniform lengths
+    assert gva.gva_pick_splits(d350, 1024, 8 * 300, 256) == (1, 0)
+    assert gva.gva_pick_splits(d350, 1024, 8 * 300, 256, chunked=False) == (1, 0)
     # fused only while the B * G * S workgroups are all resident (two per CU)
     assert gva.gva_prefer_fused(d, 2, 0, 256) and not gva.gva_prefer_fused(d, 3, 0, 256)
     assert gva.gva_prefer_fused(d3, 16, 0, 256) and not gva.gva_prefer_fused(d3, 17, 0, 256)
