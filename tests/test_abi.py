@@ -163,6 +163,9 @@ def test_pick_splits_is_host_only_and_bounded():
     # (bounded chunks or even), as for uniform lengths
     assert gva.gva_pick_splits(d350, 1024, 8 * 300, 256) == (1, 0)
     assert gva.gva_pick_splits(d350, 1024, 8 * 300, 256, chunked=False) == (1, 0)
+    # few streams (32 on 256 CUs): even splits, one workgroup per CU, also
+    # for spread lengths
+    assert gva.gva_pick_splits(d350, 4096, 8 * 1200, 256) == (8, 0)
     # fused only while the B * G * S workgroups are all resident (two per CU)
     assert gva.gva_prefer_fused(d, 2, 0, 256) and not gva.gva_prefer_fused(d, 3, 0, 256)
     assert gva.gva_prefer_fused(d3, 16, 0, 256) and not gva.gva_prefer_fused(d3, 17, 0, 256)
@@ -189,6 +192,9 @@ def test_pick_splits_bounded_chunks_for_ragged_lengths():
     assert rows - 32 < -(-stream_rows // (2 * 256 - streams))
     # uniform lengths keep even splits
     assert gva.gva_pick_splits(d4, 32768, 64 * 32768, 256)[1] == 0
+    # no chunk shorter than the (H/G) d_c = 1024 map rows its absorption reads
+    S7, rows7 = gva.gva_pick_splits(d4, 8192, 64 * 1400, 256)
+    assert rows7 == 1024 and S7 == 8
     # more streams than half the resident workgroups: chunks sized for about
     # two per CU over the whole batch (the partial chunks can no longer all fit)
     d6 = dims(batch=256, n_heads=16, n_groups=2, t_max=32768)
