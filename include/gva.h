@@ -418,8 +418,11 @@ int gva_decode_step_static(const gva_dims* dims, const void* q, const void* m, v
  * compute units (0 = ask the current device).  Returns num_splits in
  * [1, GVA_MAX_SPLITS]; when split_rows is non-NULL it receives the
  * split_rows to pass with it (0 = even splits; bounded chunks are chosen for
- * widely spread lengths).  With split_rows NULL the plan uses even splits
- * only.  Pure host code; enqueues nothing.
+ * widely spread lengths over more (sequence, group) streams than a quarter
+ * of the compute units).  Even splits: one while the longest stream holds
+ * less than 192 KiB of value rows, else about one workgroup per compute
+ * unit, none under 32 KiB, at most 16.  With split_rows NULL the plan uses
+ * even splits only.  Pure host code; enqueues nothing.
  */
 int gva_pick_splits(const gva_dims* dims, int32_t max_len, int64_t total_len, int32_t n_cu,
                     int32_t* split_rows);
