@@ -399,6 +399,17 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
                          "avg_launch_timing": "launches back to back between two events"}}
 
 
+def prefill_kernel_name(w, N: int) -> str:
+    """The prefill kernel gva_prefill_attention launches for one sequence
+    of N prompt rows at w's head shapes (the library's rule, for the label):
+    columns per wave at d_v = 128 and d_r <= 32 once its workgroups number
+    2 per CU (4 at H/G = 8), else the tile-split kernel."""
+    hpg = w.n_heads // w.n_groups
+    items = w.n_groups * -(-N // (128 // hpg))
+    per_wave = w.d_v == 128 and w.d_r <= 32 and items >= (4 if hpg >= 8 else 2) * gva.device_cu_count()
+    return "prefill_vt_kernel" if per_wave else "prefill_bf16_kernel"
+
+
 def prefill_comparison(args, w, caches, dev, stream):
     """A prompt of T tokens for one sequence at the workload's head shapes
     (its rows are the first sequence's cached rows): absorption + causal
@@ -451,7 +462,7 @@ def prefill_comparison(args, w, caches, dev, stream):
             "time_ratio_gva_with_absorb_over_gqa": round((t_att + t_abs) / t_gqa, 4),
             "flop_ratio_gva_over_gqa": round(f_gva / f_gqa, 4),
             "gqa_TFLOPs": round(f_gqa / (t_gqa * 1e-3) / 1e12, 2),
-            "roofline": {"kernel": "prefill_bf16_kernel", "bound": "mfma", "achieved": round(tf, 2),
+            "roofline": {"kernel": prefill_kernel_name(w, N), "bound": "mfma", "achieved": round(tf, 2),
                          "peak": MFMA_BF16_PEAK_TFLOPS, "unit": "TFLOP/s",
                          "frac": round(tf / MFMA_BF16_PEAK_TFLOPS, 4), "traffic": None,
                          "algorithmic_flops_per_launch": f_gva, "avg_launch_ms": round(k_ms, 5),

@@ -496,6 +496,15 @@ inline long long decode_grid(const gva_dims* d, int num_splits, int split_rows) 
   return d->n_groups * (split_rows > 0 ? (slots + 7LL) & ~7LL : slots);
 }
 
+// Compute units of the current device (256 if the runtime cannot say).
+inline int device_cu_count() {
+  int dev = 0, cu = 0;
+  if (hipGetDevice(&dev) == hipSuccess &&
+      hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cu > 0)
+    return cu;
+  return 256;
+}
+
 inline int launch_status() {
   const hipError_t e = hipGetLastError();
   return e == hipSuccess ? GVA_OK : GVA_ERR_HIP;

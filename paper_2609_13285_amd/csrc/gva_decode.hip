@@ -1203,15 +1203,6 @@ __global__ void __launch_bounds__(kThreads) combine_kernel(CombineParams p) {
   if (p.lse != nullptr && lane == 0) p.lse[row] = mx == -INFINITY ? -INFINITY : mx + logf(z);
 }
 
-// Compute units of the current device (256 if the runtime cannot say).
-int device_cu_count() {
-  int dev = 0, cu = 0;
-  if (hipGetDevice(&dev) == hipSuccess &&
-      hipDeviceGetAttribute(&cu, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess && cu > 0)
-    return cu;
-  return 256;
-}
-
 using DecodeFn = void (*)(DecodeParams);
 
 template <int HPG, int DV, bool FUSED, bool PAGED>

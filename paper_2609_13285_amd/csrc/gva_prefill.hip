@@ -394,6 +394,295 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
   }
 }
 
+// ----------------------------------------------- prefill, columns per wave
+// The same causal prefill with the work divided the other way: each of the
+// four waves owns CW (position, head) columns of its own and walks every
+// key tile of the workgroup's range, so the waves hold disjoint softmax
+// states and write their own outputs (no merge).  All four waves work on
+// one key tile at a time and share its V^T: wave w transposes NB / 4 of
+// the tile's 16-wide value blocks (identity products, fp16) into LDS, and
+// after one barrier every wave reads all NB blocks for its P.V.  Per tile a
+// wave then issues a quarter of the identity products (2 NB / 4 instead of
+// 2 NB) and converts a quarter of the blocks to fp16; the V tile itself is
+// read by all four waves from the cache hierarchy (the same rows at the
+// same time).
+__host__ __device__ constexpr int prefill_vt_cols(int dv) { return dv >= 128 ? 32 : 64; }
+
+template <int HPG, int DV, int NRC, bool KPACK>
+__global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p) {
+  static_assert(!KPACK || NRC == 1, "a packed positional chunk is a single chunk");
+  constexpr int CW = prefill_vt_cols(DV), NC = DV / 32, NB = DV / 16, CB = CW / 16;
+  constexpr int WCOLS = kWaves * CW;           // columns per workgroup
+  constexpr int QB = WCOLS / HPG;              // positions per workgroup
+  constexpr int KPW = NB / kWaves;             // V^T blocks each wave transposes
+  static_assert(KPW >= 1 && NB % kWaves == 0, "every wave transposes whole blocks");
+  constexpr int DEPTH = 2;
+  constexpr int NLO = NC + (KPACK ? 0 : NRC);
+  __shared__ bf16x8 lo_lds[kWaves * CB * NLO * 64];   // the low query parts, per wave
+  __shared__ f16x8 vt_lds[2 * NB * 64];               // V^T blocks of a tile, two buffers
+
+  const int nbg = p.B * p.G;
+  const int x = blockIdx.x;
+  const int qb = p.n_qblocks - 1 - x / nbg;    // longest query blocks first
+  const int b = (x % nbg) / p.G, g = (x % nbg) % p.G;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int w = __builtin_amdgcn_readfirstlane(tid >> 6);
+  const int n = lane & 15, qd = lane >> 4;
+  const int h0 = g * HPG;
+  const bf16x8 zero8 = as_bf16x8(u32x4{0u, 0u, 0u, 0u});
+
+  const int L = clamp_len(p.lens, b, p.t_max);
+  const int i_end = min(p.N, (qb + 1) * QB);
+  const int kend = L - p.N + i_end;            // rows the block's last position sees
+  // column CW w + 16 cb + n of this lane: position i = qb QB + col / HPG,
+  // head h0 + col % HPG; pos[cb] = its position, or -1 if it has none
+  int pos[CB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = CW * w + 16 * cb + n;
+    const int i = qb * QB + col / HPG;
+    const int ps = L - p.N + i;
+    pos[cb] = (i < p.N && ps >= 0) ? ps : -1;
+  }
+  const int p_first = L - p.N + qb * QB + (CW * w) / HPG;   // this wave's first position
+
+  // ---- key tiles: rows [0, kend), every wave all of them
+  const int kend16 = kend > 0 ? ((kend + kLayoutRows - 1) / kLayoutRows) * kLayoutRows : 0;
+  const uint16_t* vbase = static_cast<const uint16_t*>(p.v) + ((int64_t)b * p.G + g) * p.t_max * DV;
+  const uint16_t* kbase = static_cast<const uint16_t*>(p.kr) + (int64_t)b * p.t_max * p.d_r;
+  const __amdgpu_buffer_rsrc_t vres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(vbase), (short)0, kend16 * DV * 2, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<uint16_t*>(kbase), (short)0, NRC > 0 ? kend16 * p.d_r * 2 : 0, kBufferWord3);
+  const int kpieces = p.d_r / 8;
+  const int v_lane = qd * 256 + n * 16;
+  int k_lane[NRC > 0 ? NRC : 1];
+#pragma unroll
+  for (int rc = 0; rc < NRC; ++rc) {
+    const int piece = KPACK ? (qd < 2 * kpieces ? qd % kpieces : 0) : min(4 * rc + qd, kpieces - 1);
+    k_lane[rc] = piece * 256 + n * 16;
+  }
+  const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
+  const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
+  using TileT = Tile<DV, NRC, false>;
+  auto load_tile = [&](TileT& t, int row0) {
+    const int lt = row0 / kLayoutRows;
+#pragma unroll
+    for (int hf = 0; hf < 2; ++hf) {
+      const int vsoff = (lt + hf) * v_tile_bytes;
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, 0));
+#pragma unroll
+      for (int rc = 0; rc < NRC; ++rc)
+        t.k[hf][rc] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kres, k_lane[rc], (lt + hf) * k_tile_bytes, 0));
+    }
+  };
+  TileT buf[DEPTH];
+  load_tile(buf[0], 0);
+  __builtin_amdgcn_sched_barrier(0);
+
+  // ---- this wave's queries as bf16 high + low B operands (zero for columns
+  // with no position); the low parts to this wave's LDS region
+  bf16x8 bq[CB][NC];
+  bf16x8 bk[CB][NRC > 0 ? NRC : 1];
+  bf16x8* my_lo = lo_lds + w * (CB * NLO * 64);
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const int col = CW * w + 16 * cb + n;
+    const int i = min(qb * QB + col / HPG, p.N - 1);
+    const int64_t qrow = ((int64_t)b * p.N + i) * p.H + h0 + col % HPG;
+    const float* qa = p.q_abs + qrow * DV + 8 * qd;
+#pragma unroll
+    for (int c = 0; c < NC; ++c) {
+      const f32x4 u0 = *reinterpret_cast<const f32x4*>(qa + 32 * c);
+      const f32x4 u1 = *reinterpret_cast<const f32x4*>(qa + 32 * c + 4);
+      float xv[8];
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        xv[j] = u0[j] * p.scale_log2;
+        xv[4 + j] = u1[j] * p.scale_log2;
+      }
+      bq[cb][c] = pos[cb] >= 0 ? split_hi_lo(xv, false) : zero8;
+      my_lo[(cb * NLO + c) * 64 + lane] = pos[cb] >= 0 ? split_hi_lo(xv, true) : zero8;
+    }
+#pragma unroll
+    for (int rc = 0; rc < NRC; ++rc) {
+      const bool hi_slot = KPACK ? qd < kpieces : 32 * rc + 8 * qd < p.d_r;
+      const bool lo_slot = KPACK && qd >= kpieces && qd < 2 * kpieces;
+      const int j0 = KPACK ? 8 * (lo_slot ? qd - kpieces : qd) : 32 * rc + 8 * qd;
+      float xv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+      if (hi_slot || lo_slot) {
+        const float* qr = p.q_rot + qrow * p.d_r + j0;
+        const f32x4 u0 = *reinterpret_cast<const f32x4*>(qr);
+        const f32x4 u1 = *reinterpret_cast<const f32x4*>(qr + 4);
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          xv[j] = u0[j] * p.scale_log2;
+          xv[4 + j] = u1[j] * p.scale_log2;
+        }
+      }
+      bk[cb][rc] = (pos[cb] >= 0 && (hi_slot || lo_slot)) ? split_hi_lo(xv, lo_slot) : zero8;
+      if constexpr (!KPACK)
+        my_lo[(cb * NLO + NC + rc) * 64 + lane] = (pos[cb] >= 0 && hi_slot) ? split_hi_lo(xv, true) : zero8;
+    }
+  }
+
+  bf16x8 esel[2];
+#pragma unroll
+  for (int half = 0; half < 2; ++half) {
+    u32x4 u = {0u, 0u, 0u, 0u};
+#pragma unroll
+    for (int j = 0; j < 8; ++j)
+      if (8 * qd + j == n + 16 * half) u[j >> 1] |= 0x3F80u << (16 * (j & 1));
+    esel[half] = as_bf16x8(u);
+  }
+
+  float m_run[CB], l_run[CB];
+  f32x4 acc[CB][NB];
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    m_run[cb] = -INFINITY;
+    l_run[cb] = 0.f;
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib) acc[cb][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
+  }
+
+  auto compute_tile = [&](TileT& t, int row0, int vbuf) {
+    if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        const bool dead = row0 + 16 * hf + n >= kend;
+#pragma unroll
+        for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
+      }
+    }
+    // this wave's share of the tile's V^T, into LDS first: the other waves
+    // read it after the barrier below
+    f16x8* vt = vt_lds + vbuf * (NB * 64);
+#pragma unroll
+    for (int kk = 0; kk < KPW; ++kk) {
+      const int k = w * KPW + kk;              // 16-wide value block k: chunk k / 2, half k % 2
+      const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+      f32x4 t0 = z, t1 = z;
+      const bf16x8 e = (k & 1) ? esel[1] : esel[0];
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+        if (c == (k >> 1)) {
+          t0 = mfma16(t.v[0][c], e, z);
+          t1 = mfma16(t.v[1][c], e, z);
+        }
+      const float tv[8] = {t0[0], t0[1], t0[2], t0[3], t1[0], t1[1], t1[2], t1[3]};
+      vt[k * 64 + lane] = to_f16x8(tv);       // bf16 values: exact in fp16 at these magnitudes
+    }
+    const bool masked = row0 + kTileRows - 1 > p_first;   // some column may not see every row
+    int lo_off = lane;
+    asm volatile("" : "+v"(lo_off));
+    auto scores = [&](int cb, f32x4 (&sc)[2]) {
+      bf16x8 lo[NLO];
+#pragma unroll
+      for (int c = 0; c < NLO; ++c) lo[c] = my_lo[(cb * NLO + c) * 64 + lo_off];
+#pragma unroll
+      for (int hf = 0; hf < 2; ++hf) {
+        sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+        for (int c = 0; c < NC; ++c) {
+          sc[hf] = mfma16(t.v[hf][c], bq[cb][c], sc[hf]);
+          sc[hf] = mfma16(t.v[hf][c], lo[c], sc[hf]);
+        }
+#pragma unroll
+        for (int rc = 0; rc < NRC; ++rc) {
+          sc[hf] = mfma16(t.k[hf][rc], bk[cb][rc], sc[hf]);
+          if constexpr (!KPACK) sc[hf] = mfma16(t.k[hf][rc], lo[NC + rc], sc[hf]);
+        }
+      }
+    };
+    auto softmax = [&](int cb, const f32x4 (&sc)[2]) {
+      float xv[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) xv[k] = sc[k >> 2][k & 3];
+      if (masked) {
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) > pos[cb]) xv[k] = -INFINITY;
+      }
+      float mt = xv[0];
+#pragma unroll
+      for (int k = 1; k < 8; ++k) mt = fmaxf(mt, xv[k]);
+      mt = max_over_rows(mt);
+      const float m_new = fmaxf(m_run[cb], mt);
+      if (__ballot(mt > m_run[cb] + kLazyMax) != 0) {
+        const float alpha = m_new > m_run[cb] ? __builtin_amdgcn_exp2f(m_run[cb] - m_new) : 1.f;
+        l_run[cb] *= alpha;
+#pragma unroll
+        for (int ib = 0; ib < NB; ++ib) acc[cb][ib] *= alpha;
+        m_run[cb] = m_new;
+      }
+      const float m_use = m_run[cb] == -INFINITY ? 0.f : m_run[cb];
+      float pr[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        pr[k] = __builtin_amdgcn_exp2f(xv[k] - m_use);
+        l_run[cb] += pr[k];
+      }
+      return to_f16x8(pr);
+    };
+    f16x8 bp[CB];
+    f32x4 sc[2][2];
+    scores(0, sc[0]);
+#pragma unroll
+    for (int cb = 0; cb < CB; ++cb) {
+      if (cb + 1 < CB) scores(cb + 1, sc[(cb + 1) & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+      bp[cb] = softmax(cb, sc[cb & 1]);
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    __syncthreads();                           // every wave's V^T blocks of this tile are in LDS
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const f16x8 av = vt[k * 64 + lane];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp[cb], acc[cb][k]);
+    }
+  };
+
+  // Every wave runs every tile (the barrier inside compute_tile is reached
+  // the same number of times by all four); the tile after the current one
+  // is requested before it is used.
+  // (requests past the block's rows read zeros through the descriptors and
+  // cost no traffic, so they are unconditional and the waits exact)
+  for (int jt = 0; jt < ntiles; jt += DEPTH) {
+#pragma unroll
+    for (int d = 0; d < DEPTH; ++d) {
+      const int j = jt + d;
+      if (j >= ntiles) break;
+      load_tile(buf[(d + 1) % DEPTH], (j + 1) * kTileRows);
+      __builtin_amdgcn_sched_barrier(0);
+      compute_tile(buf[d], j * kTileRows, d);
+    }
+  }
+
+  // ---- this wave's columns: normalise and write
+#pragma unroll
+  for (int cb = 0; cb < CB; ++cb) {
+    const float l = sum_over_rows(l_run[cb]);
+    const int col = CW * w + 16 * cb + n;
+    const int qi = qb * QB + col / HPG;
+    if (qi >= p.N) continue;
+    const bool seen = m_run[cb] != -INFINITY && L - p.N + qi >= 0;
+    const float inv = seen ? 1.f / l : 0.f;
+    const int64_t orow = ((int64_t)b * p.N + qi) * p.H + h0 + col % HPG;
+#pragma unroll
+    for (int ib = 0; ib < NB; ++ib) {
+      f32x4 o = acc[cb][ib] * inv;
+      *reinterpret_cast<f32x4*>(p.o + orow * DV + 16 * ib + 4 * qd) = o;
+    }
+    if (qd == 0) p.lse[orow] = seen ? (m_run[cb] + log2f(l)) * kLn2 : -INFINITY;
+  }
+}
+
 using PrefillFn = void (*)(PrefillParams);
 
 template <int HPG, int DV>
@@ -425,6 +714,36 @@ PrefillFn pick_prefill(int hpg, int dv, int d_r, bool gqa) {
   return nullptr;
 }
 
+template <int HPG, int DV>
+PrefillFn pick_prefill_vt_nrc(int d_r) {
+  if (d_r == 0) return prefill_vt_kernel<HPG, DV, 0, false>;
+  if (d_r <= 16) return prefill_vt_kernel<HPG, DV, 1, true>;
+  if (d_r <= 32) return prefill_vt_kernel<HPG, DV, 1, false>;
+  return nullptr;                              // two positional chunks: the tile-split kernel
+}
+
+PrefillFn pick_prefill_vt(int hpg, int dv, int d_r) {
+  if (dv != 128) return nullptr;               // d_v = 64: the tile-split kernel (measured faster)
+  switch (hpg) {
+    case 1: return pick_prefill_vt_nrc<1, 128>(d_r);
+    case 2: return pick_prefill_vt_nrc<2, 128>(d_r);
+    case 4: return pick_prefill_vt_nrc<4, 128>(d_r);
+    case 8: return pick_prefill_vt_nrc<8, 128>(d_r);
+  }
+  return nullptr;
+}
+
+// The columns-per-wave kernel has a quarter of the workgroups of the
+// tile-split one; it wins once they fill the GPU a few times over: from
+// two per CU (H/G <= 4) or four per CU (H/G = 8), measured on prompts of
+// 1K-16K tokens at d_v = 128.
+bool prefer_prefill_vt(const gva_dims* d, int n_new) {
+  const int hpg = d->n_heads / d->n_groups;
+  const long long qblocks = (n_new + kWaves * prefill_vt_cols(d->d_v) / hpg - 1) / (kWaves * prefill_vt_cols(d->d_v) / hpg);
+  const long long items = (long long)d->batch * d->n_groups * qblocks;
+  return items >= (hpg >= 8 ? 4LL : 2LL) * device_cu_count();
+}
+
 // The launch behind gva_prefill_attention and, with k_gqa given,
 // gva_gqa_prefill_attention.
 int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const float* q_rot,
@@ -446,9 +765,14 @@ int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const 
   if (st != GVA_OK) return st;
   if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
   const int hpg = dims->n_heads / dims->n_groups;
-  PrefillFn fn = pick_prefill(hpg, dims->d_v, d_r, gqa);
+  // columns per wave where it has a kernel (GVA, d_v = 128, d_r <= 32) and
+  // the grid is large enough, else the tile-split kernel (the GQA baseline,
+  // d_v = 64, two positional chunks, short prompts)
+  PrefillFn fn = gqa || !prefer_prefill_vt(dims, n_new) ? nullptr : pick_prefill_vt(hpg, dims->d_v, d_r);
+  const bool per_wave = fn != nullptr;
+  if (!per_wave) fn = pick_prefill(hpg, dims->d_v, d_r, gqa);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const int qb_rows = prefill_cols(dims->d_v, gqa) / hpg;
+  const int qb_rows = (per_wave ? kWaves * prefill_vt_cols(dims->d_v) : prefill_cols(dims->d_v, gqa)) / hpg;
   const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;
   const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;

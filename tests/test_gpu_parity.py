@@ -1208,6 +1208,45 @@ def test_prefill_sharp_scores(qscale):
     _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"prefill sharp scores x{qscale}")
 
 
+# Prompts large enough that the launch takes the columns-per-wave prefill
+# kernel (d_v = 128, d_r <= 32, at least 2 workgroups per CU -- 4 at
+# H/G = 8 -- of 4 x 32 columns): (B, H/G, G, d_r, N, prefix rows of the
+# other sequences, query scale).
+PREFILL_WAVE_CASES = [
+    (4, 4, 4, 16, 1024, 300, 1.0),
+    (4, 8, 2, 16, 2048, 0, 1.0),
+    (4, 1, 8, 0, 2048, 77, 1.0),
+    (4, 2, 4, 32, 2048, 500, 1.0),
+    (4, 4, 4, 16, 1024, 0, 6.0),
+]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("B,hpg,G,dr,N,prefix,qscale", PREFILL_WAVE_CASES)
+def test_prefill_columns_per_wave_matches_oracle(B, hpg, G, dr, N, prefix, qscale):
+    # every row of every prompt against the oracle; the first sequence's
+    # prompt fills its cache from row 0, the others follow a cached prefix,
+    # and rows past every length hold NaN
+    n_cu = gva.device_cu_count()
+    items = B * G * -(-N // (128 // hpg))
+    assert items >= (4 if hpg >= 8 else 2) * n_cu, "the shape must take the columns-per-wave kernel"
+    T = -(-(N + prefix) // 32) * 32              # the tiled layout's capacity granularity
+    w = gva_inputs.Workload("prefill_wave", B, T, hpg * G, G, 128, 128, dr, dtype="bf16")
+    lens = torch.tensor([N] + [N + prefix] * (B - 1), dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 47, lens=lens)
+    for b, L in enumerate(lens.tolist()):
+        inp["v"][b, :, L:] = float("nan")
+        inp["kr"][b, L:] = float("nan")
+    q = (gva_inputs.prefill_queries(w, 47, N).float() * qscale).to(torch.bfloat16)
+    note(f"prefill per wave B={B} hpg={hpg} G={G} dr={dr} N={N}: oracle")
+    o_ref, lse_ref = oracle.prefill(q, inp["m"], inp["v"], inp["kr"], lens, rope_base=w.rope_base)
+    dev = upload({k: inp[k] for k in ("m", "v", "kr", "lens")})
+    note(f"prefill per wave B={B} hpg={hpg} G={G} dr={dr} N={N}: GPU")
+    o, lse = gva.prefill(dims_of(w), q.cuda(), dev["m"], dev["v"], dev["kr"], dev["lens"])
+    torch.cuda.synchronize()
+    _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"prefill per wave hpg{hpg} G{G} dr{dr} N{N} x{qscale}")
+
+
 def test_prefill_after_append_of_the_prompt():
     # Algorithm 1's append for every prompt row (gva_append_kv), then the
     # prefill over the appended caches, against the oracle doing the same
