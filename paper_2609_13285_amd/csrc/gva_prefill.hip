@@ -1,6 +1,7 @@
 // libgva.so -- causal prefill of GVA (Algorithm 1 for every prompt position at
-// once): prefill_bf16_kernel, gva_prefill_attention and the matched-GQA
-// baseline gva_gqa_prefill_attention.
+// once): prefill_bf16_kernel (the waves of a workgroup split its key tiles),
+// prefill_vt_kernel (the waves split its columns and share each tile's V^T),
+// gva_prefill_attention and the matched-GQA baseline gva_gqa_prefill_attention.
 
 #include "gva_common.h"
 
