@@ -407,12 +407,15 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
 // 2 NB) and converts a quarter of the blocks to fp16; the V tile itself is
 // read by all four waves from the cache hierarchy (the same rows at the
 // same time).
-__host__ __device__ constexpr int prefill_vt_cols(int dv) { return dv >= 128 ? 32 : 64; }
+// Columns per wave: 32, or 16 for the matched-GQA baseline, whose separate
+// key tile takes the registers of the second column block.
+__host__ __device__ constexpr int prefill_vt_cols(int dv, bool gqa) { return gqa ? 16 : (dv >= 128 ? 32 : 64); }
 
-template <int HPG, int DV, int NRC, bool KPACK>
+template <int HPG, int DV, int NRC, bool GQA, bool KPACK>
 __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p) {
   static_assert(!KPACK || NRC == 1, "a packed positional chunk is a single chunk");
-  constexpr int CW = prefill_vt_cols(DV), NC = DV / 32, NB = DV / 16, CB = CW / 16;
+  static_assert(!GQA || NRC == 0, "the GQA baseline has no positional term");
+  constexpr int CW = prefill_vt_cols(DV, GQA), NC = DV / 32, NB = DV / 16, CB = CW / 16;
   constexpr int WCOLS = kWaves * CW;           // columns per workgroup
   constexpr int QB = WCOLS / HPG;              // positions per workgroup
   constexpr int KPW = NB / kWaves;             // V^T blocks each wave transposes
@@ -455,6 +458,11 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
       const_cast<uint16_t*>(vbase), (short)0, kend16 * DV * 2, kBufferWord3);
   const __amdgpu_buffer_rsrc_t kres = __builtin_amdgcn_make_buffer_rsrc(
       const_cast<uint16_t*>(kbase), (short)0, NRC > 0 ? kend16 * p.d_r * 2 : 0, kBufferWord3);
+  const __amdgpu_buffer_rsrc_t kcres = __builtin_amdgcn_make_buffer_rsrc(
+      const_cast<void*>(GQA ? static_cast<const void*>(static_cast<const uint16_t*>(p.k_gqa) +
+                                                       ((int64_t)b * p.G + g) * p.t_max * DV)
+                            : static_cast<const void*>(vbase)),
+      (short)0, kend16 * DV * 2, kBufferWord3);
   const int kpieces = p.d_r / 8;
   const int v_lane = qd * 256 + n * 16;
   int k_lane[NRC > 0 ? NRC : 1];
@@ -465,12 +473,17 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
   }
   const int v_tile_bytes = 16 * DV * 2, k_tile_bytes = 16 * p.d_r * 2;
   const int ntiles = kend > 0 ? (kend + kTileRows - 1) / kTileRows : 0;
-  using TileT = Tile<DV, NRC, false>;
+  using TileT = Tile<DV, NRC, GQA>;
   auto load_tile = [&](TileT& t, int row0) {
     const int lt = row0 / kLayoutRows;
 #pragma unroll
     for (int hf = 0; hf < 2; ++hf) {
       const int vsoff = (lt + hf) * v_tile_bytes;
+      if constexpr (GQA) {
+#pragma unroll
+        for (int c = 0; c < NC; ++c)
+          t.kc[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(kcres, v_lane + 1024 * c, vsoff, 0));
+      }
 #pragma unroll
       for (int c = 0; c < NC; ++c)
         t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, vsoff, 0));
@@ -556,6 +569,10 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
         const bool dead = row0 + 16 * hf + n >= kend;
 #pragma unroll
         for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
+        if constexpr (GQA) {
+#pragma unroll
+          for (int c = 0; c < NC; ++c) t.kc[hf][c] = dead ? zero8 : t.kc[hf][c];
+        }
 #pragma unroll
         for (int rc = 0; rc < NRC; ++rc) t.k[hf][rc] = dead ? zero8 : t.k[hf][rc];
       }
@@ -590,8 +607,8 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
         sc[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
         for (int c = 0; c < NC; ++c) {
-          sc[hf] = mfma16(t.v[hf][c], bq[cb][c], sc[hf]);
-          sc[hf] = mfma16(t.v[hf][c], lo[c], sc[hf]);
+          sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], bq[cb][c], sc[hf]);
+          sc[hf] = mfma16(GQA ? t.kc[hf][c] : t.v[hf][c], lo[c], sc[hf]);
         }
 #pragma unroll
         for (int rc = 0; rc < NRC; ++rc) {
@@ -717,19 +734,19 @@ PrefillFn pick_prefill(int hpg, int dv, int d_r, bool gqa) {
 
 template <int HPG, int DV>
 PrefillFn pick_prefill_vt_nrc(int d_r) {
-  if (d_r == 0) return prefill_vt_kernel<HPG, DV, 0, false>;
-  if (d_r <= 16) return prefill_vt_kernel<HPG, DV, 1, true>;
-  if (d_r <= 32) return prefill_vt_kernel<HPG, DV, 1, false>;
+  if (d_r == 0) return prefill_vt_kernel<HPG, DV, 0, false, false>;
+  if (d_r <= 16) return prefill_vt_kernel<HPG, DV, 1, false, true>;
+  if (d_r <= 32) return prefill_vt_kernel<HPG, DV, 1, false, false>;
   return nullptr;                              // two positional chunks: the tile-split kernel
 }
 
-PrefillFn pick_prefill_vt(int hpg, int dv, int d_r) {
+PrefillFn pick_prefill_vt(int hpg, int dv, int d_r, bool gqa) {
   if (dv != 128) return nullptr;               // d_v = 64: the tile-split kernel (measured faster)
   switch (hpg) {
-    case 1: return pick_prefill_vt_nrc<1, 128>(d_r);
-    case 2: return pick_prefill_vt_nrc<2, 128>(d_r);
-    case 4: return pick_prefill_vt_nrc<4, 128>(d_r);
-    case 8: return pick_prefill_vt_nrc<8, 128>(d_r);
+    case 1: return gqa ? prefill_vt_kernel<1, 128, 0, true, false> : pick_prefill_vt_nrc<1, 128>(d_r);
+    case 2: return gqa ? prefill_vt_kernel<2, 128, 0, true, false> : pick_prefill_vt_nrc<2, 128>(d_r);
+    case 4: return gqa ? prefill_vt_kernel<4, 128, 0, true, false> : pick_prefill_vt_nrc<4, 128>(d_r);
+    case 8: return gqa ? prefill_vt_kernel<8, 128, 0, true, false> : pick_prefill_vt_nrc<8, 128>(d_r);
   }
   return nullptr;
 }
@@ -738,9 +755,11 @@ PrefillFn pick_prefill_vt(int hpg, int dv, int d_r) {
 // tile-split one; it wins once they fill the GPU a few times over: from
 // two per CU (H/G <= 4) or four per CU (H/G = 8), measured on prompts of
 // 1K-16K tokens at d_v = 128.
-bool prefer_prefill_vt(const gva_dims* d, int n_new) {
+bool prefer_prefill_vt(const gva_dims* d, int n_new, bool gqa) {
   const int hpg = d->n_heads / d->n_groups;
-  const long long qblocks = (n_new + kWaves * prefill_vt_cols(d->d_v) / hpg - 1) / (kWaves * prefill_vt_cols(d->d_v) / hpg);
+  const int qb = kWaves * prefill_vt_cols(d->d_v, gqa) / hpg;   // positions per workgroup
+  if (qb < 1) return false;
+  const long long qblocks = (n_new + qb - 1) / qb;
   const long long items = (long long)d->batch * d->n_groups * qblocks;
   return items >= (hpg >= 8 ? 4LL : 2LL) * device_cu_count();
 }
@@ -766,14 +785,14 @@ int prefill_impl(const gva_dims* dims, int32_t n_new, const float* q_abs, const 
   if (st != GVA_OK) return st;
   if (d_r % 8 != 0 || d_r > 64) return GVA_ERR_UNSUPPORTED;
   const int hpg = dims->n_heads / dims->n_groups;
-  // columns per wave where it has a kernel (GVA, d_v = 128, d_r <= 32) and
-  // the grid is large enough, else the tile-split kernel (the GQA baseline,
-  // d_v = 64, two positional chunks, short prompts)
-  PrefillFn fn = gqa || !prefer_prefill_vt(dims, n_new) ? nullptr : pick_prefill_vt(hpg, dims->d_v, d_r);
+  // columns per wave where it has a kernel (d_v = 128; GVA with d_r <= 32,
+  // or the GQA baseline) and the grid is large enough, else the tile-split
+  // kernel (d_v = 64, two positional chunks, short prompts)
+  PrefillFn fn = prefer_prefill_vt(dims, n_new, gqa) ? pick_prefill_vt(hpg, dims->d_v, d_r, gqa) : nullptr;
   const bool per_wave = fn != nullptr;
   if (!per_wave) fn = pick_prefill(hpg, dims->d_v, d_r, gqa);
   if (fn == nullptr) return GVA_ERR_UNSUPPORTED;
-  const int qb_rows = (per_wave ? kWaves * prefill_vt_cols(dims->d_v) : prefill_cols(dims->d_v, gqa)) / hpg;
+  const int qb_rows = (per_wave ? kWaves * prefill_vt_cols(dims->d_v, gqa) : prefill_cols(dims->d_v, gqa)) / hpg;
   const long long n_qblocks = (n_new + qb_rows - 1) / qb_rows;
   const long long n_items = (long long)dims->batch * dims->n_groups * n_qblocks;
   if (n_items > 0x7FFFFFFFLL) return GVA_ERR_UNSUPPORTED;

@@ -1247,6 +1247,48 @@ def test_prefill_columns_per_wave_matches_oracle(B, hpg, G, dr, N, prefix, qscal
     _prefill_check(o.cpu(), lse.cpu(), o_ref, lse_ref, f"prefill per wave hpg{hpg} G{G} dr{dr} N{N} x{qscale}")
 
 
+# The matched-GQA prefill at sizes that take its columns-per-wave kernel
+# (16 columns per wave): (B, H/G, G, N, prefix rows of the other sequences).
+GQA_PREFILL_WAVE_CASES = [
+    (4, 4, 4, 512, 100),
+    (4, 8, 2, 1024, 0),
+    (4, 1, 8, 1024, 50),
+]
+
+
+@pytest.mark.slow
+@pytest.mark.parametrize("B,hpg,G,N,prefix", GQA_PREFILL_WAVE_CASES)
+def test_gqa_prefill_columns_per_wave_matches_oracle(B, hpg, G, N, prefix):
+    # sampled prompt rows (every seventh and the last) as GQA decode steps of
+    # the oracle over the rows each sees
+    n_cu = gva.device_cu_count()
+    items = B * G * -(-N // (64 // hpg))
+    assert items >= (4 if hpg >= 8 else 2) * n_cu, "the shape must take the columns-per-wave kernel"
+    T = -(-(N + prefix) // 32) * 32
+    w = gva_inputs.Workload("gqa_prefill_wave", B, T, G * hpg, G, 128, 128, 0, dtype="bf16", gqa=True)
+    lens = torch.tensor([N] + [N + prefix] * (B - 1), dtype=torch.int32)
+    inp = gva_inputs.make_inputs(w, 53, lens=lens)
+    q = gva_inputs.prefill_queries(w, 53, N, gqa=True)
+    dev = upload({k: inp[k] for k in ("v", "k_gqa", "lens")})
+    d = dims_of(w)
+    o = torch.empty(B, N, w.n_heads, 128, dtype=torch.float32, device="cuda")
+    lse = torch.empty(B, N, w.n_heads, dtype=torch.float32, device="cuda")
+    note(f"gqa prefill per wave B={B} hpg={hpg} G={G} N={N}")
+    gva.gva_gqa_prefill_attention(d, N, q.cuda(), dev["k_gqa"], dev["v"], dev["lens"], o, lse)
+    torch.cuda.synchronize()
+    o, lse = o.cpu(), lse.cpu()
+    rows = sorted(set(range(0, N, 7)) | {N - 1})
+    o_ref = torch.zeros(B, len(rows), w.n_heads, 128, dtype=torch.float64)
+    lse_ref = torch.full((B, len(rows), w.n_heads), float("-inf"), dtype=torch.float64)
+    for r, i in enumerate(rows):
+        p = lens - N + i
+        oi, li = oracle.gqa_decode(q[:, i].contiguous(), inp["k_gqa"], inp["v"], (p + 1).clamp(min=0), d_k=128)
+        o_ref[:, r] = oi
+        lse_ref[:, r] = li
+    idx = torch.tensor(rows)
+    _prefill_check(o[:, idx], lse[:, idx], o_ref, lse_ref, f"gqa prefill per wave hpg{hpg} G{G} N{N}")
+
+
 def test_prefill_after_append_of_the_prompt():
     # Algorithm 1's append for every prompt row (gva_append_kv), then the
     # prefill over the appended caches, against the oracle doing the same
