@@ -422,6 +422,12 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
   static_assert(KPW >= 1 && NB % kWaves == 0, "every wave transposes whole blocks");
   constexpr int DEPTH = 2;
   constexpr int NLO = NC + (KPACK ? 0 : NRC);
+  // P.V one tile behind the scores (below), except in the matched-GQA
+  // baseline, which ran slower so; kAhead column blocks' scores are issued
+  // before that P.V: one where a separate positional chunk and its low parts
+  // already hold the registers (all of them would spill), else all
+  constexpr bool kPipe = !GQA;
+  constexpr int kAhead = (NRC > 0 && !KPACK) ? 1 : CB;
   __shared__ bf16x8 lo_lds[kWaves * CB * NLO * 64];   // the low query parts, per wave
   __shared__ f16x8 vt_lds[2 * NB * 64];               // V^T blocks of a tile, two buffers
 
@@ -562,7 +568,8 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
     for (int ib = 0; ib < NB; ++ib) acc[cb][ib] = f32x4{0.f, 0.f, 0.f, 0.f};
   }
 
-  auto compute_tile = [&](TileT& t, int row0, int vbuf) {
+  f16x8 bp_prev[CB];                           // the previous tile's weights (pipelined P.V)
+  auto compute_tile = [&](TileT& t, int row0, int vbuf, bool has_prev) {
     if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
@@ -647,22 +654,52 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
       }
       return to_f16x8(pr);
     };
-    f16x8 bp[CB];
-    f32x4 sc[2][2];
-    scores(0, sc[0]);
+    if constexpr (kPipe) {
+      // P.V of the previous tile (its V^T in the other buffer, complete since
+      // the previous barrier) is issued with this tile's softmax, so the
+      // matrix cores run it while the vector units work; it comes first in
+      // program order, before any rescale of the accumulators
+      f32x4 sc[CB][2];
 #pragma unroll
-    for (int cb = 0; cb < CB; ++cb) {
-      if (cb + 1 < CB) scores(cb + 1, sc[(cb + 1) & 1]);
+      for (int cb = 0; cb < kAhead; ++cb) scores(cb, sc[cb]);
       __builtin_amdgcn_sched_barrier(0);
-      bp[cb] = softmax(cb, sc[cb & 1]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    __syncthreads();                           // every wave's V^T blocks of this tile are in LDS
+      if (has_prev) {
+        const f16x8* vtp = vt_lds + (vbuf ^ 1) * (NB * 64);
 #pragma unroll
-    for (int k = 0; k < NB; ++k) {
-      const f16x8 av = vt[k * 64 + lane];
+        for (int k = 0; k < NB; ++k) {
+          const f16x8 av = vtp[k * 64 + lane];
 #pragma unroll
-      for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp[cb], acc[cb][k]);
+          for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp_prev[cb], acc[cb][k]);
+        }
+      }
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        if (cb >= kAhead) {
+          __builtin_amdgcn_sched_barrier(0);
+          scores(cb, sc[cb]);
+          __builtin_amdgcn_sched_barrier(0);
+        }
+        bp_prev[cb] = softmax(cb, sc[cb]);
+      }
+      __syncthreads();                         // every wave's V^T blocks of this tile are in LDS
+    } else {
+      f16x8 bp[CB];
+      f32x4 sc[2][2];
+      scores(0, sc[0]);
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) {
+        if (cb + 1 < CB) scores(cb + 1, sc[(cb + 1) & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+        bp[cb] = softmax(cb, sc[cb & 1]);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      __syncthreads();                         // every wave's V^T blocks of this tile are in LDS
+#pragma unroll
+      for (int k = 0; k < NB; ++k) {
+        const f16x8 av = vt[k * 64 + lane];
+#pragma unroll
+        for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp[cb], acc[cb][k]);
+      }
     }
   };
 
@@ -678,7 +715,16 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
       if (j >= ntiles) break;
       load_tile(buf[(d + 1) % DEPTH], (j + 1) * kTileRows);
       __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], j * kTileRows, d);
+      compute_tile(buf[d], j * kTileRows, d, j > 0);
+    }
+  }
+  if (kPipe && ntiles > 0) {                   // P.V of the last tile
+    const f16x8* vtl = vt_lds + ((ntiles - 1) & 1) * (NB * 64);
+#pragma unroll
+    for (int k = 0; k < NB; ++k) {
+      const f16x8 av = vtl[k * 64 + lane];
+#pragma unroll
+      for (int cb = 0; cb < CB; ++cb) acc[cb][k] = mfma16(av, bp_prev[cb], acc[cb][k]);
     }
   }
 
