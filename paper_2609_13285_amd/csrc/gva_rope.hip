@@ -34,13 +34,23 @@ struct RopeDecodeParams {
 
 template <int HPG, int DV, int DC>
 struct RopeCfg {
+  // 16-row blocks in a wave's tile: four (64 rows, so every W piece read
+  // from LDS feeds four products; the LDS reads of W bound the kernel at
+  // two), or two where eight 128-wide heads leave no registers for them
+  static constexpr int HF = (HPG >= 8 && DV >= 128) ? 2 : 4;
+  static constexpr int TR = 16 * HF;                       // rows per wave tile
+  // tiles in flight per wave: the next one is requested while this one is
+  // computed, or, where a second 64-row tile does not fit the registers
+  // (128-wide values, or eight heads), each half of it once the P.V has
+  // read the same half of this one
+  static constexpr int DEPTH = (HF == 4 && (DV >= 128 || HPG * DV >= 512)) ? 1 : 2;
   static constexpr int NC = DV / 32;                       // K-chunks per V row
   static constexpr int NB = DV / 16;                       // 16-wide i-blocks of the output
   static constexpr int NBC = DC / 16;                      // 16-wide column blocks of W
   static constexpr int W_FLOATS = HPG * NC * NBC * 64 * 4; // W in 16-byte pieces
   static constexpr int RED_FLOATS = kRopeWaves * HPG * (DV + 2);
   static constexpr int LDS_FLOATS = W_FLOATS > RED_FLOATS ? W_FLOATS : RED_FLOATS;
-  static constexpr int XS_FLOATS = kRopeWaves * HPG * kTileRows;   // score transpose
+  static constexpr int XS_FLOATS = kRopeWaves * HPG * TR;          // score transpose
 };
 
 template <int HPG, int DV, int DC>
@@ -48,7 +58,7 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
   const DecodeArgs a = p.a;
   using Cfg = RopeCfg<HPG, DV, DC>;
   constexpr int NC = Cfg::NC, NB = Cfg::NB, NBC = Cfg::NBC;
-  constexpr int DEPTH = 2;
+  constexpr int HF = Cfg::HF, TR = Cfg::TR, RH = HF / 2, DEPTH = Cfg::DEPTH;
   __shared__ __attribute__((aligned(16))) float lds[Cfg::LDS_FLOATS];
   __shared__ __attribute__((aligned(16))) float xs_all[Cfg::XS_FLOATS];
   // RoPE angles in turns as 32-bit fractions (wrap-around is the reduction
@@ -88,24 +98,27 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
       const_cast<uint16_t*>(vbase), (short)0, r1c * DV * 2, kBufferWord3);
   const int v_lane = qd * 256 + n * 16;
   const int v_tile_bytes = 16 * DV * 2;
-  const int ntiles = (r1 - r0 + kTileRows - 1) / kTileRows;
+  const int ntiles = (r1 - r0 + TR - 1) / TR;
   const int my_tiles = ntiles > w ? (ntiles - w + kRopeWaves - 1) / kRopeWaves : 0;
-  auto tile_row = [&](int j) { return r0 + (w + kRopeWaves * j) * kTileRows; };
-  struct VTile { bf16x8 v[2][NC]; };
-  auto load_tile = [&](VTile& t, int row0) {
+  auto tile_row = [&](int j) { return r0 + (w + kRopeWaves * j) * TR; };
+  struct VTile { bf16x8 v[HF][NC]; };
+  // the 16-row blocks [hf0, hf1) of the tile at row0
+  auto load_blocks = [&](VTile& t, int row0, int hf0, int hf1) {
     const int lt = row0 / kLayoutRows;
 #pragma unroll
-    for (int hf = 0; hf < 2; ++hf)
+    for (int hf = hf0; hf < hf1; ++hf)
 #pragma unroll
       for (int c = 0; c < NC; ++c)
         t.v[hf][c] = as_bf16x8(__builtin_amdgcn_raw_buffer_load_b128(vres, v_lane + 1024 * c, (lt + hf) * v_tile_bytes, kAuxNT));
   };
   VTile buf[DEPTH];
+  if constexpr (DEPTH == 1) {
+    load_blocks(buf[0], tile_row(0), 0, HF);
+  } else {
 #pragma unroll
-  for (int d = 0; d < DEPTH - 1; ++d) {
-    load_tile(buf[d], tile_row(d));
-    __builtin_amdgcn_sched_barrier(0);
+    for (int d = 0; d < DEPTH - 1; ++d) load_blocks(buf[d], tile_row(d), 0, HF);
   }
+  __builtin_amdgcn_sched_barrier(0);
 
   // ---- W_h for the group's heads, in LDS as 16-byte pieces:
   // piece ((hl * NC + kc) * NBC + nb) * 64 + (16 qd + n) holds
@@ -141,16 +154,16 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
       dst[1] = __builtin_bit_cast(u32x4, split_hi_lo(wo, false));
     }
     // angles of each wave's first tile, reduced exactly in fp64, and the
-    // per-tile step (the wave's tiles lie kRopeWaves * kTileRows rows apart)
+    // per-tile step (the wave's tiles lie kRopeWaves * TR rows apart)
     auto turns_u32 = [](double r) {
       return (uint32_t)(unsigned long long)((r - floor(r)) * 4294967296.0);
     };
     for (int i = tid; i < kRopeWaves * (DC / 2); i += kRopeThreads) {
       const int ww = i / (DC / 2), pi = i % (DC / 2);
-      ang_all[i] = turns_u32(p.freq_rev[pi] * (double)(r0 + kTileRows * ww - P));
+      ang_all[i] = turns_u32(p.freq_rev[pi] * (double)(r0 + TR * ww - P));
     }
     for (int i = tid; i < DC / 2; i += kRopeThreads) {
-      ang_step[i] = turns_u32(p.freq_rev[i] * (double)(kTileRows * kRopeWaves));
+      ang_step[i] = turns_u32(p.freq_rev[i] * (double)(TR * kRopeWaves));
       freq_f[i] = (float)p.freq_rev[i];
     }
   }
@@ -166,17 +179,19 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
     esel[half] = as_bf16x8(u);
   }
   const u32x4* wl = reinterpret_cast<const u32x4*>(lds);
-  float* xs = xs_all + w * HPG * kTileRows;      // this wave's score transpose: [HPG][32 rows]
+  float* xs = xs_all + w * HPG * TR;             // this wave's score transpose: [HPG][TR rows]
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x4 acc[NB];
 #pragma unroll
   for (int ib = 0; ib < NB; ++ib) acc[ib] = f32x4{0.f, 0.f, 0.f, 0.f};
 
-  auto compute_tile = [&](VTile& t, int row0, int row_end) {
-    if (row0 + kTileRows > row_end) {
+  // next_row: with one tile in flight, the tile whose blocks are requested
+  // as soon as the P.V has read this tile's (the registers are reused)
+  auto compute_tile = [&](VTile& t, int row0, int row_end, int next_row) {
+    if (row0 + TR > row_end) {
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) {
+      for (int hf = 0; hf < HF; ++hf) {
         const bool dead = row0 + 16 * hf + n >= row_end;
 #pragma unroll
         for (int c = 0; c < NC; ++c) t.v[hf][c] = dead ? zero8 : t.v[hf][c];
@@ -184,28 +199,31 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
     }
     // lane (n, qd): rows row0 + 16 hf + n, columns 16 nb + 4 qd + jj, i.e.
     // pairs i0 = 8 nb + 2 qd (jj = 0, 1) and i0 + 1 (jj = 2, 3)
-    float sp[HPG][2];
+    float sp[HPG][HF];
 #pragma unroll
-    for (int hl = 0; hl < HPG; ++hl) sp[hl][0] = sp[hl][1] = 0.f;
+    for (int hl = 0; hl < HPG; ++hl)
+#pragma unroll
+      for (int hf = 0; hf < HF; ++hf) sp[hl][hf] = 0.f;
     // cos / sin of theta_i (t - P) for this lane's rows and the column
     // block's pairs: [hf][jj] = cos, sin, cos, sin.  The tile's first row
     // comes from the wave's 32-bit angle (exact to 2^-32 turns), the
-    // lane's row offset within the tile (< 32 rows) is added in fp32.
+    // lane's row offset within the tile (< TR rows) is added in fp32.
     const uint32_t* ang = ang_all + w * (DC / 2);
     // the wave's tile index: its tiles lie kRopeWaves tiles apart
-    const uint32_t jt = (uint32_t)((row0 - r0) / (kTileRows * kRopeWaves));
-    auto trig = [&](int nb, float (&tr)[2][4]) {
+    const uint32_t jt = (uint32_t)((row0 - r0) / (TR * kRopeWaves));
+    auto trig = [&](int nb, float (&tr)[HF][4]) {
 #pragma unroll
       for (int e = 0; e < 2; ++e) {
         const int pi = 8 * nb + 2 * qd + e;
         const uint32_t a = ang[pi] + jt * ang_step[pi];               // mod one turn
         const float rb = (float)a * 2.3283064365386963e-10f;          // 2^-32
+        const float rc = rb + 0.25f;                                  // cos x = sin(x + 1/4 turn)
         const float ff = freq_f[pi];
 #pragma unroll
-        for (int hf = 0; hf < 2; ++hf) {
-          const float rho = fmaf(ff, (float)(16 * hf + n), rb);
-          tr[hf][2 * e] = __builtin_amdgcn_sinf(rho + 0.25f);
-          tr[hf][2 * e + 1] = __builtin_amdgcn_sinf(rho);
+        for (int hf = 0; hf < HF; ++hf) {
+          const float dr = (float)(16 * hf + n);
+          tr[hf][2 * e] = __builtin_amdgcn_sinf(fmaf(ff, dr, rc));
+          tr[hf][2 * e + 1] = __builtin_amdgcn_sinf(fmaf(ff, dr, rb));
         }
       }
     };
@@ -213,22 +231,32 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
     // matrix cores run one step's products, the LDS reads of the next
     // step's W piece and the cos/sin weighting of the previous step's
     // product issue (the order is pinned by scheduling barriers; left to
-    // itself the compiler serialised read, products and weighting).
+    // itself the compiler serialised read, products and weighting).  The
+    // cos / sin of a column block are computed at its first step, after
+    // the previous block's last weighting, into the same registers.
     constexpr int NIT = NBC * HPG;
     bf16x8 wa[2][NC];
-    f32x4 gt[2][2];
-    float tr[2][2][4];
+    f32x4 gt[2][HF];
+    float tr[HF][4];
     auto load_w = [&](int it, bf16x8 (&dst)[NC]) {
       const int nb = it / HPG, hl = it % HPG;
 #pragma unroll
       for (int c = 0; c < NC; ++c) dst[c] = as_bf16x8(wl[((hl * NC + c) * NBC + nb) * 64 + lane]);
     };
-    auto weight = [&](int it, const f32x4 (&g)[2], const float (&tw)[2][4]) {
+    auto weight = [&](int it, const f32x4 (&g)[HF]) {
       const int hl = it % HPG;
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf)
+      for (int hf = 0; hf < HF; ++hf)
 #pragma unroll
-        for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(g[hf][jj], tw[hf][jj], sp[hl][hf]);
+        for (int jj = 0; jj < 4; ++jj) sp[hl][hf] = fmaf(g[hf][jj], tr[hf][jj], sp[hl][hf]);
+    };
+    auto products = [&](const bf16x8 (&wp)[NC], f32x4 (&g)[HF]) {
+#pragma unroll
+      for (int hf = 0; hf < HF; ++hf) g[hf] = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int hf = 0; hf < HF; ++hf) g[hf] = mfma16(wp[c], t.v[hf][c], g[hf]);
     };
     // (eight heads of 128-wide values leave no registers for the second
     // set of operands: those steps run in order)
@@ -236,60 +264,55 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
     if constexpr (!PIPE) {
 #pragma unroll
       for (int it = 0; it < NIT; ++it) {
-        if (it % HPG == 0) trig(it / HPG, tr[0]);
+        if (it % HPG == 0) trig(it / HPG, tr);
         load_w(it, wa[0]);
-        gt[0][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-        gt[0][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-        for (int c = 0; c < NC; ++c)
-#pragma unroll
-          for (int hf = 0; hf < 2; ++hf) gt[0][hf] = mfma16(wa[0][c], t.v[hf][c], gt[0][hf]);
-        weight(it, gt[0], tr[0]);
+        products(wa[0], gt[0]);
+        weight(it, gt[0]);
       }
     } else {
-    load_w(0, wa[0]);
-    trig(0, tr[0]);
+      load_w(0, wa[0]);
+      trig(0, tr);
 #pragma unroll
-    for (int it = 0; it < NIT; ++it) {
-      const int cur = it & 1;
-      gt[cur][0] = f32x4{0.f, 0.f, 0.f, 0.f};
-      gt[cur][1] = f32x4{0.f, 0.f, 0.f, 0.f};
-#pragma unroll
-      for (int c = 0; c < NC; ++c)
-#pragma unroll
-        for (int hf = 0; hf < 2; ++hf) gt[cur][hf] = mfma16(wa[cur][c], t.v[hf][c], gt[cur][hf]);
-      __builtin_amdgcn_sched_barrier(0);
-      if (it + 1 < NIT) load_w(it + 1, wa[cur ^ 1]);
-      if (it > 0) weight(it - 1, gt[cur ^ 1], tr[((it - 1) / HPG) & 1]);
-      if ((it + 1) % HPG == 0 && it + 1 < NIT) trig((it + 1) / HPG, tr[((it + 1) / HPG) & 1]);
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    weight(NIT - 1, gt[(NIT - 1) & 1], tr[((NIT - 1) / HPG) & 1]);
+      for (int it = 0; it < NIT; ++it) {
+        const int cur = it & 1;
+        products(wa[cur], gt[cur]);
+        __builtin_amdgcn_sched_barrier(0);
+        if (it + 1 < NIT) load_w(it + 1, wa[cur ^ 1]);
+        if (it > 0) weight(it - 1, gt[cur ^ 1]);
+        if (it > 0 && it % HPG == 0) trig(it / HPG, tr);
+        __builtin_amdgcn_sched_barrier(0);
+      }
+      weight(NIT - 1, gt[(NIT - 1) & 1]);
     }
     // sum over the four 16-lane rows, then transpose through LDS: lane
-    // (n, qd) takes head col_head's rows 16 hf + 4 qd + jj
+    // (n, qd) takes head col_head's rows 32 rh + 16 k' + 4 qd + jj
 #pragma unroll
     for (int hl = 0; hl < HPG; ++hl)
 #pragma unroll
-      for (int hf = 0; hf < 2; ++hf) xs[hl * kTileRows + 16 * hf + n] = sum_over_rows(sp[hl][hf]);
-    float x[8];
-    {
-      const f32x4 lo = *reinterpret_cast<const f32x4*>(xs + col_head * kTileRows + 4 * qd);
-      const f32x4 hi = *reinterpret_cast<const f32x4*>(xs + col_head * kTileRows + 16 + 4 * qd);
+      for (int hf = 0; hf < HF; ++hf) xs[hl * TR + 16 * hf + n] = sum_over_rows(sp[hl][hf]);
+    float x[RH][8];
+#pragma unroll
+    for (int rh = 0; rh < RH; ++rh) {
+      const f32x4 lo = *reinterpret_cast<const f32x4*>(xs + col_head * TR + 32 * rh + 4 * qd);
+      const f32x4 hi = *reinterpret_cast<const f32x4*>(xs + col_head * TR + 32 * rh + 16 + 4 * qd);
 #pragma unroll
       for (int jj = 0; jj < 4; ++jj) {
-        x[jj] = lo[jj];
-        x[4 + jj] = hi[jj];
+        x[rh][jj] = lo[jj];
+        x[rh][4 + jj] = hi[jj];
       }
     }
-    if (row0 + kTileRows > row_end) {
+    if (row0 + TR > row_end) {
 #pragma unroll
-      for (int k = 0; k < 8; ++k)
-        if (row0 + 16 * (k >> 2) + 4 * qd + (k & 3) >= row_end) x[k] = -INFINITY;
+      for (int rh = 0; rh < RH; ++rh)
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+          if (row0 + 32 * rh + 16 * (k >> 2) + 4 * qd + (k & 3) >= row_end) x[rh][k] = -INFINITY;
     }
-    float mt = x[0];
+    float mt = x[0][0];
 #pragma unroll
-    for (int k = 1; k < 8; ++k) mt = fmaxf(mt, x[k]);
+    for (int rh = 0; rh < RH; ++rh)
+#pragma unroll
+      for (int k = 0; k < 8; ++k) mt = fmaxf(mt, x[rh][k]);
     mt = max_over_rows(mt);
     const float m_new = fmaxf(m_run, mt);
     if (__ballot(m_new > m_run) != 0) {
@@ -299,41 +322,53 @@ __global__ void __launch_bounds__(kRopeThreads, 1) rope_decode_kernel(RopeDecode
       for (int ib = 0; ib < NB; ++ib) acc[ib] *= alpha;
       m_run = m_new;
     }
-    float pr[8];
     float psum = 0.f;
+    bf16x8 bp[RH];
 #pragma unroll
-    for (int k = 0; k < 8; ++k) {
-      pr[k] = __builtin_amdgcn_exp2f(x[k] - m_run);
-      psum += pr[k];
+    for (int rh = 0; rh < RH; ++rh) {
+      float pr[8];
+#pragma unroll
+      for (int k = 0; k < 8; ++k) {
+        pr[k] = __builtin_amdgcn_exp2f(x[rh][k] - m_run);
+        psum += pr[k];
+      }
+      bp[rh] = active ? split_hi_lo(pr, is_lo) : zero8;
     }
     l_run += psum;
-    const bf16x8 bp = active ? split_hi_lo(pr, is_lo) : zero8;
 #pragma unroll
-    for (int c = 0; c < NC; ++c)
+    for (int rh = 0; rh < RH; ++rh) {
 #pragma unroll
-      for (int half = 0; half < 2; ++half) {
-        const f32x4 z = {0.f, 0.f, 0.f, 0.f};
-        const f32x4 t0 = mfma16(t.v[0][c], esel[half], z);
-        const f32x4 t1 = mfma16(t.v[1][c], esel[half], z);
-        bf16x8 av;
-        const bf16x2 a01 = __builtin_convertvector((f32x2{t0[0], t0[1]}), bf16x2);
-        const bf16x2 a23 = __builtin_convertvector((f32x2{t0[2], t0[3]}), bf16x2);
-        const bf16x2 a45 = __builtin_convertvector((f32x2{t1[0], t1[1]}), bf16x2);
-        const bf16x2 a67 = __builtin_convertvector((f32x2{t1[2], t1[3]}), bf16x2);
-        av[0] = a01[0]; av[1] = a01[1]; av[2] = a23[0]; av[3] = a23[1];
-        av[4] = a45[0]; av[5] = a45[1]; av[6] = a67[0]; av[7] = a67[1];
-        acc[2 * c + half] = mfma16(av, bp, acc[2 * c + half]);
-      }
+      for (int c = 0; c < NC; ++c)
+#pragma unroll
+        for (int half = 0; half < 2; ++half) {
+          const f32x4 z = {0.f, 0.f, 0.f, 0.f};
+          const f32x4 t0 = mfma16(t.v[2 * rh][c], esel[half], z);
+          const f32x4 t1 = mfma16(t.v[2 * rh + 1][c], esel[half], z);
+          bf16x8 av;
+          const bf16x2 a01 = __builtin_convertvector((f32x2{t0[0], t0[1]}), bf16x2);
+          const bf16x2 a23 = __builtin_convertvector((f32x2{t0[2], t0[3]}), bf16x2);
+          const bf16x2 a45 = __builtin_convertvector((f32x2{t1[0], t1[1]}), bf16x2);
+          const bf16x2 a67 = __builtin_convertvector((f32x2{t1[2], t1[3]}), bf16x2);
+          av[0] = a01[0]; av[1] = a01[1]; av[2] = a23[0]; av[3] = a23[1];
+          av[4] = a45[0]; av[5] = a45[1]; av[6] = a67[0]; av[7] = a67[1];
+          acc[2 * c + half] = mfma16(av, bp[rh], acc[2 * c + half]);
+        }
+      if constexpr (DEPTH == 1) load_blocks(t, next_row, 2 * rh, 2 * rh + 2);
+    }
   };
 
-  for (int jt = 0; jt < my_tiles; jt += DEPTH) {
+  if constexpr (DEPTH == 1) {
+    for (int j = 0; j < my_tiles; ++j) compute_tile(buf[0], tile_row(j), r1, tile_row(j + 1));
+  } else {
+    for (int jt = 0; jt < my_tiles; jt += DEPTH) {
 #pragma unroll
-    for (int d = 0; d < DEPTH; ++d) {
-      const int j = jt + d;
-      if (j >= my_tiles) break;
-      load_tile(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1));
-      __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], tile_row(j), r1);
+      for (int d = 0; d < DEPTH; ++d) {
+        const int j = jt + d;
+        if (j >= my_tiles) break;
+        load_blocks(buf[(d + DEPTH - 1) % DEPTH], tile_row(j + DEPTH - 1), 0, HF);
+        __builtin_amdgcn_sched_barrier(0);
+        compute_tile(buf[d], tile_row(j), r1, 0);
+      }
     }
   }
 
