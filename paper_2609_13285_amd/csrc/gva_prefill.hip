@@ -500,6 +500,7 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
   };
   TileT buf[DEPTH];
   load_tile(buf[0], 0);
+  load_tile(buf[1], kTileRows);
   __builtin_amdgcn_sched_barrier(0);
 
   // ---- this wave's queries as bf16 high + low B operands (zero for columns
@@ -569,7 +570,8 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
   }
 
   f16x8 bp_prev[CB];                           // the previous tile's weights (pipelined P.V)
-  auto compute_tile = [&](TileT& t, int row0, int vbuf, bool has_prev) {
+  // next_row: the tile requested into t's registers once its scores are issued
+  auto compute_tile = [&](TileT& t, int row0, int vbuf, bool has_prev, int next_row) {
     if (row0 + kTileRows > kend) {             // rows past the block's keys: zero
 #pragma unroll
       for (int hf = 0; hf < 2; ++hf) {
@@ -662,6 +664,7 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
       f32x4 sc[CB][2];
 #pragma unroll
       for (int cb = 0; cb < kAhead; ++cb) scores(cb, sc[cb]);
+      if constexpr (kAhead == CB) load_tile(t, next_row);
       __builtin_amdgcn_sched_barrier(0);
       if (has_prev) {
         const f16x8* vtp = vt_lds + (vbuf ^ 1) * (NB * 64);
@@ -681,6 +684,7 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
         }
         bp_prev[cb] = softmax(cb, sc[cb]);
       }
+      if constexpr (kAhead < CB) load_tile(t, next_row);
       __syncthreads();                         // every wave's V^T blocks of this tile are in LDS
     } else {
       f16x8 bp[CB];
@@ -693,6 +697,7 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
         bp[cb] = softmax(cb, sc[cb & 1]);
         __builtin_amdgcn_sched_barrier(0);
       }
+      load_tile(t, next_row);
       __syncthreads();                         // every wave's V^T blocks of this tile are in LDS
 #pragma unroll
       for (int k = 0; k < NB; ++k) {
@@ -704,8 +709,8 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
   };
 
   // Every wave runs every tile (the barrier inside compute_tile is reached
-  // the same number of times by all four); the tile after the current one
-  // is requested before it is used.
+  // the same number of times by all four); tile j + 2 is requested into
+  // tile j's registers as soon as tile j's scores no longer need them.
   // (requests past the block's rows read zeros through the descriptors and
   // cost no traffic, so they are unconditional and the waits exact)
   for (int jt = 0; jt < ntiles; jt += DEPTH) {
@@ -713,9 +718,7 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
     for (int d = 0; d < DEPTH; ++d) {
       const int j = jt + d;
       if (j >= ntiles) break;
-      load_tile(buf[(d + 1) % DEPTH], (j + 1) * kTileRows);
-      __builtin_amdgcn_sched_barrier(0);
-      compute_tile(buf[d], j * kTileRows, d, j > 0);
+      compute_tile(buf[d], j * kTileRows, d, j > 0, (j + DEPTH) * kTileRows);
     }
   }
   if (kPipe && ntiles > 0) {                   // P.V of the last tile
