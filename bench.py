@@ -39,6 +39,7 @@ from paper_2609_13285_amd import gva, traffic  # noqa: E402
 METRIC = "decode attention GB/s (fraction of HBM peak) and tokens/s"
 HBM_PEAK_GBS = 8000.0          # MI355X HBM3E, AMD's published figure
 MFMA_BF16_PEAK_TFLOPS = 2500.0  # MI355X dense bf16 matrix peak, AMD's published figure
+SIDE_WARM_S = 0.5          # minimum untimed warm-up of each side comparison, seconds
 # the decode kernel's sources (the traffic record is valid only for these)
 KERNEL_SRCS = [os.path.join(ROOT, "paper_2609_13285_amd", "csrc", f)
                for f in ("gva_common.h", "gva_decode.hip")]
@@ -190,6 +191,23 @@ def cpu_baseline(w, inp, seq, pos, budget_s: float = 20.0, min_s: float = 10.0):
 MALL_BYTES = 256 << 20
 
 
+def warm(fns, calls: int, seconds: float) -> None:
+    """Untimed calls of each of fns in turn: at least ``calls`` each, and
+    until ``seconds`` of wall time have passed.  The side comparisons use it
+    so that their kernels are timed past the device's power-management ramp
+    in a fresh process (an MFMA-bound launch runs up to ~25% slower for its
+    first tens of milliseconds), whatever --warmup the headline step uses."""
+    t0 = time.perf_counter()
+    i = 0
+    while i < calls or time.perf_counter() - t0 < seconds:
+        for f in fns:
+            f(i)
+        i += 1
+        if i % 8 == 0:
+            torch.cuda.synchronize()
+    torch.cuda.synchronize()
+
+
 def timed(step, steps: int, stream) -> float:
     """Mean ms per step over ``steps`` calls of step(i), bracketed by events
     on ``stream`` with no events inside."""
@@ -304,9 +322,7 @@ def gqa_comparison(args, w, inp, d, S, split_rows, fused, dev, caches, stream):
     def gqa_attn(i):
         gqa_fns[i % n]()
 
-    for i in range(args.warmup):
-        gva_attn(i)
-        gqa_attn(i)
+    warm([gva_attn, gqa_attn], args.warmup, SIDE_WARM_S)
     t_gva = timed(gva_attn, args.steps, stream)
     t_gqa = timed(gqa_attn, args.steps, stream)
     elem = 2
@@ -376,9 +392,7 @@ def rope_comparison(args, w, inp, S, split_rows, dev, caches, stream):
         return {"skipped": f"gva_rope_decode_attention: {gva.status_string(e.status)} at H/G = "
                            f"{w.heads_per_group}, d_v = {w.d_v}, d_c = {w.d_c} (the W_h of a group's "
                            f"heads, {w.heads_per_group * w.d_v * w.d_c * 2} bytes, exceed one workgroup's LDS)"}
-    for i in range(args.warmup):
-        absorbed(i)
-        rope(i)
+    warm([absorbed, rope], args.warmup, SIDE_WARM_S)
     t_abs = timed(absorbed, args.steps, stream)
     t_rope = timed(rope, args.steps, stream)
     # the contrast kernel alone, its launches back to back
@@ -443,10 +457,7 @@ def prefill_comparison(args, w, caches, dev, stream):
         gva.gva_gqa_prefill_attention(d1, N, qg, kg, v1, lens1, o, lse, stream)
 
     steps = max(5, args.steps // 10)
-    for i in range(2):
-        absorb(i)
-        attend(i)
-        gqa(i)
+    warm([absorb, attend, gqa], 2, SIDE_WARM_S)
     t_abs = timed(absorb, steps, stream)
     t_att = timed(attend, steps, stream)
     t_gqa = timed(gqa, steps, stream)
