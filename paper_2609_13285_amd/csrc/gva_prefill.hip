@@ -390,7 +390,7 @@ __global__ void __launch_bounds__(kThreads, prefill_min_blocks(NRC)) prefill_bf1
       mx = -INFINITY;
     }
     const int64_t orow = ((int64_t)b * p.N + qi) * p.H + h0 + col % HPG;
-    p.o[orow * DV + i] = o;
+    __builtin_nontemporal_store(o, p.o + orow * DV + i);   // written once: kept out of the L2
     if (i == 0) p.lse[orow] = mx == -INFINITY ? -INFINITY : (mx + log2f(lsum)) * kLn2;
   }
 }
@@ -744,7 +744,9 @@ __global__ void __launch_bounds__(kThreads, 2) prefill_vt_kernel(PrefillParams p
 #pragma unroll
     for (int ib = 0; ib < NB; ++ib) {
       f32x4 o = acc[cb][ib] * inv;
-      *reinterpret_cast<f32x4*>(p.o + orow * DV + 16 * ib + 4 * qd) = o;
+      // written once and not read again here: kept out of the L2, which holds
+      // the group's key and value rows
+      __builtin_nontemporal_store(o, reinterpret_cast<f32x4*>(p.o + orow * DV + 16 * ib + 4 * qd));
     }
     if (qd == 0) p.lse[orow] = seen ? (m_run[cb] + log2f(l)) * kLn2 : -INFINITY;
   }
