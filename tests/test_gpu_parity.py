@@ -1144,10 +1144,11 @@ def _prefill_check(o, lse, o_ref, lse_ref, label):
     assert lerr <= 1e-2, (label, lerr)
 
 
-@pytest.mark.parametrize("B,N,dr", [(3, 90, 16), (3, 1500, 64)])
+@pytest.mark.parametrize("B,N,dr", [(3, 90, 16), (3, 400, 32), (3, 1500, 64)])
 def test_prefill_absorb_matches_oracle(B, N, dr):
     # every prompt row absorbed and rotated at its own position L-N+i
-    # (4500 rows: the 64-rows-per-workgroup form with a ragged last block)
+    # (1200 rows: 32 rows per workgroup; 4500 rows: 64 per workgroup, each
+    # with a ragged last block)
     w = gva_inputs.Workload("prefill", B, 2048, 8, 2, 128, 96, dr, dtype="bf16")
     lens = torch.tensor([2048, 1600, N], dtype=torch.int32)
     inp = gva_inputs.make_inputs(w, 41, lens=lens)
