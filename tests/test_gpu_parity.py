@@ -1052,8 +1052,8 @@ def _rope_workload(hpg, dv, dc, T, B, G=2):
     return gva_inputs.Workload("rope", B, T, G * hpg, G, dv, dc, 0, dtype="bf16")
 
 
-@pytest.mark.parametrize("hpg,dv,dc", [(1, 64, 64), (2, 128, 64), (4, 64, 128), (4, 128, 128),
-                                       (8, 64, 64), (8, 64, 128)])
+@pytest.mark.parametrize("hpg,dv,dc", [(1, 64, 64), (1, 128, 128), (2, 128, 64), (4, 64, 128),
+                                       (4, 128, 128), (8, 64, 64), (8, 64, 128), (8, 128, 64)])
 def test_rope_decode_matches_oracle(hpg, dv, dc):
     w = _rope_workload(hpg, dv, dc, 304, 5)
     lens = torch.tensor([304, 0, 1, 45, 263], dtype=torch.int32)
